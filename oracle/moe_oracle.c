@@ -1,0 +1,421 @@
+/*
+ * moe_oracle.c -- plain fp64 CPU oracle of one routed-expert MoE layer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or
+ * calls this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline leg do.  It shares no code with the HIP library.
+ *
+ * What it computes (one layer, per token t):
+ *   1. router logits  l_e = sum_i x[t,i] * Wr[e,i] + b[e]            (fp64)
+ *   2. selection S_t  = first K experts ordered by (l_e desc, e asc)
+ *   3. gate weights   w_e = exp(l_e - m) / sum_{j in S_t} exp(l_j - m),
+ *                     m = max_{e in S_t} l_e  (softmax restricted to S_t,
+ *                     equal to a full softmax renormalised over S_t)
+ *   4. expert FFN     y = Wd (silu(Wg x) * (Wu x)),  silu(z) = z/(1+e^-z)
+ *   5. combine        out_t = y_shared + sum_{e in S_t, ascending e} w_e y_e
+ * plus the token-by-expert permutation (a stable counting sort of the T*K
+ * assignments by (expert, token)).
+ *
+ * The paper runs the stock router and "the complete gate, up, and down
+ * projections" of every selected expert (Section 5.4, principal experiment);
+ * it does not print the MoE formulas.  Steps 1-5 are the standard
+ * softmax/top-k gated-SiLU MoE with an always-on shared expert; the readings
+ * taken where the paper is silent (softmax then renormalise, ungated shared
+ * expert, bias added before selection, lower id wins ties, fp32/bf16/int4
+ * storage upcast exactly) are listed in the design notes.
+ *
+ * Inputs are read in their stored formats and upcast exactly to double:
+ *   dtype 0 f32, 1 bf16 (uint16 = top half of binary32), 2 q4b32 (nibbles
+ *   [rows, cols/2], low nibble = even column, 4-bit two's complement, then
+ *   fp16 scales [rows, cols/32]; value = scale * q).
+ * An expert object is [Wg (I x d) | Wu (I x d) | Wd (d x I)], row-major.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#ifndef MSIO_MUTANT
+#define MSIO_MUTANT 0 /* tests plant single mistakes with -DMSIO_MUTANT=n */
+#endif
+
+enum { MSIO_F32 = 0, MSIO_BF16 = 1, MSIO_Q4B32 = 2 };
+
+/* ---- exact upcasts of the stored formats ------------------------------- */
+
+double msio_bf16_to_f64(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+double msio_fp16_to_f64(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int ex = (h >> 10) & 0x1F;
+    int man = h & 0x3FF;
+    double v;
+    if (ex == 0)
+        v = ldexp((double)man, -24);                 /* zero / subnormal */
+    else if (ex == 31)
+        v = man ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + man), ex - 25);     /* (1.man) * 2^(ex-15) */
+    return sign ? -v : v;
+}
+
+/* round-to-nearest-even double -> bf16 (used only by the layer stack) */
+uint16_t msio_f64_to_bf16(double v)
+{
+    if (v != v)
+        return 0x7FC0;
+    int sign = signbit(v) ? 1 : 0;
+    double a = fabs(v);
+    uint16_t s = (uint16_t)(sign << 15);
+    if (a == 0.0)
+        return s;
+    if (a >= ldexp(255.0 / 128.0 + 1.0 / 256.0, 127))   /* rounds past max */
+        return s | 0x7F80;
+    int e;
+    frexp(a, &e);                     /* a = f * 2^e, f in [0.5, 1) */
+    int ex = e - 1;                   /* a = 1.m * 2^ex               */
+    if (ex < -126)
+        ex = -126;                    /* subnormal range: fixed quantum */
+    double q = ldexp(1.0, ex - 7);    /* spacing of bf16 values here   */
+    double n = a / q;                 /* exact: power-of-two scaling   */
+    double fl = floor(n);
+    double r = n - fl;
+    if (r > 0.5 || (r == 0.5 && fmod(fl, 2.0) != 0.0))
+        fl += 1.0;
+    double rv = fl * q;
+    float f = (float)rv;              /* exactly representable */
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    return s | (uint16_t)(u >> 16);
+}
+
+size_t msio_matrix_nbytes(int dtype, int64_t rows, int64_t cols)
+{
+    switch (dtype) {
+    case MSIO_F32: return (size_t)(rows * cols * 4);
+    case MSIO_BF16: return (size_t)(rows * cols * 2);
+    default: return (size_t)(rows * cols / 2 + rows * (cols / 32) * 2);
+    }
+}
+
+typedef struct {
+    int dtype;
+    const uint8_t *base;
+    int64_t rows, cols;
+} wmat;
+
+static inline double wmat_at(const wmat *m, int64_t r, int64_t c)
+{
+    switch (m->dtype) {
+    case MSIO_F32: {
+        float f;
+        memcpy(&f, m->base + 4 * (r * m->cols + c), 4);
+        return (double)f;
+    }
+    case MSIO_BF16: {
+        uint16_t b;
+        memcpy(&b, m->base + 2 * (r * m->cols + c), 2);
+        return msio_bf16_to_f64(b);
+    }
+    default: {
+        uint8_t byte = m->base[r * (m->cols / 2) + c / 2];
+#if MSIO_MUTANT == 8
+        int q = (c & 1) ? (byte & 0x0F) : (byte >> 4);   /* nibble order swapped */
+#else
+        int q = (c & 1) ? (byte >> 4) : (byte & 0x0F);
+#endif
+        if (q >= 8)
+            q -= 16;
+        uint16_t s;
+        memcpy(&s, m->base + (size_t)(m->rows * m->cols / 2) + 2 * (r * (m->cols / 32) + c / 32), 2);
+        return msio_fp16_to_f64(s) * (double)q;
+    }
+    }
+}
+
+/* q4b32 dequantisation of a whole matrix (for pins and the numpy cross-check) */
+void msio_dequant(int dtype, int64_t rows, int64_t cols, const void *src, double *dst)
+{
+    wmat m = {dtype, (const uint8_t *)src, rows, cols};
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t c = 0; c < cols; ++c)
+            dst[r * cols + c] = wmat_at(&m, r, c);
+}
+
+/* ---- step 1: router logits ---------------------------------------------- */
+
+static void logits_one(int64_t d, int64_t E, const wmat *x, int64_t t, const wmat *wr,
+                       const float *bias, double *L)
+{
+    for (int64_t e = 0; e < E; ++e) {
+        double acc = 0.0;
+        for (int64_t i = 0; i < d; ++i)
+            acc += wmat_at(x, t, i) * wmat_at(wr, e, i);
+#if MSIO_MUTANT == 1
+        (void)bias;                                   /* bias dropped */
+#else
+        if (bias)
+            acc += (double)bias[e];
+#endif
+        L[e] = acc;
+    }
+}
+
+void msio_router_logits(int64_t T, int64_t d, int64_t E, int xdtype, const void *x,
+                        const void *wr, const float *bias, double *L)
+{
+    wmat X = {xdtype, (const uint8_t *)x, T, d};
+    wmat W = {xdtype, (const uint8_t *)wr, E, d};
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < T; ++t)
+        logits_one(d, E, &X, t, &W, bias, L + t * E);
+}
+
+/* ---- step 2: top-K selection, ties to the lower expert id ----------------- */
+
+typedef struct {
+    double v;
+    int32_t id;
+} vid;
+
+static int cmp_rank(const void *a, const void *b)
+{
+    const vid *p = (const vid *)a, *q = (const vid *)b;
+    if (p->v > q->v) return -1;
+    if (p->v < q->v) return 1;
+#if MSIO_MUTANT == 2
+    return (p->id < q->id) ? 1 : (p->id > q->id) ? -1 : 0;  /* higher id wins */
+#else
+    return (p->id < q->id) ? -1 : (p->id > q->id) ? 1 : 0;
+#endif
+}
+
+static int cmp_i32(const void *a, const void *b)
+{
+    int32_t p = *(const int32_t *)a, q = *(const int32_t *)b;
+    return (p > q) - (p < q);
+}
+
+/* idx: K ids of S_t in ascending order.  gap: l_(K) - l_(K+1) (+inf if K == E). */
+static void select_one(int64_t E, int64_t K, const double *L, int32_t *idx, double *gap, vid *tmp)
+{
+    for (int64_t e = 0; e < E; ++e) {
+        tmp[e].v = L[e];
+        tmp[e].id = (int32_t)e;
+    }
+    qsort(tmp, (size_t)E, sizeof(vid), cmp_rank);
+    for (int64_t k = 0; k < K; ++k)
+        idx[k] = tmp[k].id;
+    qsort(idx, (size_t)K, sizeof(int32_t), cmp_i32);
+    if (gap)
+        *gap = (K < E) ? tmp[K - 1].v - tmp[K].v : INFINITY;
+}
+
+void msio_select_topk(int64_t T, int64_t E, int64_t K, const double *L, int32_t *idx, double *gap)
+{
+#pragma omp parallel
+    {
+        vid *tmp = (vid *)malloc(sizeof(vid) * (size_t)E);
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < T; ++t)
+            select_one(E, K, L + t * E, idx + t * K, gap ? gap + t : NULL, tmp);
+        free(tmp);
+    }
+}
+
+/* ---- step 3: softmax restricted to the selected set ----------------------- */
+
+static void weights_one(int64_t E, int64_t K, const double *L, const int32_t *idx, double *w)
+{
+#if MSIO_MUTANT == 3
+    /* full softmax over all E, not renormalised over S_t */
+    double m = L[0];
+    for (int64_t e = 1; e < E; ++e) m = fmax(m, L[e]);
+    double s = 0.0;
+    for (int64_t e = 0; e < E; ++e) s += exp(L[e] - m);
+    for (int64_t k = 0; k < K; ++k) w[k] = exp(L[idx[k]] - m) / s;
+#else
+    (void)E;
+    double m = L[idx[0]];
+    for (int64_t k = 1; k < K; ++k)
+        m = fmax(m, L[idx[k]]);
+    double s = 0.0;
+    for (int64_t k = 0; k < K; ++k)
+        s += exp(L[idx[k]] - m);
+    for (int64_t k = 0; k < K; ++k)
+        w[k] = exp(L[idx[k]] - m) / s;
+#endif
+}
+
+void msio_gate_weights(int64_t T, int64_t E, int64_t K, const double *L, const int32_t *idx, double *w)
+{
+    for (int64_t t = 0; t < T; ++t)
+        weights_one(E, K, L + t * E, idx + t * K, w + t * K);
+}
+
+/* ---- token-by-expert permutation: stable counting sort by (expert, token) -- */
+
+void msio_permute(int64_t T, int64_t E, int64_t K, const int32_t *idx, int32_t *counts,
+                  int32_t *offsets, int32_t *perm, int32_t *inv)
+{
+    for (int64_t e = 0; e < E; ++e)
+        counts[e] = 0;
+    for (int64_t a = 0; a < T * K; ++a)
+        counts[idx[a]]++;
+    offsets[0] = 0;
+    for (int64_t e = 0; e < E; ++e)
+        offsets[e + 1] = offsets[e] + counts[e];
+    int32_t *cursor = (int32_t *)malloc(sizeof(int32_t) * (size_t)E);
+    memcpy(cursor, offsets, sizeof(int32_t) * (size_t)E);
+#if MSIO_MUTANT == 9
+    for (int64_t t = T - 1; t >= 0; --t)              /* tokens in reverse: unstable */
+#else
+    for (int64_t t = 0; t < T; ++t)
+#endif
+        for (int64_t k = 0; k < K; ++k) {
+            int32_t e = idx[t * K + k];
+            int32_t row = cursor[e]++;
+            perm[row] = (int32_t)t;
+            inv[t * K + k] = row;
+        }
+    free(cursor);
+}
+
+/* ---- step 4: one expert's gated-SiLU FFN on one token --------------------- */
+
+static inline double silu(double z)
+{
+#if MSIO_MUTANT == 4
+    return z / (1.0 + exp(z));                        /* sign flipped */
+#else
+    return z / (1.0 + exp(-z));
+#endif
+}
+
+void msio_expert_ffn(int64_t d, int64_t I, int wdtype, const void *obj, const double *x,
+                     double *y, double *act /* [I] scratch, may be NULL */)
+{
+    const uint8_t *b = (const uint8_t *)obj;
+    size_t nb = msio_matrix_nbytes(wdtype, I, d);
+    wmat Wg = {wdtype, b, I, d};
+    wmat Wu = {wdtype, b + nb, I, d};
+    wmat Wd = {wdtype, b + 2 * nb, d, I};
+#if MSIO_MUTANT == 5
+    Wg.base = Wu.base;                                /* gate reads the up matrix */
+#endif
+    double *a = act ? act : (double *)malloc(sizeof(double) * (size_t)I);
+    for (int64_t i = 0; i < I; ++i) {
+        double g = 0.0, u = 0.0;
+        for (int64_t k = 0; k < d; ++k) {
+            g += wmat_at(&Wg, i, k) * x[k];
+            u += wmat_at(&Wu, i, k) * x[k];
+        }
+        a[i] = silu(g) * u;
+    }
+    for (int64_t j = 0; j < d; ++j) {
+        double acc = 0.0;
+        for (int64_t i = 0; i < I; ++i)
+            acc += wmat_at(&Wd, j, i) * a[i];
+        y[j] = acc;
+    }
+    if (!act)
+        free(a);
+}
+
+/* ---- steps 1-5 for a list of tokens --------------------------------------- */
+/*
+ * tokens:     n_sel token ids to evaluate (NULL = 0..n_sel-1)
+ * forced_idx: [n_sel, K] ascending expert sets to use instead of step 2 (or
+ *             NULL); weights are then the restricted softmax over that set
+ * experts:    E host pointers to expert objects; shared: object or NULL
+ * out [n_sel, d]; idx_out [n_sel, K]; w_out [n_sel, K]; gap_out [n_sel];
+ * logits_out [n_sel, E] -- each output pointer may be NULL except out.
+ */
+void msio_moe_layer(int64_t T, int64_t d, int64_t E, int64_t K, int64_t I, int wdtype, int xdtype,
+                    const void *x, const void *wr, const float *bias,
+                    const void *const *experts, const void *shared,
+                    int64_t n_sel, const int64_t *tokens, const int32_t *forced_idx,
+                    double *out, int32_t *idx_out, double *w_out, double *gap_out,
+                    double *logits_out)
+{
+    wmat X = {xdtype, (const uint8_t *)x, T, d};
+    wmat W = {xdtype, (const uint8_t *)wr, E, d};
+#pragma omp parallel
+    {
+        double *L = (double *)malloc(sizeof(double) * (size_t)E);
+        vid *tmp = (vid *)malloc(sizeof(vid) * (size_t)E);
+        double *xt = (double *)malloc(sizeof(double) * (size_t)d);
+        double *y = (double *)malloc(sizeof(double) * (size_t)d);
+        double *act = (double *)malloc(sizeof(double) * (size_t)I);
+        int32_t idx[64];
+        double w[64];
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t s = 0; s < n_sel; ++s) {
+            int64_t t = tokens ? tokens[s] : s;
+            for (int64_t i = 0; i < d; ++i)
+                xt[i] = wmat_at(&X, t, i);
+            logits_one(d, E, &X, t, &W, bias, L);
+            double gap = NAN;
+            if (forced_idx)
+                memcpy(idx, forced_idx + s * K, sizeof(int32_t) * (size_t)K);
+            else
+                select_one(E, K, L, idx, &gap, tmp);
+            weights_one(E, K, L, idx, w);
+            double *o = out + s * d;
+            for (int64_t j = 0; j < d; ++j)
+                o[j] = 0.0;
+#if MSIO_MUTANT != 6
+            if (shared) {
+                msio_expert_ffn(d, I, wdtype, shared, xt, y, act);
+                for (int64_t j = 0; j < d; ++j)
+                    o[j] += y[j];
+            }
+#endif
+            for (int64_t k = 0; k < K; ++k) {              /* ascending expert id */
+                if (!experts[idx[k]]) {                    /* caller omitted this object */
+                    for (int64_t j = 0; j < d; ++j)
+                        o[j] = NAN;
+                    break;
+                }
+                msio_expert_ffn(d, I, wdtype, experts[idx[k]], xt, y, act);
+                for (int64_t j = 0; j < d; ++j)
+                    o[j] += w[k] * y[j];
+            }
+            if (idx_out)
+                memcpy(idx_out + s * K, idx, sizeof(int32_t) * (size_t)K);
+            if (w_out)
+                memcpy(w_out + s * K, w, sizeof(double) * (size_t)K);
+            if (gap_out)
+                gap_out[s] = gap;
+            if (logits_out)
+                memcpy(logits_out + s * E, L, sizeof(double) * (size_t)E);
+        }
+        free(L);
+        free(tmp);
+        free(xt);
+        free(y);
+        free(act);
+    }
+}
+
+int msio_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+int msio_mutant(void) { return MSIO_MUTANT; }

@@ -1,0 +1,264 @@
+"""Seeded synthetic inputs for the slot-backed MoE layer.
+
+This module is shared by the HIP path's tests/bench and by the CPU oracle's
+tests.  It holds none of the layer's arithmetic: it only draws random numbers
+and stores them in the byte formats the layer consumes (fp32, bf16, and a
+symmetric 4-bit block format).  Every draw comes from numpy's PCG64 seeded by a
+SeedSequence over (MASTER, workload, layer, kind, index, step), so any object
+can be regenerated alone.
+
+Byte formats (little endian):
+
+* ``f32``   -- IEEE binary32.
+* ``bf16``  -- the upper 16 bits of binary32 after round-to-nearest-even.
+* ``q4b32`` -- a matrix [rows, cols] is stored as nibbles [rows, cols/2]
+  (element 2j in the low nibble of byte j, 2j+1 in the high nibble, 4-bit
+  two's complement, range [-8, 7]) followed by fp16 scales [rows, cols/32]
+  (one per 32 consecutive elements of a row).  Value = scale * q.  The
+  quantizer below only builds test data: scale = fp16(amax / 7),
+  q = clamp(rint(w / scale), -8, 7), amax == 0 gives scale 0 and q 0.
+
+An expert object is the concatenation [Wg | Wu | Wd] with Wg, Wu of shape
+[I, d] (row-major, the reduction axis d contiguous) and Wd of shape [d, I]
+(reduction axis I contiguous).  The router weight is stored [E, d].
+
+Workload shapes follow the paper's model (48 MoE layers of 512 experts,
+Section 4 and Section 5.4); expert popularity priors (Dirichlet, Zipf) and
+the bias temperature are this build's recipe for "every expert receives
+tokens, with uneven counts".
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+MASTER = 20260821
+
+# kinds used in the seed tuple
+KIND_X = 0
+KIND_ROUTER = 1
+KIND_PRIOR = 2
+KIND_EXPERT = 3
+KIND_SHARED = 4
+KIND_PERM = 5
+
+WDTYPES = ("f32", "bf16", "q4b32")
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerShape:
+    """Shape of one routed-expert layer.  ``T`` tokens, hidden ``d``, ``E``
+    routed experts, top-``K``, expert intermediate ``I`` (shared expert uses
+    the same ``I``)."""
+
+    T: int
+    d: int
+    E: int
+    K: int
+    I: int
+    wdtype: str = "bf16"
+    shared: bool = True
+
+    def __post_init__(self):
+        assert self.wdtype in WDTYPES, self.wdtype
+        assert 1 <= self.K <= self.E
+
+    @property
+    def xdtype(self) -> str:
+        """Storage type of hidden states and router weight."""
+        return "f32" if self.wdtype == "f32" else "bf16"
+
+    def object_bytes(self) -> int:
+        return object_nbytes(self.d, self.I, self.wdtype)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One named synthetic workload."""
+
+    name: str
+    wid: int                      # workload id in the seed tuple
+    shape: LayerShape
+    prior: str = "none"           # none | dirichlet | zipf
+    prior_param: float = 0.0      # Dirichlet alpha or Zipf exponent
+    tau: float = 0.0              # bias = tau * ln(p)
+    n_layers: int = 1
+    capacity: int = 64            # slots per layer for the LRU arm
+
+
+WORKLOADS = {
+    "tiny_f32": Workload("tiny_f32", 1, LayerShape(64, 256, 16, 2, 128, "f32"),
+                         capacity=4),
+    "decode_bf16": Workload("decode_bf16", 2, LayerShape(16, 2048, 512, 10, 512, "bf16"),
+                            capacity=64),
+    "prefill_bf16": Workload("prefill_bf16", 3, LayerShape(32768, 2048, 512, 10, 512, "bf16"),
+                             prior="dirichlet", prior_param=0.3, tau=0.2, capacity=512),
+    "stack_bf16": Workload("stack_bf16", 4, LayerShape(4096, 2048, 512, 10, 512, "bf16"),
+                           prior="zipf", prior_param=1.1, tau=0.3, n_layers=48, capacity=64),
+    "prefill_q4": Workload("prefill_q4", 5, LayerShape(32768, 2048, 512, 10, 512, "q4b32"),
+                           prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
+    "decode_q4": Workload("decode_q4", 5, LayerShape(1, 2048, 512, 10, 512, "q4b32"),
+                          prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
+}
+
+
+def rng(wid: int, layer: int, kind: int, index: int = 0, step: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+        [MASTER, int(wid), int(layer), int(kind), int(index), int(step)])))
+
+
+# ----------------------------------------------------------------------------
+# storage conversions (data construction only)
+# ----------------------------------------------------------------------------
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round binary32 to bfloat16 (nearest, ties to even); finite input."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    assert np.all((u & 0x7F800000) != 0x7F800000), "non-finite input"
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def quantize_q4b32(w: np.ndarray) -> bytes:
+    """Quantize a float32 matrix [rows, cols] (cols % 32 == 0) to the q4b32
+    byte layout described in the module docstring."""
+    w = np.asarray(w, dtype=np.float32)
+    rows, cols = w.shape
+    assert cols % 32 == 0
+    blk = w.reshape(rows, cols // 32, 32)
+    amax = np.abs(blk).max(axis=2)
+    scale16 = (amax / np.float32(7.0)).astype(np.float16)
+    s32 = scale16.astype(np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        q = np.where(s32[:, :, None] > 0, np.rint(blk / s32[:, :, None]), 0.0)
+    q = np.clip(q, -8, 7).astype(np.int8).reshape(rows, cols)
+    nib = (q.astype(np.uint8) & np.uint8(0x0F))
+    packed = (nib[:, 0::2] | (nib[:, 1::2] << np.uint8(4))).astype(np.uint8)
+    return packed.tobytes() + scale16.view(np.uint16).tobytes()
+
+
+def q4b32_matrix_nbytes(rows: int, cols: int) -> int:
+    return rows * cols // 2 + rows * (cols // 32) * 2
+
+
+def object_nbytes(d: int, I: int, wdtype: str) -> int:
+    if wdtype == "f32":
+        return 3 * I * d * 4
+    if wdtype == "bf16":
+        return 3 * I * d * 2
+    return 2 * q4b32_matrix_nbytes(I, d) + q4b32_matrix_nbytes(d, I)
+
+
+def encode_matrix(w: np.ndarray, wdtype: str) -> bytes:
+    if wdtype == "f32":
+        return np.ascontiguousarray(w, dtype=np.float32).tobytes()
+    if wdtype == "bf16":
+        return f32_to_bf16_bits(w).tobytes()
+    return quantize_q4b32(w)
+
+
+def encode_dense(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Hidden states / router weight storage: f32 or bf16 (as uint16 bits)."""
+    if dtype == "f32":
+        return np.ascontiguousarray(a, dtype=np.float32)
+    return f32_to_bf16_bits(a)
+
+
+# ----------------------------------------------------------------------------
+# draws
+# ----------------------------------------------------------------------------
+
+def expert_object(wl: Workload, layer: int, expert: int, shared: bool = False) -> np.ndarray:
+    """One expert object [Wg | Wu | Wd] as a uint8 array.  ``shared`` selects
+    the layer's always-on shared expert (its own seed stream)."""
+    s = wl.shape
+    g = rng(wl.wid, layer, KIND_SHARED if shared else KIND_EXPERT, expert)
+    wg = g.standard_normal((s.I, s.d), dtype=np.float32) * np.float32(0.02)
+    wu = g.standard_normal((s.I, s.d), dtype=np.float32) * np.float32(0.02)
+    wd = g.standard_normal((s.d, s.I), dtype=np.float32) * np.float32(0.02)
+    b = encode_matrix(wg, s.wdtype) + encode_matrix(wu, s.wdtype) + encode_matrix(wd, s.wdtype)
+    out = np.frombuffer(b, dtype=np.uint8).copy()
+    assert out.nbytes == s.object_bytes()
+    return out
+
+
+def hidden_states(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] = None) -> np.ndarray:
+    """x [T, d]: float32 array (f32 workloads) or uint16 bf16 bits."""
+    s = wl.shape
+    T = s.T if T is None else T
+    g = rng(wl.wid, layer, KIND_X, 0, step)
+    return encode_dense(g.standard_normal((T, s.d), dtype=np.float32), s.xdtype)
+
+
+def router_weight(wl: Workload, layer: int = 0) -> np.ndarray:
+    """Wr stored [E, d]: float32 (f32 workloads) or uint16 bf16 bits."""
+    s = wl.shape
+    g = rng(wl.wid, layer, KIND_ROUTER)
+    return encode_dense(g.standard_normal((s.E, s.d), dtype=np.float32) * np.float32(0.02), s.xdtype)
+
+
+def popularity_prior(wl: Workload, layer: int = 0) -> Optional[np.ndarray]:
+    """Per-expert popularity p (sums to 1) or None for the unbiased workloads."""
+    E = wl.shape.E
+    if wl.prior == "none":
+        return None
+    g = rng(wl.wid, layer, KIND_PRIOR)
+    if wl.prior == "dirichlet":
+        p = g.dirichlet(np.full(E, wl.prior_param))
+    elif wl.prior == "zipf":
+        ranks = np.arange(1, E + 1, dtype=np.float64) ** (-wl.prior_param)
+        perm = rng(wl.wid, layer, KIND_PERM).permutation(E)
+        p = np.empty(E)
+        p[perm] = ranks / ranks.sum()
+    else:
+        raise ValueError(wl.prior)
+    return np.maximum(p, 1e-30)
+
+
+def router_bias(wl: Workload, layer: int = 0) -> Optional[np.ndarray]:
+    """bias [E] float32 = tau * ln p, or None."""
+    p = popularity_prior(wl, layer)
+    if p is None:
+        return None
+    return (wl.tau * np.log(p)).astype(np.float32)
+
+
+@dataclasses.dataclass
+class LayerInputs:
+    wl: Workload
+    layer: int
+    x: np.ndarray                   # [T, d] f32 or bf16 bits
+    wr: np.ndarray                  # [E, d] f32 or bf16 bits
+    bias: Optional[np.ndarray]      # [E] f32 or None
+    experts: list                   # E uint8 objects (or None when lazy)
+    shared: Optional[np.ndarray]    # uint8 object
+
+    def expert(self, e: int) -> np.ndarray:
+        if self.experts[e] is None:
+            self.experts[e] = expert_object(self.wl, self.layer, e)
+        return self.experts[e]
+
+
+def layer_inputs(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] = None,
+                 lazy: bool = False, shape: Optional[LayerShape] = None) -> LayerInputs:
+    """All inputs of one layer.  ``lazy`` defers drawing expert objects until
+    ``LayerInputs.expert(e)`` is called.  ``shape`` overrides the workload's
+    shape (same seeds) for reduced test sizes."""
+    if shape is not None:
+        wl = dataclasses.replace(wl, shape=shape)
+    s = wl.shape
+    experts = [None] * s.E if lazy else [expert_object(wl, layer, e) for e in range(s.E)]
+    return LayerInputs(
+        wl=wl, layer=layer,
+        x=hidden_states(wl, layer, step, T),
+        wr=router_weight(wl, layer),
+        bias=router_bias(wl, layer),
+        experts=experts,
+        shared=expert_object(wl, layer, 0, shared=True) if s.shared else None,
+    )

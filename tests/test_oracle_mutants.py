@@ -1,0 +1,35 @@
+"""Each planted mistake in the oracle (compiled with -DMSIO_MUTANT=n) must be
+caught by at least one pin.  The mistakes cover the bias term, the tie-break
+direction, the renormalisation, the SiLU sign, the gate/up operand, the shared
+expert, the 4-bit nibble order and the stability of the permutation."""
+import os
+
+import pytest
+
+import oracle
+import _pins
+
+MUTANTS = {
+    1: "bias dropped",
+    2: "ties go to the higher id",
+    3: "softmax not renormalised over the selected set",
+    4: "SiLU sign flipped",
+    5: "gate projection reads the up matrix",
+    6: "shared expert dropped",
+    8: "nibble order swapped",
+    9: "permutation walks tokens in reverse",
+}
+
+
+@pytest.mark.parametrize("mutant", sorted(MUTANTS), ids=lambda m: MUTANTS[m].replace(" ", "_"))
+def test_mutant_is_caught(tmp_path, mutant):
+    so = oracle.build(out=str(tmp_path / f"libmsi_oracle_m{mutant}.so"), mutant=mutant)
+    o = oracle.Oracle(oracle.load(so))
+    assert o.lib.msio_mutant() == mutant
+    caught = []
+    for pin in _pins.ALL_PINS:
+        try:
+            pin(o)
+        except AssertionError:
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches mutant {mutant} ({MUTANTS[mutant]})"
