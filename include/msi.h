@@ -1,0 +1,285 @@
+/*
+ * msi.h -- C ABI of the slot-backed routed-expert MoE layer for MI355X (gfx950).
+ *
+ * One MoE FFN layer (router softmax/top-K, token-by-expert permutation,
+ * gate/up projections with SiLU gating, down projection, weighted combine plus
+ * an always-on shared expert) executes against a bounded pool of reusable GPU
+ * expert slots.  Logical expert objects live in caller-owned host windows; the
+ * plan copies them into slots with stable device addresses, versions every
+ * copy with a generation, and the compute kernels check the generation of
+ * each slot they read, failing closed on a mismatch.
+ *
+ * The plan abstraction follows the paper's Section 3 (Design): an immutable
+ * manifest of objects, extents, windows and slots with stable addresses
+ * (Section 3.1), slot generations and bundle publication (Section 3.3), the
+ * separate window / GPU-slot state machines with tickets, epochs and consumer
+ * counts (Section 3.4, state sequences), replacement policy kept apart from
+ * the lifecycle (Section 3.1), and the scheduling loop of Section 4 ("Scheduling
+ * and copies": layer entry requests the bundle, misses are copied into
+ * reserved slots, a device event publishes readiness, layer exit releases the
+ * consumer ticket).  The lifetime obligations of Table 2 (row L) are the error
+ * behaviour below.  The MoE arithmetic itself is the layer every selected
+ * expert executes in the paper's principal experiment (Section 5.4: the stock
+ * router, then the complete gate, up and down projections).
+ *
+ * Conventions
+ *  - Every call returns msi_status (0 = MSI_OK, negative = error).  The text
+ *    of the last error on the calling thread is msi_last_error().  No C++
+ *    exception crosses this boundary.
+ *  - The caller owns every large buffer: the slot pool (device), the host
+ *    windows (pinned host memory), x / out / routing arrays / workspace
+ *    (device), and the HIP streams (passed as void* = hipStream_t; NULL is the
+ *    null stream).  The plan owns host metadata and small device arrays
+ *    (slot generation words, status word, schedule tables), freed by
+ *    msi_plan_destroy.
+ *  - Device pointers must be 16-byte aligned; the slot pool and slot stride
+ *    256-byte aligned.
+ *  - A plan is not thread-safe: calls on one plan must not overlap.  Plans
+ *    on the same device are independent.
+ *  - Storage formats (wdtype): MSI_W_F32 binary32; MSI_W_BF16 bfloat16 (top
+ *    half of binary32); MSI_W_Q4B32 4-bit blocks: a [rows, cols] matrix is
+ *    nibbles [rows, cols/2] (element 2j in the low nibble of byte j, 4-bit
+ *    two's complement) followed by fp16 scales [rows, cols/32], value =
+ *    scale * q.  Hidden states and the router weight are f32 for MSI_W_F32
+ *    and bf16 otherwise.
+ *  - An expert object is [Wg | Wu | Wd]: Wg, Wu are [d_ff, d_model] and Wd is
+ *    [d_model, d_ff], each row-major with the reduction axis contiguous.
+ *    The router weight is [n_experts, d_model] row-major.
+ */
+#ifndef MSI_H
+#define MSI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MSI_ABI_VERSION 1u
+
+typedef int32_t msi_status;
+
+#define MSI_OK 0
+#define MSI_E_INVALID_ARG (-1)  /* malformed argument, shape or alignment            */
+#define MSI_E_SHORT (-2)        /* extent shorter/longer than the object, or past the window */
+#define MSI_E_WRONG_OBJECT (-3) /* object not in this layer's manifest / slot not in its pool */
+#define MSI_E_BUSY (-4)         /* slot has live consumers; no slot can be freed      */
+#define MSI_E_STALE (-5)        /* a kernel saw a slot generation it did not expect    */
+#define MSI_E_DEVICE (-6)       /* HIP runtime error                                  */
+#define MSI_E_NOMEM (-7)        /* workspace too small or host allocation failed      */
+#define MSI_E_STATE (-8)        /* lifecycle transition not allowed in this state     */
+
+typedef enum { MSI_W_F32 = 0, MSI_W_BF16 = 1, MSI_W_Q4B32 = 2 } msi_wdtype;
+
+typedef struct msi_plan msi_plan;
+
+/* One logical object of the manifest: expert `expert` of layer `layer`,
+ * stored as `nbytes` bytes at `offset` inside host window `window`. */
+typedef struct {
+    uint32_t layer;
+    uint32_t expert;
+    uint32_t window;
+    uint32_t reserved;
+    uint64_t offset;
+    uint64_t nbytes;
+} msi_object_desc;
+
+/* Immutable manifest (Section 3.1).  Slot s (0 <= s < pool_slots) of layer l
+ * lives at slot_pool + (l * pool_slots + s) * slot_stride for the life of the
+ * plan, where pool_slots = slots_per_layer, or transient_slots when
+ * slots_per_layer == 0 (zero-cache: every use refills, nothing is retained
+ * across rounds or calls).  slot_pool_bytes must cover
+ * n_layers * pool_slots * slot_stride. */
+typedef struct {
+    uint32_t abi_version;        /* MSI_ABI_VERSION */
+    uint32_t n_layers;
+    uint32_t n_experts;          /* E, routed experts per layer, <= 1024     */
+    uint32_t d_model;            /* d, multiple of 256                        */
+    uint32_t d_ff;               /* I, expert intermediate, multiple of 128   */
+    uint32_t top_k;              /* K, 1 <= K <= min(E, 16)                   */
+    uint32_t wdtype;             /* msi_wdtype                                */
+    uint32_t slots_per_layer;    /* C >= 0; 0 selects zero-cache              */
+    uint32_t transient_slots;    /* zero-cache staging slots (0 -> 8), >= 2   */
+    uint32_t reserved0;
+    void *slot_pool;             /* device, caller-owned                      */
+    uint64_t slot_pool_bytes;
+    uint64_t slot_stride;        /* >= object bytes, multiple of 256          */
+    const void *const *windows;  /* n_windows host pointers, caller-owned; pinned memory */
+    uint32_t n_windows;
+    uint32_t n_objects;
+    uint64_t window_bytes;       /* size of every window                      */
+    const msi_object_desc *objects;
+} msi_plan_desc;
+
+/* Ticket of a fill (Section 3.4: tickets carry object, generation, epoch and
+ * resource identity). */
+typedef struct {
+    uint32_t layer;
+    uint32_t expert;
+    int32_t slot;
+    uint32_t generation;
+    uint32_t epoch;
+    uint32_t hit;                /* 1 if the object was already resident       */
+} msi_ticket;
+
+/* Device arrays describing one routing of T tokens (all caller-owned). */
+typedef struct {
+    int32_t *idx;                /* [T, K] selected experts, ascending per token      */
+    float *weights;              /* [T, K] gate weights (restricted softmax), fp32    */
+    int32_t *counts;             /* [E] tokens per expert                             */
+    int32_t *offsets;            /* [E + 1] exclusive prefix of counts                */
+    int32_t *perm;               /* [T * K] token of each permuted row; rows ordered by (expert, token) */
+    int32_t *inv;                /* [T, K] permuted row of each (token, k)            */
+    float *row_weight;           /* [T * K] gate weight of each permuted row          */
+} msi_routing;
+
+typedef struct {
+    uint32_t n_tokens;           /* T >= 0                                             */
+    uint32_t reserved;
+    const void *x;               /* [T, d] hidden states (f32 or bf16, see wdtype)     */
+    const void *w_router;        /* [E, d] router weight, same type as x               */
+    const float *bias;           /* [E] added to the logits before selection, or NULL  */
+    msi_routing r;               /* outputs                                            */
+    void *workspace;             /* msi_workspace_size(plan, T) bytes                  */
+    uint64_t workspace_bytes;
+} msi_route_args;
+
+typedef struct {
+    uint32_t layer;
+    uint32_t n_tokens;           /* T, same as the routing's                           */
+    const void *x;               /* [T, d] the routed hidden states                    */
+    msi_routing r;               /* produced by msi_route for this x                    */
+    const void *shared_object;   /* device [Wg | Wu | Wd] of the always-on shared expert, or NULL */
+    float *out;                  /* [T, d] fp32 output; written only on MSI_OK         */
+    void *workspace;
+    uint64_t workspace_bytes;
+} msi_forward_args;
+
+/* Per-slot view for tests and telemetry. */
+typedef enum {
+    MSI_SLOT_VACANT = 0,
+    MSI_SLOT_LOADING = 1,
+    MSI_SLOT_DEVICE_READY = 2,
+    MSI_SLOT_IN_USE = 3,
+    MSI_SLOT_RECYCLABLE = 4
+} msi_slot_state;
+
+typedef struct {
+    uint32_t state;              /* msi_slot_state                                     */
+    int32_t expert;              /* resident object, -1 if none                         */
+    uint32_t generation;
+    uint32_t epoch;
+    uint32_t consumers;          /* live consumers (forward rounds + holds)             */
+    uint32_t holds;              /* consumers held through msi_slot_hold                */
+    uint64_t last_use;           /* LRU tick                                            */
+} msi_slot_info;
+
+typedef struct {
+    uint64_t forwards;
+    uint64_t rounds;
+    uint64_t fills;              /* copies submitted                                    */
+    uint64_t fills_published;    /* completions that became DeviceReady                 */
+    uint64_t fills_discarded;    /* completions rejected (epoch/generation mismatch)    */
+    uint64_t hits;               /* demanded objects found resident                     */
+    uint64_t misses;
+    uint64_t evictions;          /* resident objects replaced                           */
+    uint64_t h2d_bytes;
+    uint64_t rejections;         /* BUSY / WRONG_OBJECT / SHORT / STATE returned        */
+    uint64_t stale_detected;     /* forwards that returned MSI_E_STALE                  */
+    uint64_t fills_in_flight;
+    uint64_t windows_busy;       /* windows with a copy in flight                       */
+    uint64_t consumers_live;
+    uint32_t epoch;
+    uint32_t reserved;
+} msi_stats;
+
+/* Text of the last error on this thread ("" if none).  Never NULL. */
+const char *msi_last_error(void);
+
+/* ABI version of the loaded library (MSI_ABI_VERSION). */
+uint32_t msi_abi_version(void);
+
+/* Validate the manifest and create a plan on the current HIP device
+ * (Section 3.1; stable addresses, Section 3.3; extent rejection conditions,
+ * Section 3.2).  Errors: MSI_E_INVALID_ARG (shape, alignment, pool too small,
+ * duplicate (layer, expert), window index out of range), MSI_E_SHORT (extent
+ * past its window, or nbytes != object size for wdtype and shape),
+ * MSI_E_DEVICE.  All slots start Vacant with generation 0, epoch 0. */
+msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out);
+
+/* Drain in-flight fills and free plan-owned memory.  MSI_E_BUSY (plan kept)
+ * if a consumer is still held through msi_slot_hold (shutdown with a live
+ * consumer, Section 3.4 / Table 5). */
+msi_status msi_plan_destroy(msi_plan *plan);
+
+/* Advance the request epoch (Section 3.4).  Fills still in flight become
+ * unpublishable: their completion leaves the slot Vacant.  Resident
+ * DeviceReady slots stay valid.  MSI_E_BUSY if a consumer is held. */
+msi_status msi_plan_reset(msi_plan *plan);
+
+/* Bytes of device workspace msi_route and msi_moe_forward need for T tokens. */
+msi_status msi_workspace_size(const msi_plan *plan, uint32_t n_tokens, uint64_t *bytes);
+
+/* Make expert `expert` of `layer` resident (Section 3.3; Section 4 scheduling).
+ * slot = -1 lets the replacement policy choose (least recently used slot
+ * without consumers); slot >= 0 forces that slot.  If the object is already
+ * resident and ready (in `slot` when forced) this is a hit: the ticket
+ * carries the current generation and nothing is copied.  Otherwise the slot
+ * goes Loading with generation g+1 and, on `side_stream`, its device
+ * generation word is invalidated, the extent is copied window -> slot, the
+ * word is set to g+1 and a ready event is recorded.  The completion is
+ * published (DeviceReady) only if the ticket's epoch and generation are still
+ * current when it is observed.  Errors: MSI_E_WRONG_OBJECT (no such object in
+ * this layer's manifest, or slot outside the layer's pool), MSI_E_BUSY (forced
+ * slot has live consumers, or every slot does), MSI_E_DEVICE. */
+msi_status msi_slot_fill(msi_plan *plan, uint32_t layer, uint32_t expert, int32_t slot,
+                         void *side_stream, msi_ticket *ticket);
+
+/* Observe completed fills and consumer releases without blocking. */
+msi_status msi_plan_poll(msi_plan *plan);
+
+/* Router and permutation on `stream` (no host synchronisation): logits
+ * (bf16 MFMA or fp32 with fp32 accumulation) plus bias, top-K by (logit desc,
+ * expert id asc), softmax restricted to the selected set in fp32, then the
+ * stable token-by-expert permutation.  Fully deterministic.  Errors:
+ * MSI_E_INVALID_ARG, MSI_E_NOMEM (workspace), MSI_E_DEVICE. */
+msi_status msi_route(msi_plan *plan, const msi_route_args *args, void *stream);
+
+/* One MoE layer against the slot pool (Section 4 scheduling).  Reads the
+ * per-expert counts (one device-to-host copy), resolves the demanded set
+ * against the residency state (hits first, then misses in ascending expert
+ * id, in rounds of at most the pool size), fills misses on `side_stream`
+ * overlapped with compute, runs the expert kernels on `compute_stream` with
+ * in-kernel generation checks, runs the shared expert, and publishes
+ * out[t] = shared(x_t) + sum over the token's experts in ascending id of
+ * w * expert(x_t), in fp32.  Blocks until the status word is known.
+ * out is bit-identical for every slot capacity.  Errors: MSI_E_STALE (a
+ * kernel saw an unexpected slot generation; out is untouched), MSI_E_BUSY (no
+ * slot could be freed), MSI_E_INVALID_ARG, MSI_E_NOMEM, MSI_E_DEVICE. */
+msi_status msi_moe_forward(msi_plan *plan, const msi_forward_args *args,
+                           void *compute_stream, void *side_stream);
+
+/* Hold / release one external consumer on a slot (a consumer ticket that
+ * outlives a forward; a held slot is never chosen as a victim and cannot be
+ * refilled).  MSI_E_STATE when unholding a slot with no holds. */
+msi_status msi_slot_hold(msi_plan *plan, uint32_t layer, uint32_t slot);
+msi_status msi_slot_unhold(msi_plan *plan, uint32_t layer, uint32_t slot);
+
+msi_status msi_slot_query(const msi_plan *plan, uint32_t layer, uint32_t slot, msi_slot_info *info);
+msi_status msi_plan_stats(const msi_plan *plan, msi_stats *stats);
+
+/* Test hook: overwrite one slot's device generation word (synchronously). */
+msi_status msi_debug_set_device_gen(msi_plan *plan, uint32_t layer, uint32_t slot, uint32_t gen);
+
+/* Expert-path selector of a forward, for tests: tokens-per-expert at or below
+ * which the weight-streaming path runs (the rest take the tiled MFMA path).
+ * Returns the current value; 0 keeps it.  The choice is a function of the
+ * routing only, never of capacity. */
+uint32_t msi_stream_threshold(uint32_t new_value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MSI_H */

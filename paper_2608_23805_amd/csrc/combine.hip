@@ -1,0 +1,75 @@
+// combine.hip -- publication of the layer output and slot generation words.
+//
+// The combine is the only kernel that writes the caller's output, and it does
+// so only when the status word is clean: an invalid completion never makes
+// data visible (lifetime obligations, Table 2 row L; fatal fault cells publish
+// nothing, Section 5.7).  out[t] = shared(x_t) + sum over the token's
+// experts in ascending id of the weighted contributions, summed in fp32 in
+// that fixed order so the result does not depend on slot capacity.
+#include "common.h"
+#include "kernels.h"
+
+namespace msi {
+
+__global__ void __launch_bounds__(256) combine_kernel(const float *__restrict__ y, const float *__restrict__ ys,
+                                                      const int32_t *__restrict__ inv, float *__restrict__ out,
+                                                      const uint32_t *__restrict__ status, int T, int K, int d)
+{
+    if (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+        return;
+    const int d4 = d / 4;
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(T) * d4)
+        return;
+    const int t = int(i / d4), c = int(i % d4) * 4;
+    float4 acc = ys ? *reinterpret_cast<const float4 *>(ys + int64_t(t) * d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < K; ++k) {
+        const int64_t row = inv[int64_t(t) * K + k];
+        const float4 v = *reinterpret_cast<const float4 *>(y + row * d + c);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    *reinterpret_cast<float4 *>(out + int64_t(t) * d + c) = acc;
+}
+
+hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,
+                          int T, int K, int d, hipStream_t s)
+{
+    const int64_t n = int64_t(T) * (d / 4);
+    if (n == 0)
+        return hipSuccess;
+    combine_kernel<<<unsigned((n + 255) / 256), 256, 0, s>>>(y, ys, inv, out, status, T, K, d);
+    return hipGetLastError();
+}
+
+// Generation words are written with vector stores from one lane per entry.
+__global__ void set_gens_kernel(uint32_t *gen_dev, GenBatch b)
+{
+    const uint32_t i = threadIdx.x;
+    if (i < b.n)
+        __hip_atomic_store(gen_dev + b.slot[i], b.value[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+hipError_t launch_set_gens(uint32_t *gen_dev, const GenBatch &b, hipStream_t s)
+{
+    if (b.n == 0)
+        return hipSuccess;
+    set_gens_kernel<<<1, GEN_BATCH, 0, s>>>(gen_dev, b);
+    return hipGetLastError();
+}
+
+__global__ void clear_word_kernel(uint32_t *w)
+{
+    if (threadIdx.x == 0)
+        __hip_atomic_store(w, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+hipError_t launch_clear_word(uint32_t *word, hipStream_t s)
+{
+    clear_word_kernel<<<1, 64, 0, s>>>(word);
+    return hipGetLastError();
+}
+
+}  // namespace msi

@@ -1,0 +1,118 @@
+// common.h -- device helpers shared by the gfx950 kernels of the MoE layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace msi {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+// 16-byte streaming load (non-temporal: the data is read once)
+__device__ __forceinline__ u32x4 load_stream16(const void *p)
+{
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+struct alignas(16) u16x8 {
+    uint16_t v[8];
+};
+
+// tokens per block of the permutation's bitmask ranks
+constexpr int PERM_BLOCK = 256;
+
+// status word bits written by kernels that detect a problem
+constexpr uint32_t STATUS_STALE = 1u;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+
+// binary32 -> bfloat16, round to nearest even (finite inputs; NaN stays NaN)
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u)
+        return uint16_t((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
+}
+
+// SiLU(z) = z * sigmoid(z) = z / (1 + e^-z), with the device library's expf
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8 &a, const bf16x8 &b, const f32x4 &c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8 &a, const bf16x8 &b, const f32x16 &c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <typename T>
+__device__ __forceinline__ bf16x8 as_bf16x8(const T &v)
+{
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Work item of one expert inside a launch: rows [row0, row0 + nrows) of the
+// permuted order, weights at pool + slot * stride, expected generation gen.
+// slot < 0 marks the shared expert (weights given directly, no generation).
+struct WorkItem {
+    int32_t expert;
+    int32_t slot;      // global slot index (layer * pool_slots + s) or -1
+    uint32_t gen;
+    int32_t row0;
+    int32_t nrows;
+    int32_t tile0;     // first tile of this item in the launch's tile space
+};
+
+// Find the item owning tile `t` (items sorted by tile0, tile0[0] == 0).
+__device__ __forceinline__ int find_item(const WorkItem *items, int n_items, int t)
+{
+    int lo = 0, hi = n_items - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (items[mid].tile0 <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// Generation check done by every tile before it reads a slot: true if the
+// slot denotes the version the host scheduled.  A mismatch raises the stale
+// bit (vector atomic) and the tile must write nothing.
+__device__ __forceinline__ bool slot_current(const WorkItem &it, const uint32_t *gen_dev, uint32_t *status)
+{
+    if (it.slot < 0)
+        return true;
+    uint32_t g = __hip_atomic_load(gen_dev + it.slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (g == it.gen)
+        return true;
+    if (threadIdx.x == 0)
+        atomicOr(status, STATUS_STALE);
+    return false;
+}
+
+// Logical tile index with consecutive tiles kept on one XCD: hardware hands
+// workgroup b to XCD b % 8, so XCD x walks tiles [x*per, (x+1)*per).
+__device__ __forceinline__ int xcd_swizzle(int b, int n)
+{
+    const int per = n / 8;
+    const int full = per * 8;
+    if (b >= full)
+        return b;
+    return (b % 8) * per + (b / 8);
+}
+
+}  // namespace msi

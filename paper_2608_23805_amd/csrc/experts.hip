@@ -1,0 +1,368 @@
+// experts.hip -- per-expert gate/up (SiLU-gated) and down projections for
+// gfx950, three variants chosen per expert from its routed-token count only:
+//
+//  * tile path (bf16, > STREAM tokens): LDS-staged MFMA tiles of gemm_tile.h.
+//  * stream path (bf16, <= 16 tokens): weight streaming.  The weights are the
+//    MFMA A operand read straight from HBM in the 16x16x32 fragment layout
+//    (each wavefront owns 16 weight rows; each weight byte is read once), the
+//    expert's tokens (at most 16, zero-padded) are the B operand held in LDS.
+//  * f32 path (fp32 layers): FMA dot products in fixed sequential order.
+//
+// Every workgroup checks the slot generation first and writes nothing on a
+// mismatch (fail closed).  Outputs: act[row, I] = silu(x Wg^T) * (x Wu^T) and
+// y[row, d] = row_weight * (act Wd^T), rows in permuted order.
+#include "common.h"
+#include "gemm_tile.h"
+#include "kernels.h"
+
+namespace msi {
+
+// ============================================================== tile path
+
+static TileArgs tile_args(const ExpertLaunch &L, bool gateup)
+{
+    TileArgs p{};
+    if (gateup) {
+        p.a = reinterpret_cast<const uint16_t *>(L.x);
+        p.lda = L.d;
+        p.perm = L.perm;
+        p.K = L.d;
+        p.n_tiles_n = L.I / 128;
+        p.out = L.act;
+        p.ldo = L.I;
+    } else {
+        p.a = reinterpret_cast<const uint16_t *>(L.act);
+        p.lda = L.I;
+        p.perm = nullptr;
+        p.K = L.I;
+        p.n_tiles_n = L.d / tile::BN;
+        p.out = L.y;
+        p.ldo = L.d;
+        p.row_weight = L.row_weight;
+    }
+    p.wbase = L.wbase;
+    p.wstride = L.wstride;
+    p.n_valid = 1 << 30;
+    p.d = L.d;
+    p.I = L.I;
+    p.items = L.items;
+    p.n_items = L.n_items;
+    p.gen_dev = L.gen_dev;
+    p.status = L.status;
+    return p;
+}
+
+int tiles_gateup_tile(int nrows, int d, int I)
+{
+    (void)d;
+    return ((nrows + tile::BM - 1) / tile::BM) * (I / 128);
+}
+
+int tiles_down_tile(int nrows, int d, int I)
+{
+    (void)I;
+    return ((nrows + tile::BM - 1) / tile::BM) * (d / tile::BN);
+}
+
+hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    tile_gemm_kernel<TileMode::GateUp><<<L.n_tiles, tile::THREADS, tile::LDS_BYTES, s>>>(tile_args(L, true));
+    return hipGetLastError();
+}
+
+hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    tile_gemm_kernel<TileMode::Down><<<L.n_tiles, tile::THREADS, tile::LDS_BYTES, s>>>(tile_args(L, false));
+    return hipGetLastError();
+}
+
+hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T,
+                                     int d, int E, hipStream_t s)
+{
+    if (T == 0)
+        return hipSuccess;
+    TileArgs p{};
+    p.a = x;
+    p.lda = d;
+    p.perm = nullptr;
+    p.wbase = reinterpret_cast<const uint8_t *>(wr);
+    p.wstride = 0;
+    p.K = d;
+    p.n_valid = E;
+    p.n_tiles_n = (E + tile::BN - 1) / tile::BN;
+    p.d = d;
+    p.items = nullptr;
+    p.n_items = 1;
+    p.single = WorkItem{-1, -1, 0u, 0, T, 0};
+    p.gen_dev = nullptr;
+    p.status = nullptr;
+    p.out = L;
+    p.ldo = E;
+    p.bias = bias;
+    const int tiles = ((T + tile::BM - 1) / tile::BM) * p.n_tiles_n;
+    tile_gemm_kernel<TileMode::Router><<<tiles, tile::THREADS, tile::LDS_BYTES, s>>>(p);
+    return hipGetLastError();
+}
+
+// ============================================================== stream path
+
+namespace stream {
+constexpr int MAXN = 16;        // tokens per expert handled by this path
+constexpr int WAVES = 4;
+constexpr int ROWS = 16;        // weight rows per wavefront
+}  // namespace stream
+
+int tiles_gateup_stream(int nrows, int d, int I)
+{
+    (void)nrows;
+    (void)d;
+    return I / (stream::WAVES * stream::ROWS);
+}
+
+int tiles_down_stream(int nrows, int d, int I)
+{
+    (void)nrows;
+    (void)I;
+    return d / (stream::WAVES * stream::ROWS);
+}
+
+// Stage the (<= 16) B-operand rows of one expert into LDS [16][K + 8].
+__device__ __forceinline__ void stage_rows(uint16_t *xs, const uint16_t *__restrict__ src, const int32_t *perm,
+                                           int row0, int n, int K)
+{
+    const int ldk = K + 8;
+    const int chunks = K / 8;
+    for (int c = threadIdx.x; c < n * chunks; c += blockDim.x) {
+        const int j = c / chunks, q = c % chunks;
+        const int64_t r = perm ? int64_t(perm[row0 + j]) : int64_t(row0 + j);
+        *reinterpret_cast<uint4 *>(xs + j * ldk + q * 8) =
+            *reinterpret_cast<const uint4 *>(src + r * K + q * 8);
+    }
+}
+
+template <int U>
+__global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
+{
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
+    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
+    if (!slot_current(it, L.gen_dev, L.status))
+        return;
+    const int n = it.nrows;
+    const int d = L.d, I = L.I, ldk = d + 8;
+    stage_rows(xs, reinterpret_cast<const uint16_t *>(L.x), L.perm, it.row0, n, d);
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int i0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
+    const int j = lane & 15, kg = (lane >> 4) * 8;
+    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + kg;
+    const uint16_t *up = gp + int64_t(I) * d;
+    const uint16_t *xr = xs + j * ldk + kg;
+    const bool live = j < n;
+
+    f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < d; k0 += 32 * U) {
+        u32x4 wg[U], wu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            wg[u] = load_stream16(gp + k0 + 32 * u);
+            wu[u] = load_stream16(up + k0 + 32 * u);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint4 xv = live ? *reinterpret_cast<const uint4 *>(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
+            const bf16x8 b = as_bf16x8(xv);
+            ag = mfma16(as_bf16x8(wg[u]), b, ag);
+            au = mfma16(as_bf16x8(wu[u]), b, au);
+        }
+    }
+    // lane holds rows i0 + 4*(lane/16) + r of token j
+    if (live) {
+        uint2 v;
+        v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
+        v.y = pack_bf16x2(silu(ag[2]) * au[2], silu(ag[3]) * au[3]);
+        uint16_t *act = reinterpret_cast<uint16_t *>(L.act) + int64_t(it.row0 + j) * I + i0 + 4 * (lane >> 4);
+        *reinterpret_cast<uint2 *>(act) = v;
+    }
+}
+
+template <int U>
+__global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
+{
+    extern __shared__ __attribute__((aligned(16))) uint16_t as[];
+    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
+    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
+    if (!slot_current(it, L.gen_dev, L.status))
+        return;
+    const int n = it.nrows;
+    const int d = L.d, I = L.I, ldk = I + 8;
+    stage_rows(as, reinterpret_cast<const uint16_t *>(L.act), nullptr, it.row0, n, I);
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int c0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
+    const int j = lane & 15, kg = (lane >> 4) * 8;
+    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const uint16_t *wp = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0 + j) * I + kg;
+    const uint16_t *ar = as + j * ldk + kg;
+    const bool live = j < n;
+
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < I; k0 += 32 * U) {
+        u32x4 w[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            w[u] = load_stream16(wp + k0 + 32 * u);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint4 av = live ? *reinterpret_cast<const uint4 *>(ar + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
+            acc = mfma16(as_bf16x8(w[u]), as_bf16x8(av), acc);
+        }
+    }
+    if (live) {
+        const int64_t row = it.row0 + j;
+        const float w = L.row_weight ? L.row_weight[row] : 1.0f;
+        float4 o = make_float4(acc[0] * w, acc[1] * w, acc[2] * w, acc[3] * w);
+        *reinterpret_cast<float4 *>(L.y + row * d + c0 + 4 * (lane >> 4)) = o;
+    }
+}
+
+hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    const size_t lds = size_t(stream::MAXN) * (L.d + 8) * sizeof(uint16_t);
+    if (L.d % 256 == 0)
+        stream_gateup_kernel<8><<<L.n_tiles, 256, lds, s>>>(L);
+    else
+        stream_gateup_kernel<1><<<L.n_tiles, 256, lds, s>>>(L);
+    return hipGetLastError();
+}
+
+hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    const size_t lds = size_t(stream::MAXN) * (L.I + 8) * sizeof(uint16_t);
+    if (L.I % 512 == 0)
+        stream_down_kernel<16><<<L.n_tiles, 256, lds, s>>>(L);
+    else
+        stream_down_kernel<4><<<L.n_tiles, 256, lds, s>>>(L);
+    return hipGetLastError();
+}
+
+// ============================================================== f32 path
+
+namespace f32p {
+constexpr int TR = 16, TC = 16;   // 16 rows x 16 columns per 256-thread block
+}
+
+int tiles_gateup_f32(int nrows, int d, int I)
+{
+    (void)d;
+    return ((nrows + f32p::TR - 1) / f32p::TR) * (I / f32p::TC);
+}
+
+int tiles_down_f32(int nrows, int d, int I)
+{
+    (void)I;
+    return ((nrows + f32p::TR - 1) / f32p::TR) * (d / f32p::TC);
+}
+
+__global__ void __launch_bounds__(256) gateup_f32_kernel(ExpertLaunch L)
+{
+    const int t = int(blockIdx.x);
+    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
+    if (!slot_current(it, L.gen_dev, L.status))
+        return;
+    const int local = t - it.tile0;
+    const int nct = L.I / f32p::TC;
+    const int r = (local / nct) * f32p::TR + int(threadIdx.x) / f32p::TC;
+    const int c = (local % nct) * f32p::TC + int(threadIdx.x) % f32p::TC;
+    if (r >= it.nrows)
+        return;
+    const int d = L.d;
+    const int64_t src = L.perm ? int64_t(L.perm[it.row0 + r]) : int64_t(it.row0 + r);
+    const float *x = reinterpret_cast<const float *>(L.x) + src * d;
+    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const float *wg = reinterpret_cast<const float *>(base) + int64_t(c) * d;
+    const float *wu = wg + int64_t(L.I) * d;
+    float g = 0.f, u = 0.f;
+    for (int k = 0; k < d; ++k) {
+        g = fmaf(x[k], wg[k], g);
+        u = fmaf(x[k], wu[k], u);
+    }
+    reinterpret_cast<float *>(L.act)[int64_t(it.row0 + r) * L.I + c] = silu(g) * u;
+}
+
+__global__ void __launch_bounds__(256) down_f32_kernel(ExpertLaunch L)
+{
+    const int t = int(blockIdx.x);
+    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
+    if (!slot_current(it, L.gen_dev, L.status))
+        return;
+    const int local = t - it.tile0;
+    const int nct = L.d / f32p::TC;
+    const int r = (local / nct) * f32p::TR + int(threadIdx.x) / f32p::TC;
+    const int c = (local % nct) * f32p::TC + int(threadIdx.x) % f32p::TC;
+    if (r >= it.nrows)
+        return;
+    const int I = L.I;
+    const int64_t row = it.row0 + r;
+    const float *a = reinterpret_cast<const float *>(L.act) + row * I;
+    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const float *wd = reinterpret_cast<const float *>(base) + int64_t(2) * I * L.d + int64_t(c) * I;
+    float acc = 0.f;
+    for (int k = 0; k < I; ++k)
+        acc = fmaf(a[k], wd[k], acc);
+    const float w = L.row_weight ? L.row_weight[row] : 1.0f;
+    L.y[row * L.d + c] = acc * w;
+}
+
+hipError_t launch_gateup_f32(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    gateup_f32_kernel<<<L.n_tiles, 256, 0, s>>>(L);
+    return hipGetLastError();
+}
+
+hipError_t launch_down_f32(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    down_f32_kernel<<<L.n_tiles, 256, 0, s>>>(L);
+    return hipGetLastError();
+}
+
+}  // namespace msi
+
+namespace msi {
+
+hipError_t init_kernel_attributes()
+{
+    const int big = 160 * 1024;
+    hipError_t e = hipSuccess;
+    auto set = [&](const void *f) {
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+    };
+    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
+    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
+    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Down>));
+    set(reinterpret_cast<const void *>(&stream_gateup_kernel<8>));
+    set(reinterpret_cast<const void *>(&stream_gateup_kernel<1>));
+    set(reinterpret_cast<const void *>(&stream_down_kernel<16>));
+    set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
+    return e;
+}
+
+}  // namespace msi

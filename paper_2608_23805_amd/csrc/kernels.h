@@ -1,0 +1,69 @@
+// kernels.h -- host launchers of the gfx950 kernels (all asynchronous on the
+// given stream; they return the launch error, if any).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace msi {
+
+// ---- router and permutation (route.hip)
+hipError_t launch_router_logits_f32(const float *x, const float *wr, const float *bias, float *L, int T, int d,
+                                    int E, hipStream_t s);
+hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T,
+                                     int d, int E, hipStream_t s);
+// raise the dynamic LDS limit of the kernels that use more than 64 KiB
+hipError_t init_kernel_attributes();
+hipError_t launch_topk(const float *L, int32_t *idx, float *w, int T, int E, int K, hipStream_t s);
+hipError_t launch_permute(const int32_t *idx, const float *w, int32_t *counts, int32_t *offsets, int32_t *perm,
+                          int32_t *inv, float *row_weight, int32_t *blockhist, int T, int K, int E,
+                          hipStream_t s);
+
+// ---- expert projections (experts.hip).  `items` lists the experts of one
+// launch (device memory), `n_tiles` the launch's total tile count.
+struct ExpertLaunch {
+    const WorkItem *items;
+    int n_items;
+    int n_tiles;
+    const void *x;               // [T, d] hidden states (bf16 or f32)
+    const int32_t *perm;         // gather map, null for the shared expert
+    const uint8_t *wbase;        // slot pool (routed) or shared object
+    uint64_t wstride;
+    const uint32_t *gen_dev;
+    uint32_t *status;
+    void *act;                   // [rows, I] bf16 (f32 for f32 layers)
+    float *y;                    // [rows, d]
+    const float *row_weight;     // per permuted row, or null (1.0)
+    int d, I;
+};
+
+// tiles per item of each launch kind
+int tiles_gateup_tile(int nrows, int d, int I);
+int tiles_down_tile(int nrows, int d, int I);
+int tiles_gateup_stream(int nrows, int d, int I);
+int tiles_down_stream(int nrows, int d, int I);
+int tiles_gateup_f32(int nrows, int d, int I);
+int tiles_down_f32(int nrows, int d, int I);
+
+hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_gateup_f32(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_f32(const ExpertLaunch &L, hipStream_t s);
+
+// ---- combine / publication and slot generation words (combine.hip)
+hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,
+                          int T, int K, int d, hipStream_t s);
+constexpr int GEN_BATCH = 64;
+struct GenBatch {
+    uint32_t n;
+    uint32_t slot[GEN_BATCH];
+    uint32_t value[GEN_BATCH];
+};
+hipError_t launch_set_gens(uint32_t *gen_dev, const GenBatch &b, hipStream_t s);
+hipError_t launch_clear_word(uint32_t *word, hipStream_t s);
+
+}  // namespace msi

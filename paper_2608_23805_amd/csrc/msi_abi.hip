@@ -1,0 +1,673 @@
+// msi_abi.hip -- C ABI of the slot-backed MoE layer (declared in include/msi.h).
+//
+// Host side of the paper's Section 4 scheduling loop: layer entry requests
+// the bundle of demanded experts, misses are copied from their host windows
+// into reserved slots on a side stream, a device event publishes readiness,
+// the expert kernels consume the slots at stable addresses, and layer exit
+// releases the consumers.  Residency decisions live in PlanCore (pure C++);
+// this file owns HIP memory, streams, events and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/msi.h"
+#include "kernels.h"
+#include "plan_core.hpp"
+
+using namespace msi;
+
+namespace {
+
+thread_local std::string g_err;
+uint32_t g_stream_threshold = 16;   // tokens per expert at or below which the stream path runs
+
+msi_status fail(msi_status st, const std::string &m)
+{
+    g_err = m;
+    return st;
+}
+
+#define HIP_OK(expr)                                                                        \
+    do {                                                                                    \
+        hipError_t e_ = (expr);                                                             \
+        if (e_ != hipSuccess)                                                               \
+            return fail(MSI_E_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+uint64_t matrix_bytes(uint32_t wdtype, uint64_t rows, uint64_t cols)
+{
+    switch (wdtype) {
+    case MSI_W_F32: return rows * cols * 4;
+    case MSI_W_BF16: return rows * cols * 2;
+    default: return rows * cols / 2 + rows * (cols / 32) * 2;
+    }
+}
+
+uint64_t object_bytes_of(const msi_plan_desc &d)
+{
+    return 2 * matrix_bytes(d.wdtype, d.d_ff, d.d_model) + matrix_bytes(d.wdtype, d.d_model, d.d_ff);
+}
+
+// Workspace layout for T tokens (offsets in bytes, each region 256-aligned).
+struct Workspace {
+    size_t logits, blockhist, act, act_s, y, ys, total;
+};
+
+Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
+{
+    const uint64_t E = d.n_experts, K = d.top_k, I = d.d_ff, D = d.d_model;
+    const uint64_t nblk = (T + PERM_BLOCK - 1) / PERM_BLOCK;
+    const uint64_t ab = d.wdtype == MSI_W_F32 ? 4 : 2;   // act element bytes
+    Workspace w{};
+    size_t off = 0;
+    w.logits = off;
+    off += align256(T * E * 4);
+    w.blockhist = off;
+    off += align256(std::max<uint64_t>(nblk, 1) * E * 4);
+    w.act = off;
+    off += align256(T * K * I * ab);
+    w.act_s = off;
+    off += align256(T * I * ab);
+    w.y = off;
+    off += align256(T * K * D * 4);
+    w.ys = off;
+    off += align256(T * D * 4);
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
+struct msi_plan {
+    msi_plan_desc desc{};
+    std::vector<const void *> windows;
+    uint64_t object_bytes = 0;
+    PlanCore *core = nullptr;
+    int device = 0;
+    uint32_t *gen_dev = nullptr;        // [n_layers * pool_slots]
+    uint32_t *status_dev = nullptr;
+    WorkItem *table_dev = nullptr;
+    WorkItem *table_host = nullptr;     // pinned staging
+    size_t table_cap = 0;
+    int32_t *counts_host = nullptr;     // pinned [E]
+    uint32_t *status_host = nullptr;    // pinned
+    std::vector<hipEvent_t> free_events;
+    std::vector<hipEvent_t> all_events;
+    std::vector<hipEvent_t> fill_ev;    // per global slot: pending fill (owned)
+    std::vector<int64_t> fill_ev_id;    // fill id the pending event completes
+    std::vector<hipEvent_t> release_ev; // per global slot: last round reading it (current forward)
+    std::vector<uint8_t> fill_ev_shared;// event shared by a round batch (not owned per slot)
+
+    hipEvent_t get_event()
+    {
+        if (free_events.empty()) {
+            hipEvent_t e;
+            if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess)
+                return nullptr;
+            all_events.push_back(e);
+            return e;
+        }
+        hipEvent_t e = free_events.back();
+        free_events.pop_back();
+        return e;
+    }
+};
+
+namespace {
+
+// Observe a completed fill event of global slot gs.
+void observe_fill(msi_plan *p, uint32_t gs)
+{
+    if (!p->fill_ev[gs])
+        return;
+    p->core->complete_fill(p->fill_ev_id[gs]);
+    if (!p->fill_ev_shared[gs])
+        p->free_events.push_back(p->fill_ev[gs]);
+    p->fill_ev[gs] = nullptr;
+    p->fill_ev_id[gs] = -1;
+    p->fill_ev_shared[gs] = 0;
+}
+
+void poll_fills(msi_plan *p)
+{
+    for (uint32_t gs = 0; gs < p->fill_ev.size(); ++gs)
+        if (p->fill_ev[gs] && hipEventQuery(p->fill_ev[gs]) == hipSuccess)
+            observe_fill(p, gs);
+}
+
+// Enqueue on `side` the invalidate -> copy -> publish sequence of a batch of
+// fills (all ids already recorded by the core).  The side stream first waits
+// for every earlier fill and every reading round of each target slot.
+msi_status enqueue_fills(msi_plan *p, uint32_t layer, const std::vector<FillRecord> &fills, hipStream_t side)
+{
+    const PlanCore &c = *p->core;
+    for (const FillRecord &fr : fills) {
+        const FillRecord *f = &fr;
+        const uint32_t gs = c.global_slot(layer, f->slot);
+        if (p->fill_ev[gs])
+            HIP_OK(hipStreamWaitEvent(side, p->fill_ev[gs], 0));
+        if (p->release_ev[gs])
+            HIP_OK(hipStreamWaitEvent(side, p->release_ev[gs], 0));
+    }
+    for (size_t b = 0; b < fills.size(); b += GEN_BATCH) {
+        GenBatch inval{}, pub{};
+        const size_t e = std::min(fills.size(), b + GEN_BATCH);
+        for (size_t i = b; i < e; ++i) {
+            const FillRecord *f = &fills[i];
+            const uint32_t gs = c.global_slot(layer, f->slot);
+            inval.slot[inval.n] = gs;
+            inval.value[inval.n++] = 0u;
+            pub.slot[pub.n] = gs;
+            pub.value[pub.n++] = f->gen;
+        }
+        HIP_OK(launch_set_gens(p->gen_dev, inval, side));
+        for (size_t i = b; i < e; ++i) {
+            const FillRecord *f = &fills[i];
+            const uint32_t gs = c.global_slot(layer, f->slot);
+            uint8_t *dst = static_cast<uint8_t *>(p->desc.slot_pool) + uint64_t(gs) * p->desc.slot_stride;
+            const uint8_t *src = static_cast<const uint8_t *>(p->windows[f->window]) + f->offset;
+            HIP_OK(hipMemcpyAsync(dst, src, f->nbytes, hipMemcpyHostToDevice, side));
+        }
+        HIP_OK(launch_set_gens(p->gen_dev, pub, side));
+    }
+    return MSI_OK;
+}
+
+bool routing_ok(const msi_routing &r)
+{
+    return r.idx && r.weights && r.counts && r.offsets && r.perm && r.inv && r.row_weight;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *msi_last_error(void) { return g_err.c_str(); }
+
+uint32_t msi_abi_version(void) { return MSI_ABI_VERSION; }
+
+uint32_t msi_stream_threshold(uint32_t v)
+{
+    if (v)
+        g_stream_threshold = std::min<uint32_t>(v, 16u);
+    return g_stream_threshold;
+}
+
+msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
+{
+    if (!desc || !out)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    *out = nullptr;
+    const uint64_t ob = object_bytes_of(*desc);
+    PlanCore *core = new (std::nothrow) PlanCore(*desc, ob);
+    if (!core)
+        return fail(MSI_E_NOMEM, "host allocation failed");
+    if (core->status() != MSI_OK) {
+        const msi_status st = core->status();
+        const std::string m = core->error();
+        delete core;
+        return fail(st, m);
+    }
+    msi_plan *p = new (std::nothrow) msi_plan();
+    if (!p) {
+        delete core;
+        return fail(MSI_E_NOMEM, "host allocation failed");
+    }
+    p->desc = *desc;
+    p->windows.assign(desc->windows, desc->windows + desc->n_windows);
+    p->desc.windows = nullptr;
+    p->desc.objects = nullptr;
+    p->object_bytes = ob;
+    p->core = core;
+    const size_t nslots = size_t(core->n_layers()) * core->pool_slots();
+    p->fill_ev.assign(nslots, nullptr);
+    p->fill_ev_id.assign(nslots, -1);
+    p->release_ev.assign(nslots, nullptr);
+    p->fill_ev_shared.assign(nslots, 0);
+    p->table_cap = 2 * size_t(desc->n_experts) + 8;
+    auto cleanup = [&](msi_status st, const std::string &m) {
+        msi_plan_destroy(p);
+        return fail(st, m);
+    };
+    if (hipGetDevice(&p->device) != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "no HIP device");
+    if (init_kernel_attributes() != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "hipFuncSetAttribute failed");
+    if (hipMalloc(&p->gen_dev, nslots * sizeof(uint32_t)) != hipSuccess ||
+        hipMalloc(&p->status_dev, 256) != hipSuccess ||
+        hipMalloc(&p->table_dev, p->table_cap * sizeof(WorkItem)) != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "device allocation failed");
+    if (hipHostMalloc(&p->table_host, p->table_cap * sizeof(WorkItem), hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->counts_host, sizeof(int32_t) * desc->n_experts, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->status_host, 256, hipHostMallocDefault) != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "pinned host allocation failed");
+    if (hipMemset(p->gen_dev, 0, nslots * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(p->status_dev, 0, 256) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "device initialisation failed");
+    *out = p;
+    return MSI_OK;
+}
+
+msi_status msi_plan_destroy(msi_plan *p)
+{
+    if (!p)
+        return MSI_OK;
+    if (p->core) {
+        for (uint32_t gs = 0; gs < p->fill_ev.size(); ++gs)
+            if (p->fill_ev[gs]) {
+                (void)hipEventSynchronize(p->fill_ev[gs]);
+                observe_fill(p, gs);
+            }
+        if (p->core->any_holds()) {
+            p->core->stats().rejections++;
+            return fail(MSI_E_BUSY, "shutdown with a live held consumer");
+        }
+    }
+    for (hipEvent_t e : p->all_events)
+        (void)hipEventDestroy(e);
+    if (p->gen_dev)
+        (void)hipFree(p->gen_dev);
+    if (p->status_dev)
+        (void)hipFree(p->status_dev);
+    if (p->table_dev)
+        (void)hipFree(p->table_dev);
+    if (p->table_host)
+        (void)hipHostFree(p->table_host);
+    if (p->counts_host)
+        (void)hipHostFree(p->counts_host);
+    if (p->status_host)
+        (void)hipHostFree(p->status_host);
+    delete p->core;
+    delete p;
+    return MSI_OK;
+}
+
+msi_status msi_plan_reset(msi_plan *p)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    poll_fills(p);
+    const msi_status st = p->core->reset();
+    return st == MSI_OK ? st : fail(st, p->core->error());
+}
+
+msi_status msi_workspace_size(const msi_plan *p, uint32_t T, uint64_t *bytes)
+{
+    if (!p || !bytes)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    *bytes = workspace_layout(p->desc, T).total;
+    return MSI_OK;
+}
+
+msi_status msi_plan_poll(msi_plan *p)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    poll_fills(p);
+    return MSI_OK;
+}
+
+msi_status msi_slot_fill(msi_plan *p, uint32_t layer, uint32_t expert, int32_t slot, void *side_stream,
+                         msi_ticket *ticket)
+{
+    if (!p || !ticket)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    HIP_OK(hipSetDevice(p->device));
+    poll_fills(p);
+    int64_t id = -1;
+    const msi_status st = p->core->request_fill(layer, expert, slot, ticket, &id);
+    if (st != MSI_OK)
+        return fail(st, p->core->error());
+    if (ticket->hit)
+        return MSI_OK;
+    hipStream_t side = static_cast<hipStream_t>(side_stream);
+    const uint32_t gs = p->core->global_slot(layer, uint32_t(ticket->slot));
+    const std::vector<FillRecord> fills{*p->core->fill(id)};
+    msi_status est = enqueue_fills(p, layer, fills, side);
+    if (est != MSI_OK)
+        return est;
+    // the superseded fill (if any) was accounted by the core; its event is
+    // still waited on above, so release it now
+    if (p->fill_ev[gs]) {
+        if (!p->fill_ev_shared[gs])
+            p->free_events.push_back(p->fill_ev[gs]);
+        p->fill_ev[gs] = nullptr;
+    }
+    hipEvent_t ev = p->get_event();
+    if (!ev)
+        return fail(MSI_E_DEVICE, "event creation failed");
+    HIP_OK(hipEventRecord(ev, side));
+    p->fill_ev[gs] = ev;
+    p->fill_ev_id[gs] = id;
+    p->fill_ev_shared[gs] = 0;
+    return MSI_OK;
+}
+
+msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
+{
+    if (!p || !a)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    const msi_plan_desc &d = p->desc;
+    const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model);
+    if (a->n_tokens > (1u << 24))
+        return fail(MSI_E_INVALID_ARG, "n_tokens too large");
+    if (!routing_ok(a->r) || (T > 0 && (!a->x || !a->w_router)))
+        return fail(MSI_E_INVALID_ARG, "null routing or input pointer");
+    const Workspace ws = workspace_layout(d, a->n_tokens);
+    if (!a->workspace || a->workspace_bytes < ws.total)
+        return fail(MSI_E_NOMEM, "workspace smaller than msi_workspace_size");
+    HIP_OK(hipSetDevice(p->device));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
+    float *L = reinterpret_cast<float *>(wsb + ws.logits);
+    if (T > 0) {
+        if (d.wdtype == MSI_W_F32)
+            HIP_OK(launch_router_logits_f32(static_cast<const float *>(a->x), static_cast<const float *>(a->w_router),
+                                            a->bias, L, T, D, E, s));
+        else
+            HIP_OK(launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
+                                             static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s));
+        HIP_OK(launch_topk(L, a->r.idx, a->r.weights, T, E, K, s));
+    }
+    HIP_OK(launch_permute(a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv, a->r.row_weight,
+                          reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s));
+    return MSI_OK;
+}
+
+msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute_stream, void *side_stream)
+{
+    if (!p || !a)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    const msi_plan_desc &d = p->desc;
+    PlanCore &core = *p->core;
+    const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model), I = int(d.d_ff);
+    if (a->layer >= d.n_layers)
+        return fail(MSI_E_INVALID_ARG, "layer out of range");
+    if (a->n_tokens > (1u << 24))
+        return fail(MSI_E_INVALID_ARG, "n_tokens too large");
+    if (!routing_ok(a->r) || !a->out || (T > 0 && !a->x))
+        return fail(MSI_E_INVALID_ARG, "null routing, input or output pointer");
+    const Workspace ws = workspace_layout(d, a->n_tokens);
+    if (!a->workspace || a->workspace_bytes < ws.total)
+        return fail(MSI_E_NOMEM, "workspace smaller than msi_workspace_size");
+    HIP_OK(hipSetDevice(p->device));
+    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
+    hipStream_t side = static_cast<hipStream_t>(side_stream);
+    uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
+    poll_fills(p);
+
+    // ---- layer entry: the demanded set (one device-to-host read of the counts)
+    HIP_OK(hipMemcpyAsync(p->counts_host, a->r.counts, sizeof(int32_t) * E, hipMemcpyDeviceToHost, cs));
+    HIP_OK(hipStreamSynchronize(cs));
+    std::vector<int32_t> demanded;
+    std::vector<int32_t> counts(p->counts_host, p->counts_host + E);
+    std::vector<int32_t> offsets(E + 1, 0);
+    for (int e = 0; e < E; ++e) {
+        if (counts[e] < 0 || counts[e] > T)
+            return fail(MSI_E_INVALID_ARG, "routing counts out of range");
+        offsets[e + 1] = offsets[e] + counts[e];
+        if (counts[e] > 0)
+            demanded.push_back(e);
+    }
+    if (offsets[E] != T * K)
+        return fail(MSI_E_INVALID_ARG, "routing counts do not sum to T * K");
+
+    Schedule sched;
+    const msi_status sst = core.schedule_forward(a->layer, demanded, &sched);
+    if (sst != MSI_OK)
+        return fail(sst, core.error());
+
+    // ---- work tables: per round, gate/up and down launches of each path
+    enum Kind { GU_TILE, GU_STREAM, GU_F32, DN_TILE, DN_STREAM, DN_F32, NKIND };
+    struct Launch {
+        int kind;
+        bool shared;
+        size_t off;
+        int n_items;
+        int n_tiles;
+    };
+    std::vector<std::vector<Launch>> launches(sched.rounds.size());
+    std::vector<WorkItem> table;
+    const bool f32 = d.wdtype == MSI_W_F32;
+    auto add_launch = [&](size_t r, int kind, bool shared, const std::vector<WorkItem> &items) {
+        if (items.empty())
+            return;
+        Launch l{kind, shared, table.size(), int(items.size()), 0};
+        int tiles = 0;
+        for (WorkItem w : items) {
+            int n;
+            switch (kind) {
+            case GU_TILE: n = tiles_gateup_tile(w.nrows, D, I); break;
+            case GU_STREAM: n = tiles_gateup_stream(w.nrows, D, I); break;
+            case GU_F32: n = tiles_gateup_f32(w.nrows, D, I); break;
+            case DN_TILE: n = tiles_down_tile(w.nrows, D, I); break;
+            case DN_STREAM: n = tiles_down_stream(w.nrows, D, I); break;
+            default: n = tiles_down_f32(w.nrows, D, I); break;
+            }
+            w.tile0 = tiles;
+            tiles += n;
+            table.push_back(w);
+        }
+        l.n_tiles = tiles;
+        launches[r].push_back(l);
+    };
+    const uint32_t thr = g_stream_threshold;
+    for (size_t r = 0; r < sched.rounds.size(); ++r) {
+        std::vector<WorkItem> tile_items, stream_items;
+        for (const SchedItem &si : sched.rounds[r].items) {
+            WorkItem w{si.expert, int32_t(core.global_slot(a->layer, uint32_t(si.slot))), si.gen, offsets[si.expert],
+                       counts[si.expert], 0};
+            (f32 || uint32_t(w.nrows) > thr ? tile_items : stream_items).push_back(w);
+        }
+        add_launch(r, f32 ? GU_F32 : GU_TILE, false, tile_items);
+        add_launch(r, GU_STREAM, false, stream_items);
+        add_launch(r, f32 ? DN_F32 : DN_TILE, false, tile_items);
+        add_launch(r, DN_STREAM, false, stream_items);
+    }
+    const bool has_shared = a->shared_object && T > 0;
+    if (has_shared) {
+        if (sched.rounds.empty())
+            launches.emplace_back();
+        const std::vector<WorkItem> sh{WorkItem{-1, -1, 0u, 0, T, 0}};
+        const bool st = !f32 && uint32_t(T) <= thr;
+        add_launch(0, f32 ? GU_F32 : (st ? GU_STREAM : GU_TILE), true, sh);
+        add_launch(0, f32 ? DN_F32 : (st ? DN_STREAM : DN_TILE), true, sh);
+    }
+    if (table.size() > p->table_cap)
+        return fail(MSI_E_INVALID_ARG, "internal: schedule table overflow");
+    if (!table.empty()) {
+        std::memcpy(p->table_host, table.data(), table.size() * sizeof(WorkItem));
+        HIP_OK(hipMemcpyAsync(p->table_dev, p->table_host, table.size() * sizeof(WorkItem), hipMemcpyHostToDevice,
+                              cs));
+    }
+    HIP_OK(launch_clear_word(p->status_dev, cs));
+
+    // ---- rounds: fills on the side stream, kernels on the compute stream
+    std::vector<hipEvent_t> round_events;
+    auto new_event = [&]() -> hipEvent_t {
+        hipEvent_t e = p->get_event();
+        if (e)
+            round_events.push_back(e);
+        return e;
+    };
+    msi_status rst = MSI_OK;
+    for (size_t r = 0; r < launches.size() && rst == MSI_OK; ++r) {
+        if (r < sched.rounds.size()) {
+            const SchedRound &round = sched.rounds[r];
+            if (!round.fills.empty()) {
+                rst = enqueue_fills(p, a->layer, round.fills, side);
+                if (rst != MSI_OK)
+                    break;
+                hipEvent_t fe = new_event();
+                if (!fe) {
+                    rst = fail(MSI_E_DEVICE, "event creation failed");
+                    break;
+                }
+                HIP_OK(hipEventRecord(fe, side));
+                for (const FillRecord &f : round.fills) {
+                    const uint32_t gs = core.global_slot(a->layer, f.slot);
+                    if (p->fill_ev[gs] && !p->fill_ev_shared[gs])
+                        p->free_events.push_back(p->fill_ev[gs]);
+                    p->fill_ev[gs] = fe;
+                    p->fill_ev_id[gs] = f.id;
+                    p->fill_ev_shared[gs] = 1;
+                }
+            }
+            // hits whose fill (an earlier explicit request) is still pending
+            for (const SchedItem &si : round.items) {
+                const uint32_t gs = core.global_slot(a->layer, uint32_t(si.slot));
+                if (p->fill_ev[gs])
+                    HIP_OK(hipStreamWaitEvent(cs, p->fill_ev[gs], 0));
+            }
+        }
+        for (const Launch &l : launches[r]) {
+            ExpertLaunch L{};
+            L.items = p->table_dev + l.off;
+            L.n_items = l.n_items;
+            L.n_tiles = l.n_tiles;
+            L.x = a->x;
+            L.gen_dev = p->gen_dev;
+            L.status = p->status_dev;
+            L.d = D;
+            L.I = I;
+            if (l.shared) {
+                L.perm = nullptr;
+                L.wbase = static_cast<const uint8_t *>(a->shared_object);
+                L.wstride = 0;
+                L.act = wsb + ws.act_s;
+                L.y = reinterpret_cast<float *>(wsb + ws.ys);
+                L.row_weight = nullptr;
+            } else {
+                L.perm = a->r.perm;
+                L.wbase = static_cast<const uint8_t *>(d.slot_pool);
+                L.wstride = d.slot_stride;
+                L.act = wsb + ws.act;
+                L.y = reinterpret_cast<float *>(wsb + ws.y);
+                L.row_weight = a->r.row_weight;
+            }
+            hipError_t e;
+            switch (l.kind) {
+            case GU_TILE: e = launch_gateup_tile(L, cs); break;
+            case GU_STREAM: e = launch_gateup_stream(L, cs); break;
+            case GU_F32: e = launch_gateup_f32(L, cs); break;
+            case DN_TILE: e = launch_down_tile(L, cs); break;
+            case DN_STREAM: e = launch_down_stream(L, cs); break;
+            default: e = launch_down_f32(L, cs); break;
+            }
+            if (e != hipSuccess) {
+                rst = fail(MSI_E_DEVICE, std::string("expert kernel launch: ") + hipGetErrorString(e));
+                break;
+            }
+        }
+        if (rst != MSI_OK)
+            break;
+        if (r < sched.rounds.size()) {
+            hipEvent_t re = new_event();
+            if (!re) {
+                rst = fail(MSI_E_DEVICE, "event creation failed");
+                break;
+            }
+            HIP_OK(hipEventRecord(re, cs));
+            for (const SchedItem &si : sched.rounds[r].items)
+                p->release_ev[core.global_slot(a->layer, uint32_t(si.slot))] = re;
+        }
+    }
+
+    // ---- publication: out written only if every tile saw its generation
+    if (rst == MSI_OK)
+        if (launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
+                           has_shared ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv, a->out,
+                           p->status_dev, T, K, D, cs) != hipSuccess)
+            rst = fail(MSI_E_DEVICE, "combine launch failed");
+    if (rst == MSI_OK && hipMemcpyAsync(p->status_host, p->status_dev, sizeof(uint32_t), hipMemcpyDeviceToHost,
+                                        cs) != hipSuccess)
+        rst = fail(MSI_E_DEVICE, "status read failed");
+    const hipError_t se = hipStreamSynchronize(cs);
+    (void)hipStreamSynchronize(side);
+    if (se != hipSuccess && rst == MSI_OK)
+        rst = fail(MSI_E_DEVICE, std::string("compute stream: ") + hipGetErrorString(se));
+
+    // ---- layer exit: observe this forward's fills, release consumers
+    for (const SchedRound &round : sched.rounds)
+        for (const FillRecord &f : round.fills) {
+            if (!core.fill(f.id))
+                continue;      // superseded by a later round of this forward
+            const uint32_t gs = core.global_slot(a->layer, f.slot);
+            if (p->fill_ev_id[gs] == f.id)
+                observe_fill(p, gs);
+            else
+                core.complete_fill(f.id);
+        }
+    for (const SchedRound &round : sched.rounds)
+        for (const SchedItem &si : round.items)
+            p->release_ev[core.global_slot(a->layer, uint32_t(si.slot))] = nullptr;
+    for (hipEvent_t e : round_events)
+        p->free_events.push_back(e);
+    core.end_forward(a->layer, sched);
+    if (rst != MSI_OK)
+        return rst;
+    if (*p->status_host & STATUS_STALE) {
+        core.stats().stale_detected++;
+        return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
+    }
+    return MSI_OK;
+}
+
+msi_status msi_slot_hold(msi_plan *p, uint32_t layer, uint32_t slot)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    const msi_status st = p->core->hold(layer, slot);
+    return st == MSI_OK ? st : fail(st, p->core->error());
+}
+
+msi_status msi_slot_unhold(msi_plan *p, uint32_t layer, uint32_t slot)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    const msi_status st = p->core->unhold(layer, slot);
+    return st == MSI_OK ? st : fail(st, p->core->error());
+}
+
+msi_status msi_slot_query(const msi_plan *p, uint32_t layer, uint32_t slot, msi_slot_info *info)
+{
+    if (!p || !info)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    if (layer >= p->core->n_layers() || slot >= p->core->pool_slots())
+        return fail(MSI_E_INVALID_ARG, "layer or slot out of range");
+    const Slot &s = p->core->slot(layer, slot);
+    *info = msi_slot_info{uint32_t(s.state), s.expert, s.gen, s.epoch, s.consumers + s.holds, s.holds, s.last_use};
+    return MSI_OK;
+}
+
+msi_status msi_plan_stats(const msi_plan *p, msi_stats *st)
+{
+    if (!p || !st)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    *st = p->core->stats();
+    st->fills_in_flight = p->core->fills_in_flight();
+    st->windows_busy = p->core->windows_busy();
+    st->consumers_live = p->core->consumers_live();
+    st->epoch = p->core->epoch();
+    return MSI_OK;
+}
+
+msi_status msi_debug_set_device_gen(msi_plan *p, uint32_t layer, uint32_t slot, uint32_t gen)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    if (layer >= p->core->n_layers() || slot >= p->core->pool_slots())
+        return fail(MSI_E_INVALID_ARG, "layer or slot out of range");
+    HIP_OK(hipSetDevice(p->device));
+    HIP_OK(hipDeviceSynchronize());
+    HIP_OK(hipMemcpy(p->gen_dev + p->core->global_slot(layer, slot), &gen, sizeof(uint32_t), hipMemcpyHostToDevice));
+    return MSI_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,418 @@
+// plan_core.cpp -- residency planner: manifest checks, slot lifecycle,
+// generations and epochs, LRU / zero-cache policies, forward round schedule.
+// Section 3.1 (manifest and mutable state), Section 3.2 (extent rejection
+// conditions), Section 3.3 (stable slots, publication), Section 3.4 (state
+// sequences, tickets, reset), Section 4 (scheduling and copies).
+#include "plan_core.hpp"
+
+#include <algorithm>
+#include <limits>
+
+namespace msi {
+
+PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
+{
+    auto fail = [&](msi_status st, std::string m) { set_error(st, std::move(m)); };
+    if (d.abi_version != MSI_ABI_VERSION)
+        { fail(MSI_E_INVALID_ARG, "abi_version mismatch"); return; }
+    if (d.n_layers == 0 || d.n_experts == 0 || d.n_experts > 1024)
+        { fail(MSI_E_INVALID_ARG, "n_layers must be >= 1 and n_experts in [1, 1024]"); return; }
+    if (d.d_model == 0 || d.d_model % 256 != 0)
+        { fail(MSI_E_INVALID_ARG, "d_model must be a positive multiple of 256"); return; }
+    if (d.d_ff == 0 || d.d_ff % 128 != 0)
+        { fail(MSI_E_INVALID_ARG, "d_ff must be a positive multiple of 128"); return; }
+    if (d.top_k == 0 || d.top_k > d.n_experts || d.top_k > 16)
+        { fail(MSI_E_INVALID_ARG, "top_k must be in [1, min(n_experts, 16)]"); return; }
+    if (d.wdtype > MSI_W_Q4B32)
+        { fail(MSI_E_INVALID_ARG, "unknown wdtype"); return; }
+    zero_cache_ = d.slots_per_layer == 0;
+    pool_slots_ = zero_cache_ ? (d.transient_slots ? d.transient_slots : 8u) : d.slots_per_layer;
+    if (zero_cache_ && pool_slots_ < 2)
+        { fail(MSI_E_INVALID_ARG, "transient_slots must be >= 2"); return; }
+    if (d.slot_stride < object_bytes || d.slot_stride % 256 != 0)
+        { fail(MSI_E_INVALID_ARG, "slot_stride must be >= the object size and a multiple of 256"); return; }
+    if (!d.slot_pool || reinterpret_cast<uintptr_t>(d.slot_pool) % 256 != 0)
+        { fail(MSI_E_INVALID_ARG, "slot_pool must be non-null and 256-byte aligned"); return; }
+    const double need = double(d.n_layers) * pool_slots_ * double(d.slot_stride);
+    if (double(d.slot_pool_bytes) < need)
+        { fail(MSI_E_INVALID_ARG, "slot_pool_bytes smaller than n_layers * pool_slots * slot_stride"); return; }
+    if (d.n_windows == 0 || !d.windows || d.window_bytes == 0)
+        { fail(MSI_E_INVALID_ARG, "windows missing"); return; }
+    for (uint32_t w = 0; w < d.n_windows; ++w)
+        if (!d.windows[w])
+            { fail(MSI_E_INVALID_ARG, "null window " + std::to_string(w)); return; }
+    if (d.n_objects && !d.objects)
+        { fail(MSI_E_INVALID_ARG, "objects missing"); return; }
+
+    n_layers_ = d.n_layers;
+    n_experts_ = d.n_experts;
+    objects_.assign(size_t(n_layers_) * n_experts_, ObjectInfo{0, 0, 0});
+    has_object_.assign(size_t(n_layers_) * n_experts_, 0);
+    for (uint32_t i = 0; i < d.n_objects; ++i) {
+        const msi_object_desc &o = d.objects[i];
+        if (o.layer >= n_layers_ || o.expert >= n_experts_ || o.window >= d.n_windows)
+            { fail(MSI_E_INVALID_ARG, "object " + std::to_string(i) + ": layer/expert/window out of range"); return; }
+        if (o.nbytes != object_bytes)
+            { fail(MSI_E_SHORT, "object " + std::to_string(i) + ": extent length " +
+                                         std::to_string(o.nbytes) + " != object size " +
+                                         std::to_string(object_bytes)); return; }
+        if (o.offset > d.window_bytes || o.nbytes > d.window_bytes - o.offset)
+            { fail(MSI_E_SHORT, "object " + std::to_string(i) + ": extent runs past its window"); return; }
+        const size_t k = size_t(o.layer) * n_experts_ + o.expert;
+        if (has_object_[k])
+            { fail(MSI_E_INVALID_ARG, "duplicate object (layer " + std::to_string(o.layer) +
+                                               ", expert " + std::to_string(o.expert) + ")"); return; }
+        has_object_[k] = 1;
+        objects_[k] = ObjectInfo{o.window, o.offset, o.nbytes};
+    }
+    slots_.assign(size_t(n_layers_) * pool_slots_, Slot{});
+    window_busy_.assign(d.n_windows, 0);
+}
+
+const ObjectInfo *PlanCore::object(uint32_t layer, uint32_t expert) const
+{
+    if (layer >= n_layers_ || expert >= n_experts_)
+        return nullptr;
+    const size_t k = size_t(layer) * n_experts_ + expert;
+    return has_object_[k] ? &objects_[k] : nullptr;
+}
+
+const FillRecord *PlanCore::fill(int64_t id) const
+{
+    auto it = fills_.find(id);
+    return it == fills_.end() ? nullptr : &it->second;
+}
+
+int32_t PlanCore::resident_slot(uint32_t layer, uint32_t expert) const
+{
+    if (zero_cache_)
+        return -1;
+    for (uint32_t s = 0; s < pool_slots_; ++s) {
+        const Slot &sl = slot(layer, s);
+        if (sl.expert != int32_t(expert))
+            continue;
+        switch (sl.state) {
+        case SlotState::DeviceReady:
+        case SlotState::InUse:
+        case SlotState::Recyclable:
+            return int32_t(s);
+        case SlotState::Loading:
+            if (sl.epoch == epoch_)
+                return int32_t(s);   // usable once its ready event has completed
+            break;
+        default:
+            break;
+        }
+    }
+    return -1;
+}
+
+int32_t PlanCore::choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude) const
+{
+    int32_t best = -1;
+    uint64_t best_key = std::numeric_limits<uint64_t>::max();
+    for (uint32_t s = 0; s < pool_slots_; ++s) {
+        const Slot &sl = slot(layer, s);
+        if (sl.holds > 0 || (!exclude.empty() && exclude[s]))
+            continue;
+        const uint64_t key = sl.state == SlotState::Vacant ? 0 : sl.last_use + 1;
+        if (key < best_key) {
+            best_key = key;
+            best = int32_t(s);
+        }
+    }
+    return best;
+}
+
+int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
+{
+    Slot &sl = slot(layer, s);
+    if (sl.state != SlotState::Vacant && sl.expert >= 0)
+        stats_.evictions++;
+    if (sl.fill_id >= 0) {
+        // An earlier fill of this slot is superseded; the device layer orders
+        // the new copy after it.  Its version was either read by a round of
+        // this forward (published in stream order) or never visible.
+        auto it = fills_.find(sl.fill_id);
+        if (it != fills_.end() && !it->second.consumed)
+            stats_.fills_discarded++;
+        else
+            stats_.fills_published++;
+        if (it != fills_.end()) {
+            window_busy_[it->second.window]--;
+            fills_.erase(it);
+        }
+    }
+    const ObjectInfo &o = objects_[size_t(layer) * n_experts_ + expert];
+    FillRecord r;
+    r.id = next_fill_++;
+    r.layer = layer;
+    r.slot = s;
+    r.expert = expert;
+    r.gen = ++sl.gen;
+    r.epoch = epoch_;
+    r.window = o.window;
+    r.offset = o.offset;
+    r.nbytes = o.nbytes;
+    sl.expert = int32_t(expert);
+    sl.epoch = epoch_;
+    sl.state = SlotState::Loading;
+    sl.fill_id = r.id;
+    sl.last_use = ++tick_;
+    window_busy_[o.window]++;
+    stats_.fills++;
+    stats_.h2d_bytes += o.nbytes;
+    fills_.emplace(r.id, r);
+    return r.id;
+}
+
+void PlanCore::publish_state(Slot &sl)
+{
+    sl.state = (sl.consumers + sl.holds) > 0 ? SlotState::InUse : SlotState::DeviceReady;
+}
+
+msi_status PlanCore::request_fill(uint32_t layer, uint32_t expert, int32_t forced_slot, msi_ticket *t,
+                                  int64_t *fill_id)
+{
+    *fill_id = -1;
+    if (layer >= n_layers_) {
+        stats_.rejections++;
+        set_error(MSI_E_INVALID_ARG, "layer out of range");
+        return MSI_E_INVALID_ARG;
+    }
+    if (!object(layer, expert) || (forced_slot >= 0 && uint32_t(forced_slot) >= pool_slots_) ||
+        forced_slot < -1) {
+        stats_.rejections++;
+        set_error(MSI_E_WRONG_OBJECT, "object not in this layer's manifest or slot outside its pool");
+        return MSI_E_WRONG_OBJECT;
+    }
+    const int32_t r = resident_slot(layer, expert);
+    if (r >= 0 && (forced_slot < 0 || forced_slot == r)) {
+        Slot &sl = slot(layer, uint32_t(r));
+        sl.last_use = ++tick_;
+        stats_.hits++;
+        *t = msi_ticket{layer, expert, r, sl.gen, sl.epoch, 1u};
+        return MSI_OK;
+    }
+    int32_t s = forced_slot;
+    if (s >= 0) {
+        const Slot &sl = slot(layer, uint32_t(s));
+        if (sl.holds > 0 || sl.consumers > 0) {
+            stats_.rejections++;
+            set_error(MSI_E_BUSY, "slot has live consumers; reuse is delayed");
+            return MSI_E_BUSY;
+        }
+    } else {
+        s = choose_victim(layer, {});
+        if (s < 0) {
+            stats_.rejections++;
+            set_error(MSI_E_BUSY, "every slot of the layer has live consumers");
+            return MSI_E_BUSY;
+        }
+    }
+    // one version per object: forget an older copy held elsewhere (no consumers)
+    for (uint32_t o = 0; o < pool_slots_; ++o) {
+        Slot &sl = slot(layer, o);
+        if (int32_t(o) != s && sl.expert == int32_t(expert) && sl.holds == 0 && sl.consumers == 0 &&
+            sl.fill_id < 0) {
+            sl.state = SlotState::Vacant;
+            sl.expert = -1;
+        }
+    }
+    stats_.misses++;
+    *fill_id = new_fill(layer, uint32_t(s), expert);
+    const Slot &sl = slot(layer, uint32_t(s));
+    *t = msi_ticket{layer, expert, s, sl.gen, sl.epoch, 0u};
+    return MSI_OK;
+}
+
+void PlanCore::complete_fill(int64_t id)
+{
+    auto it = fills_.find(id);
+    if (it == fills_.end())
+        return;
+    const FillRecord rec = it->second;
+    fills_.erase(it);
+    window_busy_[rec.window]--;
+    Slot &sl = slot(rec.layer, rec.slot);
+    if (sl.fill_id != id)
+        return;
+    sl.fill_id = -1;
+    if (sl.state == SlotState::Loading && sl.gen == rec.gen && rec.epoch == epoch_) {
+        publish_state(sl);
+        stats_.fills_published++;
+    } else {
+        // the ticket's epoch or generation is no longer current: never visible
+        sl.state = SlotState::Vacant;
+        sl.expert = -1;
+        stats_.fills_discarded++;
+    }
+}
+
+msi_status PlanCore::schedule_forward(uint32_t layer, const std::vector<int32_t> &demanded, Schedule *out)
+{
+    out->rounds.clear();
+    if (layer >= n_layers_) {
+        set_error(MSI_E_INVALID_ARG, "layer out of range");
+        return MSI_E_INVALID_ARG;
+    }
+    std::vector<int32_t> hits, misses;
+    for (int32_t e : demanded) {
+        if (e < 0 || !object(layer, uint32_t(e))) {
+            stats_.rejections++;
+            set_error(MSI_E_WRONG_OBJECT, "demanded expert " + std::to_string(e) +
+                                              " has no object in layer " + std::to_string(layer));
+            return MSI_E_WRONG_OBJECT;
+        }
+        (resident_slot(layer, uint32_t(e)) >= 0 ? hits : misses).push_back(e);
+    }
+    uint32_t eligible = 0;
+    for (uint32_t s = 0; s < pool_slots_; ++s)
+        eligible += slot(layer, s).holds == 0;
+    if (!misses.empty() && eligible == 0) {
+        stats_.rejections++;
+        set_error(MSI_E_BUSY, "no slot of the layer can be freed (all held)");
+        return MSI_E_BUSY;
+    }
+    const size_t n = hits.size() + misses.size();
+    uint32_t R = n <= pool_slots_ ? pool_slots_ : std::max(1u, pool_slots_ / 2);
+    R = std::max(1u, std::min(R, eligible ? eligible : pool_slots_));
+
+    size_t hi = 0, mi = 0;
+    while (hi < hits.size() || mi < misses.size()) {
+        SchedRound round;
+        std::vector<uint8_t> exclude(pool_slots_, 0);
+        uint32_t taken = 0;      // eligible slots this round occupies
+        while (hi < hits.size()) {
+            const int32_t s = resident_slot(layer, uint32_t(hits[hi]));
+            const bool el = slot(layer, uint32_t(s)).holds == 0;
+            if (el && taken + 1 > R)
+                break;
+            exclude[s] = 1;
+            taken += el;
+            round.items.push_back(SchedItem{hits[hi], s, slot(layer, uint32_t(s)).gen});
+            stats_.hits++;
+            ++hi;
+        }
+        while (hi == hits.size() && mi < misses.size() && taken + 1 <= R) {
+            const int32_t v = choose_victim(layer, exclude);
+            if (v < 0)
+                break;
+            const uint32_t e = uint32_t(misses[mi]);
+            const int64_t id = new_fill(layer, uint32_t(v), e);
+            fills_[id].consumed = true;
+            exclude[v] = 1;
+            taken++;
+            round.fills.push_back(fills_[id]);
+            round.items.push_back(SchedItem{int32_t(e), v, slot(layer, uint32_t(v)).gen});
+            stats_.misses++;
+            ++mi;
+        }
+        if (round.items.empty()) {   // cannot happen with eligible > 0; guard the loop
+            set_error(MSI_E_BUSY, "scheduler made no progress");
+            return MSI_E_BUSY;
+        }
+        for (const SchedItem &it : round.items) {
+            Slot &sl = slot(layer, uint32_t(it.slot));
+            sl.consumers++;
+            sl.last_use = ++tick_;
+            if (sl.state != SlotState::Loading)
+                sl.state = SlotState::InUse;
+        }
+        stats_.rounds++;
+        out->rounds.push_back(std::move(round));
+    }
+    stats_.forwards++;
+    return MSI_OK;
+}
+
+void PlanCore::end_forward(uint32_t layer, const Schedule &s)
+{
+    for (const SchedRound &r : s.rounds)
+        for (const SchedItem &it : r.items) {
+            Slot &sl = slot(layer, uint32_t(it.slot));
+            if (sl.consumers)
+                sl.consumers--;
+            if (sl.consumers + sl.holds == 0 &&
+                (sl.state == SlotState::InUse || sl.state == SlotState::DeviceReady))
+                sl.state = SlotState::Recyclable;
+        }
+    if (zero_cache_)
+        for (uint32_t s2 = 0; s2 < pool_slots_; ++s2) {
+            Slot &sl = slot(layer, s2);
+            if (sl.holds == 0 && sl.consumers == 0 && sl.fill_id < 0) {
+                sl.state = SlotState::Vacant;
+                sl.expert = -1;
+            }
+        }
+}
+
+msi_status PlanCore::hold(uint32_t layer, uint32_t s)
+{
+    if (layer >= n_layers_ || s >= pool_slots_) {
+        set_error(MSI_E_INVALID_ARG, "layer or slot out of range");
+        return MSI_E_INVALID_ARG;
+    }
+    Slot &sl = slot(layer, s);
+    sl.holds++;
+    if (sl.state == SlotState::DeviceReady || sl.state == SlotState::Recyclable)
+        sl.state = SlotState::InUse;
+    return MSI_OK;
+}
+
+msi_status PlanCore::unhold(uint32_t layer, uint32_t s)
+{
+    if (layer >= n_layers_ || s >= pool_slots_) {
+        set_error(MSI_E_INVALID_ARG, "layer or slot out of range");
+        return MSI_E_INVALID_ARG;
+    }
+    Slot &sl = slot(layer, s);
+    if (sl.holds == 0) {
+        stats_.rejections++;
+        set_error(MSI_E_STATE, "slot has no held consumer");
+        return MSI_E_STATE;
+    }
+    sl.holds--;
+    if (sl.holds + sl.consumers == 0 && sl.state == SlotState::InUse)
+        sl.state = SlotState::Recyclable;
+    return MSI_OK;
+}
+
+bool PlanCore::any_holds() const
+{
+    for (const Slot &s : slots_)
+        if (s.holds)
+            return true;
+    return false;
+}
+
+msi_status PlanCore::reset()
+{
+    if (any_holds()) {
+        stats_.rejections++;
+        set_error(MSI_E_BUSY, "reset with a live held consumer");
+        return MSI_E_BUSY;
+    }
+    epoch_++;
+    return MSI_OK;
+}
+
+uint64_t PlanCore::fills_in_flight() const { return fills_.size(); }
+
+uint64_t PlanCore::windows_busy() const
+{
+    uint64_t n = 0;
+    for (uint32_t b : window_busy_)
+        n += b > 0;
+    return n;
+}
+
+uint64_t PlanCore::consumers_live() const
+{
+    uint64_t n = 0;
+    for (const Slot &s : slots_)
+        n += s.consumers + s.holds;
+    return n;
+}
+
+}  // namespace msi

@@ -1,0 +1,149 @@
+// plan_core.hpp -- host-side residency planner of the slot-backed MoE layer.
+//
+// Pure C++17, no HIP: the HIP layer (msi_abi.cpp) owns events, streams and
+// device memory and drives this class with explicit calls.  It holds the
+// immutable manifest and the mutable per-slot / per-window state of the
+// paper's Plan (Section 3.1: object, generation, request epoch, readiness,
+// live-consumer count; replacement policy kept apart from the lifecycle) and
+// the GPU-slot state sequence Vacant -> Loading -> DeviceReady -> InUse ->
+// Recyclable -> Vacant of Section 3.4, with tickets carrying object,
+// generation, epoch and slot.  Host windows are caller-owned pinned buffers
+// that always hold their extents, so of the window sequence only
+// HostReady <-> Copying is tracked (a window is busy while a copy reads it).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/msi.h"
+
+namespace msi {
+
+enum class SlotState : uint32_t {
+    Vacant = MSI_SLOT_VACANT,
+    Loading = MSI_SLOT_LOADING,
+    DeviceReady = MSI_SLOT_DEVICE_READY,
+    InUse = MSI_SLOT_IN_USE,
+    Recyclable = MSI_SLOT_RECYCLABLE,
+};
+
+struct Slot {
+    SlotState state = SlotState::Vacant;
+    int32_t expert = -1;       // object currently denoted (or being loaded)
+    uint32_t gen = 0;          // generation of that version; bumps on every fill
+    uint32_t epoch = 0;        // epoch of the fill that produced it
+    uint32_t consumers = 0;    // live consumers from forward rounds
+    uint32_t holds = 0;        // consumers held through the API
+    uint64_t last_use = 0;     // LRU tick
+    int64_t fill_id = -1;      // unobserved fill targeting this slot, -1 if none
+};
+
+struct FillRecord {
+    int64_t id = -1;
+    uint32_t layer = 0, slot = 0, expert = 0, gen = 0, epoch = 0, window = 0;
+    uint64_t offset = 0, nbytes = 0;
+    bool consumed = false;     // a forward round reads this version (stream-ordered)
+};
+
+struct SchedItem {
+    int32_t expert;
+    int32_t slot;      // index within the layer's pool
+    uint32_t gen;      // generation the kernels must see
+};
+
+struct SchedRound {
+    std::vector<SchedItem> items;     // ascending by position in the demand order
+    std::vector<FillRecord> fills;    // copies of the fills submitted for this round
+                                      // (a later round may supersede the core's record)
+};
+
+struct Schedule {
+    std::vector<SchedRound> rounds;
+};
+
+struct ObjectInfo {
+    uint32_t window;
+    uint64_t offset, nbytes;
+};
+
+class PlanCore {
+public:
+    // Validates the manifest; on failure status() != MSI_OK and error() says why.
+    PlanCore(const msi_plan_desc &d, uint64_t object_bytes);
+
+    msi_status status() const { return status_; }
+    const std::string &error() const { return err_; }
+
+    uint32_t n_layers() const { return n_layers_; }
+    uint32_t n_experts() const { return n_experts_; }
+    uint32_t pool_slots() const { return pool_slots_; }
+    bool zero_cache() const { return zero_cache_; }
+    uint32_t epoch() const { return epoch_; }
+    const msi_stats &stats() const { return stats_; }
+    msi_stats &stats() { return stats_; }
+
+    const Slot &slot(uint32_t layer, uint32_t s) const { return slots_[layer * pool_slots_ + s]; }
+    Slot &slot(uint32_t layer, uint32_t s) { return slots_[layer * pool_slots_ + s]; }
+    uint32_t global_slot(uint32_t layer, uint32_t s) const { return layer * pool_slots_ + s; }
+    const ObjectInfo *object(uint32_t layer, uint32_t expert) const;
+    const FillRecord *fill(int64_t id) const;
+
+    // Slot holding a published (or same-epoch loading) version of the object,
+    // usable as a hit; -1 if none.  Zero-cache plans never report hits.
+    int32_t resident_slot(uint32_t layer, uint32_t expert) const;
+
+    // Least recently used slot of `layer` that has no holds and is not in
+    // `exclude` (one flag per pool slot); -1 if none.
+    int32_t choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude) const;
+
+    // Explicit fill (msi_slot_fill).  On MSI_OK *t is the ticket and, unless
+    // t->hit, *fill_id the new fill to submit.
+    msi_status request_fill(uint32_t layer, uint32_t expert, int32_t forced_slot, msi_ticket *t,
+                            int64_t *fill_id);
+
+    // Completion of a submitted fill observed by the device layer.
+    void complete_fill(int64_t fill_id);
+
+    // Resolve the demanded experts (ascending ids) of one forward into
+    // rounds: hits first, then misses in ascending id; rounds hold at most
+    // the pool size (half of it when there are several, so the next round's
+    // fills go to slots the current round does not read).  Submits the fills
+    // and takes one consumer per round item.  MSI_E_BUSY if no victim exists.
+    msi_status schedule_forward(uint32_t layer, const std::vector<int32_t> &demanded, Schedule *out);
+
+    // Drop the consumers a schedule took (after its kernels completed).
+    // Zero-cache plans then forget every object they loaded.
+    void end_forward(uint32_t layer, const Schedule &s);
+
+    msi_status hold(uint32_t layer, uint32_t s);
+    msi_status unhold(uint32_t layer, uint32_t s);
+    msi_status reset();                        // epoch++ (MSI_E_BUSY with holds)
+    bool any_holds() const;
+    uint64_t fills_in_flight() const;
+    uint64_t windows_busy() const;
+    uint64_t consumers_live() const;
+
+    void set_error(msi_status st, const std::string &msg) { status_ = st; err_ = msg; }
+
+private:
+    int64_t new_fill(uint32_t layer, uint32_t s, uint32_t expert);
+    void publish_state(Slot &sl);
+
+    msi_status status_ = MSI_OK;
+    std::string err_;
+    uint32_t n_layers_ = 0, n_experts_ = 0, pool_slots_ = 0;
+    bool zero_cache_ = false;
+    uint32_t epoch_ = 0;
+    uint64_t tick_ = 0;
+    std::vector<Slot> slots_;
+    std::vector<ObjectInfo> objects_;          // [layer * E + expert]
+    std::vector<uint8_t> has_object_;
+    std::vector<uint32_t> window_busy_;
+    std::unordered_map<int64_t, FillRecord> fills_;   // unobserved fills
+    int64_t next_fill_ = 0;
+    msi_stats stats_{};
+};
+
+}  // namespace msi

@@ -244,6 +244,18 @@ class LayerInputs:
             self.experts[e] = expert_object(self.wl, self.layer, e)
         return self.experts[e]
 
+    def prefetch(self, ids=None, threads: int = 0) -> "LayerInputs":
+        """Draw the listed expert objects (default all) on a thread pool."""
+        import concurrent.futures
+        import os
+        ids = range(len(self.experts)) if ids is None else ids
+        todo = [e for e in ids if self.experts[e] is None]
+        n = threads or min(16, os.cpu_count() or 1)
+        with concurrent.futures.ThreadPoolExecutor(n) as ex:
+            for e, obj in zip(todo, ex.map(lambda e: expert_object(self.wl, self.layer, e), todo)):
+                self.experts[e] = obj
+        return self
+
 
 def layer_inputs(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] = None,
                  lazy: bool = False, shape: Optional[LayerShape] = None) -> LayerInputs:
@@ -253,12 +265,12 @@ def layer_inputs(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] =
     if shape is not None:
         wl = dataclasses.replace(wl, shape=shape)
     s = wl.shape
-    experts = [None] * s.E if lazy else [expert_object(wl, layer, e) for e in range(s.E)]
-    return LayerInputs(
+    li = LayerInputs(
         wl=wl, layer=layer,
         x=hidden_states(wl, layer, step, T),
         wr=router_weight(wl, layer),
         bias=router_bias(wl, layer),
-        experts=experts,
+        experts=[None] * s.E,
         shared=expert_object(wl, layer, 0, shared=True) if s.shared else None,
     )
+    return li if lazy else li.prefetch()

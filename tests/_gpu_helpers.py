@@ -1,0 +1,129 @@
+"""Shared set-up of the GPU parity tests: inputs from ``synth`` copied into
+pinned windows and device tensors, one route + forward through the C ABI, and
+the comparison rules against the fp64 oracle."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+from typing import Optional, Sequence
+
+import numpy as np
+
+import synth
+
+NEAR_TIE = 1e-5          # oracle logit gap under which a different selection is accepted
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_device(a: np.ndarray, dtype: str):
+    import torch
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+@dataclasses.dataclass
+class DeviceLayer:
+    li: synth.LayerInputs
+    x: object
+    wr: object
+    bias: Optional[object]
+    shared: Optional[object]
+
+
+def device_layer(li: synth.LayerInputs) -> DeviceLayer:
+    import torch
+    s = li.wl.shape
+    return DeviceLayer(
+        li=li, x=to_device(li.x, s.xdtype), wr=to_device(li.wr, s.xdtype),
+        bias=None if li.bias is None else torch.from_numpy(li.bias).cuda(),
+        shared=None if li.shared is None else torch.from_numpy(li.shared).cuda())
+
+
+def make_plan(li: synth.LayerInputs, capacity: int, transient: int = 8, per_window: int = 8,
+              experts: Optional[Sequence[int]] = None):
+    """Plan over one layer whose objects sit in pinned windows of
+    ``per_window`` experts.  ``experts`` restricts the manifest."""
+    import paper_2608_23805_amd as msi
+    s = li.wl.shape
+    ids = list(range(s.E)) if experts is None else list(experts)
+    wins, entries = msi.pack_windows([li.expert(e) for e in ids], per_window, layer=0, expert_ids=ids)
+    return msi.Plan(n_layers=1, n_experts=s.E, d_model=s.d, d_ff=s.I, top_k=s.K, wdtype=s.wdtype,
+                    slots_per_layer=capacity, transient_slots=transient if capacity == 0 else 0,
+                    windows=wins, objects=entries)
+
+
+def run_layer(plan, dl: DeviceLayer, T: Optional[int] = None, compute=None, side=None, out=None,
+              check=True):
+    """route + forward; returns host copies of every output and the status."""
+    import torch
+    import paper_2608_23805_amd as msi
+    s = dl.li.wl.shape
+    T = s.T if T is None else T
+    x = dl.x[:T]
+    r = msi.Routing.alloc(T, s.K, s.E)
+    ws = plan.workspace(T)
+    if out is None:
+        out = torch.empty((T, s.d), dtype=torch.float32, device="cuda")
+    compute = compute or torch.cuda.current_stream()
+    side = side or torch.cuda.Stream()
+    plan.route(x, dl.wr, dl.bias, r, ws, compute)
+    st = plan.forward_status(0, x, r, dl.shared, out, ws, compute, side)
+    torch.cuda.synchronize()
+    if check and st != 0:
+        raise msi.MsiError(st, msi.last_error())
+    L = ws[: T * s.E * 4].view(torch.float32).view(T, s.E)
+    return {"status": st, "out": out, "idx": r.idx.cpu().numpy(), "w": r.weights.cpu().numpy(),
+            "counts": r.counts.cpu().numpy(), "offsets": r.offsets.cpu().numpy(),
+            "perm": r.perm.cpu().numpy(), "inv": r.inv.cpu().numpy(),
+            "row_weight": r.row_weight.cpu().numpy(), "logits": L.cpu().numpy(), "routing": r}
+
+
+def check_selection(gpu_idx: np.ndarray, ora: dict, tokens: Sequence[int]):
+    """Selected sets must match exactly, except on tokens whose oracle top-K
+    gap is below NEAR_TIE, where every differing expert must lie within
+    NEAR_TIE of the K-th oracle logit.  Returns the list of accepted
+    near-tie tokens."""
+    near = []
+    L = ora["logits"]
+    for j, t in enumerate(tokens):
+        g = np.sort(gpu_idx[t])
+        o = ora["idx"][j]
+        if np.array_equal(g, o):
+            continue
+        kth = np.sort(L[j])[::-1][len(o) - 1]
+        diff = set(g.tolist()) ^ set(o.tolist())
+        ok = ora["gap"][j] < NEAR_TIE and all(abs(L[j][e] - kth) < NEAR_TIE for e in diff)
+        assert ok, f"token {t}: gpu {g} oracle {o} gap {ora['gap'][j]:.3e}"
+        near.append(t)
+    return near
+
+
+def rel_err(a: np.ndarray, ref: np.ndarray) -> float:
+    den = float(np.abs(ref).max())
+    return float(np.abs(np.asarray(a, np.float64) - ref).max() / (den if den > 0 else 1.0))
+
+
+def oracle_compare(o, li: synth.LayerInputs, res: dict, tokens: Sequence[int], tol: float):
+    """Oracle on ``tokens``; near-tie tokens are recomputed with the GPU's set.
+    Returns (err, near_tie_tokens)."""
+    s = li.wl.shape
+    experts = [li.expert(e) for e in range(s.E)]
+    ora = o.moe_layer(li.x, li.wr, li.bias, experts, li.shared, s.K, s.I, s.wdtype, s.xdtype,
+                      tokens=tokens, want_logits=True)
+    near = check_selection(res["idx"], ora, tokens)
+    ref = ora["out"].copy()
+    if near:
+        pos = [list(tokens).index(t) for t in near]
+        forced = np.sort(res["idx"][near], axis=1)
+        r2 = o.moe_layer(li.x, li.wr, li.bias, experts, li.shared, s.K, s.I, s.wdtype, s.xdtype,
+                         tokens=near, forced_idx=forced)
+        ref[pos] = r2["out"]
+    got = res["out"].cpu().numpy()[list(tokens)]
+    err = rel_err(got, ref)
+    assert err <= tol, f"max-abs/max|ref| {err:.3e} > {tol:.1e}"
+    return err, near, ora

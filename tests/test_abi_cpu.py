@@ -1,0 +1,91 @@
+"""The C ABI library loads without a GPU, exports every symbol the header
+declares, and rejects malformed manifests before touching the device
+(extent past its window, extent length disagreeing with the object size,
+duplicate objects, bad shapes): the rejection conditions of the paper's
+bounded source service and manifest (Section 3.1, Section 3.2)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "msi.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:msi_status|const char \*|uint32_t)\s*(msi_\w+)\s*\(", src, re.M)))
+
+
+def test_header_matches_binding_exports():
+    import paper_2608_23805_amd as msi
+    assert sorted(msi.EXPORTS) == _header_functions()
+
+
+def test_library_exports_every_symbol():
+    import paper_2608_23805_amd as msi
+    lib = ctypes.CDLL(msi.LIB_PATH)
+    for name in _header_functions():
+        assert hasattr(lib, name), name
+    assert msi.lib.msi_abi_version() == msi.MSI_ABI_VERSION
+
+
+def _desc(msi, **over):
+    """A small valid-looking manifest whose pool pointer is never dereferenced
+    (creation fails during validation)."""
+    d, I, E = 256, 128, 4
+    ob = msi.object_nbytes(d, I, "bf16")
+    win = (ctypes.c_uint8 * (4 * ob))()
+    wins = (ctypes.c_void_p * 1)(ctypes.addressof(win))
+    objs = over.pop("objects", [(0, e, 0, e * ob, ob) for e in range(E)])
+    arr = (msi.msi_object_desc * len(objs))(*[msi.msi_object_desc(l, e, w, 0, o, n) for l, e, w, o, n in objs])
+    kw = dict(abi_version=msi.MSI_ABI_VERSION, n_layers=1, n_experts=E, d_model=d, d_ff=I, top_k=2,
+              wdtype=msi.MSI_W_BF16, slots_per_layer=2, transient_slots=0, reserved0=0,
+              slot_pool=1 << 20, slot_pool_bytes=2 * ob + 4096, slot_stride=(ob + 255) // 256 * 256,
+              windows=ctypes.cast(wins, ctypes.POINTER(ctypes.c_void_p)), n_windows=1, n_objects=len(objs),
+              window_bytes=4 * ob, objects=ctypes.cast(arr, ctypes.POINTER(msi.msi_object_desc)))
+    kw.update(over)
+    return msi.msi_plan_desc(**kw), (win, wins, arr), ob
+
+
+def _create(msi, **over):
+    desc, keep, ob = _desc(msi, **over)
+    h = ctypes.c_void_p()
+    st = msi.lib.msi_plan_create(ctypes.byref(desc), ctypes.byref(h))
+    return st, msi.last_error()
+
+
+@pytest.mark.parametrize("case,status,fragment", [
+    ("extent_past_window", -2, "past its window"),
+    ("short_extent", -2, "extent length"),
+    ("duplicate", -1, "duplicate"),
+    ("bad_topk", -1, "top_k"),
+    ("bad_d", -1, "d_model"),
+    ("bad_stride", -1, "slot_stride"),
+    ("bad_version", -1, "abi_version"),
+    ("window_index", -1, "out of range"),
+])
+def test_manifest_rejections(case, status, fragment):
+    import paper_2608_23805_amd as msi
+    ob = msi.object_nbytes(256, 128, "bf16")
+    over = {
+        "extent_past_window": dict(objects=[(0, 0, 0, 3 * ob + 16, ob)]),
+        "short_extent": dict(objects=[(0, 0, 0, 0, ob - 2)]),
+        "duplicate": dict(objects=[(0, 1, 0, 0, ob), (0, 1, 0, ob, ob)]),
+        "bad_topk": dict(top_k=5),
+        "bad_d": dict(d_model=200),
+        "bad_stride": dict(slot_stride=1000),
+        "bad_version": dict(abi_version=99),
+        "window_index": dict(objects=[(0, 0, 3, 0, ob)]),
+    }[case]
+    st, err = _create(msi, **over)
+    assert st == status and fragment in err, (st, err)
+
+
+def test_null_arguments():
+    import paper_2608_23805_amd as msi
+    assert msi.lib.msi_plan_create(None, None) == msi.MSI_E_INVALID_ARG
+    assert msi.lib.msi_route(None, None, None) == msi.MSI_E_INVALID_ARG
+    assert msi.lib.msi_moe_forward(None, None, None, None) == msi.MSI_E_INVALID_ARG
+    assert msi.lib.msi_plan_destroy(None) == msi.MSI_OK
+    assert msi.stream_threshold() == 16
