@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Throughput of the slot-backed routed-expert MoE layer on one MI355X.
+
+One step = one pass of the whole hot path over one batch: router logits,
+top-K and restricted softmax, permutation, residency resolution (device-to-
+host read of the per-expert counts, hits / misses / rounds), slot fills for
+misses, the routed-expert gate/up and down projections, the shared expert,
+and the fail-closed combine with its status read.
+
+Headline (decode): T = 16 tokens, d = 2048, E = 512, top-10 + 1 shared
+expert, intermediate 512, bf16 weights, fp32 router; all demanded experts
+resident (512 slots), fresh hidden states each step (16 seeded batches in
+rotation).  Secondary objects: the same decode with a 64-slot LRU pool
+(fills over PCIe inside the step), and prefill T = 32768 with a
+Dirichlet(0.3) router bias.  Every input is synthetic and seeded.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+METRIC = "routed tokens/sec per MoE layer (decode T=16, prefill T=32K); % HBM / MFMA peak"
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _setup(wl, capacity, T=None, n_batches=1):
+    import torch
+    import synth
+    import paper_2608_23805_amd as msi
+    from _gpu_helpers import to_device
+    s = wl.shape
+    T = s.T if T is None else T
+    t0 = time.time()
+    li = synth.layer_inputs(wl)
+    wins, entries = msi.pack_windows([li.expert(e) for e in range(s.E)], 8, layer=0)
+    plan = msi.Plan(n_layers=1, n_experts=s.E, d_model=s.d, d_ff=s.I, top_k=s.K, wdtype=s.wdtype,
+                    slots_per_layer=capacity, transient_slots=8 if capacity == 0 else 0,
+                    windows=wins, objects=entries)
+    xs = [to_device(synth.hidden_states(wl, 0, step, T), s.xdtype) for step in range(n_batches)]
+    dev = dict(wr=to_device(li.wr, s.xdtype),
+               bias=None if li.bias is None else torch.from_numpy(li.bias).cuda(),
+               shared=torch.from_numpy(li.shared).cuda())
+    r = msi.Routing.alloc(T, s.K, s.E)
+    ws = plan.workspace(T)
+    out = torch.empty((T, s.d), dtype=torch.float32, device="cuda")
+    log(f"[bench] {wl.name}: set up in {time.time() - t0:.1f}s (capacity {capacity}, T {T})")
+    return li, plan, xs, dev, r, ws, out
+
+
+def _run(plan, xs, dev, r, ws, out, steps, warmup, cs, side, on_step=None):
+    """warmup + timed steps; returns ms per step of the timed region."""
+    import torch
+
+    def step(i):
+        x = xs[i % len(xs)]
+        plan.route(x, dev["wr"], dev["bias"], r, ws, cs)
+        plan.forward(0, x, r, dev["shared"], out, ws, cs, side)
+        if on_step is not None:
+            on_step(i)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    plan.timings(reset=True)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(warmup + i)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / max(steps, 1)
+
+
+def bench_decode(args, cs, side):
+    import synth
+    wl = synth.WORKLOADS["decode_bf16"]
+    s = wl.shape
+    li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=16)
+    # warm-up fills every expert the rotation demands; the timed region then runs all-resident
+    plan.set_timing(True)
+    _run(plan, xs, dev, r, ws, out, 0, args.warmup, cs, side)
+    ms = _run(plan, xs, dev, r, ws, out, args.steps, 0, cs, side)
+    t = plan.timings()
+    st = plan.stats()
+    # algorithmic bytes of each step's routed gate/up launch (one round): the
+    # demanded experts' Wg and Wu once, their tokens' x rows once, act written
+    # once; the down launch reads Wd and act once and writes fp32 rows once
+    bytes_b, down_b = [], []
+    for b in range(len(xs)):
+        plan.route(xs[b], dev["wr"], dev["bias"], r, ws, cs)
+        c = r.counts.cpu().numpy()
+        dem = c[c > 0]
+        bytes_b.append(len(dem) * 2 * s.I * s.d * 2 + int(dem.sum()) * (s.d * 2 + s.I * 2))
+        down_b.append(len(dem) * s.d * s.I * 2 + int(dem.sum()) * (s.I * 2 + s.d * 4))
+    per_step_bytes = [bytes_b[i % len(xs)] for i in range(args.steps)]
+    per_step_down = [down_b[i % len(xs)] for i in range(args.steps)]
+    n_gu, ms_gu = t["gateup_stream"]
+    n_dn, ms_dn = t["down_stream"]
+    avg_gu = ms_gu / max(n_gu, 1)
+    avg_dn = ms_dn / max(n_dn, 1)
+    bytes_gu = sum(per_step_bytes) / max(len(per_step_bytes), 1)
+    bytes_dn = sum(per_step_down) / max(len(per_step_down), 1)
+    achieved = bytes_gu / (avg_gu * 1e-3) / 1e9
+    kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 2)} for k, (n, v) in t.items() if n}
+    plan.close()
+    res = dict(ms=ms, T=s.T, tokens_per_s=s.T / (ms * 1e-3), kernels=kernels,
+               roofline={"bound": "hbm", "kernel": "stream_gateup_kernel", "achieved": round(achieved, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                         "traffic": None, "bytes_per_launch": int(bytes_gu), "avg_launch_us": round(avg_gu * 1e3, 2)},
+               down={"achieved_GBs": round(bytes_dn / (avg_dn * 1e-3) / 1e9, 1), "avg_launch_us": round(avg_dn * 1e3, 2)},
+               stats={k: st[k] for k in ("fills", "hits", "misses", "rounds")})
+    log(f"[bench] decode: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s, gate/up {avg_gu * 1e3:.1f} us "
+        f"= {achieved:.0f} GB/s, down {avg_dn * 1e3:.1f} us")
+    return res, li
+
+
+def bench_decode_lru(args, cs, side):
+    import synth
+    wl = synth.WORKLOADS["decode_bf16"]
+    li, plan, xs, dev, r, ws, out = _setup(wl, capacity=64, n_batches=16)
+    ms = _run(plan, xs, dev, r, ws, out, args.lru_steps, 4, cs, side)
+    st = plan.stats()
+    plan.close()
+    res = dict(ms=round(ms, 3), tokens_per_s=round(wl.shape.T / (ms * 1e-3), 1), slots_per_layer=64,
+               fills_per_step=round(st["fills"] / (args.lru_steps + 4), 1),
+               h2d_GBs=round(st["h2d_bytes"] / (args.lru_steps + 4) / (ms * 1e-3) / 1e9, 1))
+    log(f"[bench] decode LRU64: {ms:.2f} ms/step, {res['tokens_per_s']:.0f} tok/s")
+    return res
+
+
+def bench_prefill(args, cs, side):
+    import synth
+    wl = synth.WORKLOADS["prefill_bf16"]
+    s = wl.shape
+    li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=1)
+    plan.set_timing(True)
+    ms = _run(plan, xs, dev, r, ws, out, args.prefill_steps, 2, cs, side)
+    t = plan.timings()
+    n_gu, ms_gu = t["gateup_tile"]
+    avg_gu = ms_gu / max(n_gu, 1)
+    c = r.counts.cpu().numpy()
+    rows_tile = int(c[c > 16].sum())          # rows taken by the tiled path (the rest stream)
+    flops_gu = 2.0 * rows_tile * s.d * 2 * s.I
+    layer_flops = 2.0 * s.T * (s.K * 3 * s.d * s.I + 3 * s.d * s.I + s.d * s.E)
+    achieved = flops_gu / (avg_gu * 1e-3) / 1e12
+    kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 1)} for k, (n, v) in t.items() if n}
+    plan.close()
+    res = dict(value=round(s.T / (ms * 1e-3), 1), unit="routed tokens/s per layer", ms_per_step=round(ms, 3),
+               T=s.T, layer_tflops=round(layer_flops / (ms * 1e-3) / 1e12, 1),
+               layer_mfma_frac=round(layer_flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+               roofline={"bound": "mfma", "kernel": "tile_gemm_kernel<GateUp>", "achieved": round(achieved, 1),
+                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                         "flops_per_launch": flops_gu, "avg_launch_us": round(avg_gu * 1e3, 1)},
+               kernels=kernels)
+    log(f"[bench] prefill: {ms:.3f} ms/step, {res['value']:.0f} tok/s, layer {res['layer_tflops']} TFLOP/s, "
+        f"gate/up {avg_gu * 1e3:.0f} us = {achieved:.0f} TFLOP/s")
+    return res
+
+
+def cpu_baseline(li, budget_s):
+    """The fp64 oracle, as it stands, on the decode batch 0 (16 tokens), repeated
+    until about budget_s seconds of wall time."""
+    import oracle
+    s = li.wl.shape
+    o = oracle.Oracle()
+    experts = [li.expert(e) for e in range(s.E)]
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        o.moe_layer(li.x, li.wr, li.bias, experts, li.shared, s.K, s.I, s.wdtype, s.xdtype)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {"value": round(reps * s.T / el, 2), "unit": "routed tokens/s per layer", "cores": o.max_threads(),
+            "kind": "oracle", "sample": f"decode layer T=16 (one seeded batch), {reps} repetitions, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--prefill-steps", type=int, default=10)
+    ap.add_argument("--lru-steps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    skip = set(filter(None, args.skip.split(",")))
+    import torch
+    torch.cuda.set_device(0)
+    cs = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+
+    dec, li = bench_decode(args, cs, side)
+    extra = {}
+    if "lru" not in skip:
+        extra["decode_lru64"] = bench_decode_lru(args, cs, side)
+    if "prefill" not in skip:
+        extra["prefill"] = bench_prefill(args, cs, side)
+    cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds)
+
+    s = li.wl.shape
+    line = {
+        "metric": METRIC, "value": round(dec["tokens_per_s"], 1), "unit": "routed tokens/s per layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dec["ms"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "decode_bf16 (Qwen3-Next-shaped MoE layer, all demanded experts resident)",
+                   "T": s.T, "d": s.d, "E": s.E, "top_k": s.K, "d_ff": s.I, "shared_experts": 1,
+                   "slots_per_layer": 512, "batches_in_rotation": 16},
+        "roofline": dec["roofline"], "cpu_baseline": cpu,
+        "kernels": dec["kernels"], "down": dec["down"],
+    }
+    line.update(extra)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -194,6 +194,27 @@ typedef struct {
     uint32_t reserved;
 } msi_stats;
 
+/* Kernel kinds of the per-kind timing telemetry. */
+typedef enum {
+    MSI_K_ROUTER_LOGITS = 0,
+    MSI_K_TOPK = 1,
+    MSI_K_PERMUTE = 2,
+    MSI_K_GATEUP_TILE = 3,     /* routed experts, tiled MFMA path                 */
+    MSI_K_GATEUP_STREAM = 4,   /* routed experts, weight-streaming path           */
+    MSI_K_DOWN_TILE = 5,
+    MSI_K_DOWN_STREAM = 6,
+    MSI_K_EXPERT_F32 = 7,      /* fp32 layers, gate/up and down                   */
+    MSI_K_SHARED = 8,          /* shared expert, gate/up and down                 */
+    MSI_K_COMBINE = 9,
+    MSI_K_FILL = 10,           /* one batch of slot fills on the side stream      */
+    MSI_NKERN = 11
+} msi_kernel_kind;
+
+typedef struct {
+    uint64_t launches[MSI_NKERN];
+    double ms[MSI_NKERN];       /* summed device time between events around each launch */
+} msi_timings;
+
 /* Text of the last error on this thread ("" if none).  Never NULL. */
 const char *msi_last_error(void);
 
@@ -268,6 +289,13 @@ msi_status msi_slot_unhold(msi_plan *plan, uint32_t layer, uint32_t slot);
 
 msi_status msi_slot_query(const msi_plan *plan, uint32_t layer, uint32_t slot, msi_slot_info *info);
 msi_status msi_plan_stats(const msi_plan *plan, msi_stats *stats);
+
+/* Telemetry: when enabled, every kernel launch of route/forward/fill on this
+ * plan is bracketed by two HIP events on its own stream; msi_plan_timings
+ * waits for the recorded events, accumulates the elapsed times per kernel
+ * kind into *out and, if reset != 0, clears the accumulators. */
+msi_status msi_plan_set_timing(msi_plan *plan, int enable);
+msi_status msi_plan_timings(msi_plan *plan, msi_timings *out, int reset);
 
 /* Test hook: overwrite one slot's device generation word (synchronously). */
 msi_status msi_debug_set_device_gen(msi_plan *plan, uint32_t layer, uint32_t slot, uint32_t gen);

@@ -83,7 +83,15 @@ class msi_stats(ctypes.Structure):
                                     "consumers_live")] + [("epoch", _u32), ("reserved", _u32)]
 
 
-EXPORTS = ["msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy", "msi_plan_reset",
+KERNEL_KINDS = ["router_logits", "topk", "permute", "gateup_tile", "gateup_stream", "down_tile",
+                "down_stream", "expert_f32", "shared", "combine", "fill"]
+
+
+class msi_timings(ctypes.Structure):
+    _fields_ = [("launches", _u64 * len(KERNEL_KINDS)), ("ms", ctypes.c_double * len(KERNEL_KINDS))]
+
+
+EXPORTS = ["msi_plan_set_timing", "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy", "msi_plan_reset",
            "msi_workspace_size", "msi_slot_fill", "msi_plan_poll", "msi_route", "msi_moe_forward",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
            "msi_debug_set_device_gen", "msi_stream_threshold"]
@@ -115,6 +123,8 @@ def _load():
     L.msi_slot_query.argtypes = [_vp, _u32, _u32, P(msi_slot_info)]
     L.msi_plan_stats.argtypes = [_vp, P(msi_stats)]
     L.msi_debug_set_device_gen.argtypes = [_vp, _u32, _u32, _u32]
+    L.msi_plan_set_timing.argtypes = [_vp, ctypes.c_int]
+    L.msi_plan_timings.argtypes = [_vp, P(msi_timings), ctypes.c_int]
     L.msi_stream_threshold.argtypes = [_u32]
     L.msi_stream_threshold.restype = _u32
     for n in EXPORTS:
@@ -304,6 +314,15 @@ class Plan:
         s = msi_stats()
         _check(lib.msi_plan_stats(self.h, ctypes.byref(s)))
         return {n: getattr(s, n) for n, _ in msi_stats._fields_ if n != "reserved"}
+
+    def set_timing(self, enable: bool):
+        _check(lib.msi_plan_set_timing(self.h, int(bool(enable))))
+
+    def timings(self, reset: bool = False) -> dict:
+        """{kind: (launches, total_ms)} of the timing telemetry."""
+        t = msi_timings()
+        _check(lib.msi_plan_timings(self.h, ctypes.byref(t), int(bool(reset))))
+        return {k: (int(t.launches[i]), float(t.ms[i])) for i, k in enumerate(KERNEL_KINDS)}
 
     def debug_set_device_gen(self, layer: int, slot: int, gen: int):
         _check(lib.msi_debug_set_device_gen(self.h, layer, slot, gen))

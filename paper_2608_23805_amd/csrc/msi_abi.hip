@@ -103,6 +103,62 @@ struct msi_plan {
     std::vector<int64_t> fill_ev_id;    // fill id the pending event completes
     std::vector<hipEvent_t> release_ev; // per global slot: last round reading it (current forward)
     std::vector<uint8_t> fill_ev_shared;// event shared by a round batch (not owned per slot)
+    // timing telemetry
+    struct Timed {
+        int kind;
+        hipEvent_t a, b;
+    };
+    bool timing = false;
+    std::vector<Timed> timed;
+    std::vector<hipEvent_t> tfree;
+    uint64_t t_launches[MSI_NKERN] = {};
+    double t_ms[MSI_NKERN] = {};
+
+    hipEvent_t get_tevent()
+    {
+        if (tfree.empty()) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess)
+                return nullptr;
+            all_events.push_back(e);
+            return e;
+        }
+        hipEvent_t e = tfree.back();
+        tfree.pop_back();
+        return e;
+    }
+
+    // Run `launch` bracketed by timing events on `s` when telemetry is on.
+    template <typename F>
+    hipError_t timed_launch(int kind, hipStream_t s, F &&launch)
+    {
+        if (!timing)
+            return launch();
+        hipEvent_t a = get_tevent(), b = get_tevent();
+        if (!a || !b)
+            return hipErrorOutOfMemory;
+        hipError_t e = hipEventRecord(a, s);
+        if (e == hipSuccess)
+            e = launch();
+        if (e == hipSuccess)
+            e = hipEventRecord(b, s);
+        timed.push_back(Timed{kind, a, b});
+        return e;
+    }
+
+    void resolve_timings()
+    {
+        for (const Timed &t : timed) {
+            float ms = 0.f;
+            if (hipEventSynchronize(t.b) == hipSuccess && hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
+                t_launches[t.kind]++;
+                t_ms[t.kind] += ms;
+            }
+            tfree.push_back(t.a);
+            tfree.push_back(t.b);
+        }
+        timed.clear();
+    }
 
     hipEvent_t get_event()
     {
@@ -258,6 +314,7 @@ msi_status msi_plan_destroy(msi_plan *p)
 {
     if (!p)
         return MSI_OK;
+    p->resolve_timings();
     if (p->core) {
         for (uint32_t gs = 0; gs < p->fill_ev.size(); ++gs)
             if (p->fill_ev[gs]) {
@@ -368,15 +425,21 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
     float *L = reinterpret_cast<float *>(wsb + ws.logits);
     if (T > 0) {
         if (d.wdtype == MSI_W_F32)
-            HIP_OK(launch_router_logits_f32(static_cast<const float *>(a->x), static_cast<const float *>(a->w_router),
-                                            a->bias, L, T, D, E, s));
+            HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
+                return launch_router_logits_f32(static_cast<const float *>(a->x),
+                                                static_cast<const float *>(a->w_router), a->bias, L, T, D, E, s);
+            }));
         else
-            HIP_OK(launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
-                                             static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s));
-        HIP_OK(launch_topk(L, a->r.idx, a->r.weights, T, E, K, s));
+            HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
+                return launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
+                                                 static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s);
+            }));
+        HIP_OK(p->timed_launch(MSI_K_TOPK, s, [&] { return launch_topk(L, a->r.idx, a->r.weights, T, E, K, s); }));
     }
-    HIP_OK(launch_permute(a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv, a->r.row_weight,
-                          reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s));
+    HIP_OK(p->timed_launch(MSI_K_PERMUTE, s, [&] {
+        return launch_permute(a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv,
+                              a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s);
+    }));
     return MSI_OK;
 }
 
@@ -501,7 +564,12 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         if (r < sched.rounds.size()) {
             const SchedRound &round = sched.rounds[r];
             if (!round.fills.empty()) {
-                rst = enqueue_fills(p, a->layer, round.fills, side);
+                msi_status fst = MSI_OK;
+                const hipError_t fe_ = p->timed_launch(MSI_K_FILL, side, [&] {
+                    fst = enqueue_fills(p, a->layer, round.fills, side);
+                    return fst == MSI_OK ? hipSuccess : hipErrorUnknown;
+                });
+                rst = fst != MSI_OK ? fst : (fe_ != hipSuccess ? fail(MSI_E_DEVICE, "fill timing event") : MSI_OK);
                 if (rst != MSI_OK)
                     break;
                 hipEvent_t fe = new_event();
@@ -551,15 +619,18 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
                 L.y = reinterpret_cast<float *>(wsb + ws.y);
                 L.row_weight = a->r.row_weight;
             }
-            hipError_t e;
-            switch (l.kind) {
-            case GU_TILE: e = launch_gateup_tile(L, cs); break;
-            case GU_STREAM: e = launch_gateup_stream(L, cs); break;
-            case GU_F32: e = launch_gateup_f32(L, cs); break;
-            case DN_TILE: e = launch_down_tile(L, cs); break;
-            case DN_STREAM: e = launch_down_stream(L, cs); break;
-            default: e = launch_down_f32(L, cs); break;
-            }
+            static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
+                                             MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32};
+            const hipError_t e = p->timed_launch(l.shared ? MSI_K_SHARED : tkind[l.kind], cs, [&] {
+                switch (l.kind) {
+                case GU_TILE: return launch_gateup_tile(L, cs);
+                case GU_STREAM: return launch_gateup_stream(L, cs);
+                case GU_F32: return launch_gateup_f32(L, cs);
+                case DN_TILE: return launch_down_tile(L, cs);
+                case DN_STREAM: return launch_down_stream(L, cs);
+                default: return launch_down_f32(L, cs);
+                }
+            });
             if (e != hipSuccess) {
                 rst = fail(MSI_E_DEVICE, std::string("expert kernel launch: ") + hipGetErrorString(e));
                 break;
@@ -581,9 +652,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
 
     // ---- publication: out written only if every tile saw its generation
     if (rst == MSI_OK)
-        if (launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
-                           has_shared ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv, a->out,
-                           p->status_dev, T, K, D, cs) != hipSuccess)
+        if (p->timed_launch(MSI_K_COMBINE, cs, [&] {
+                return launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
+                                      has_shared ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv,
+                                      a->out, p->status_dev, T, K, D, cs);
+            }) != hipSuccess)
             rst = fail(MSI_E_DEVICE, "combine launch failed");
     if (rst == MSI_OK && hipMemcpyAsync(p->status_host, p->status_dev, sizeof(uint32_t), hipMemcpyDeviceToHost,
                                         cs) != hipSuccess)
@@ -610,6 +683,8 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     for (hipEvent_t e : round_events)
         p->free_events.push_back(e);
     core.end_forward(a->layer, sched);
+    if (p->timing)
+        p->resolve_timings();
     if (rst != MSI_OK)
         return rst;
     if (*p->status_host & STATUS_STALE) {
@@ -655,6 +730,31 @@ msi_status msi_plan_stats(const msi_plan *p, msi_stats *st)
     st->windows_busy = p->core->windows_busy();
     st->consumers_live = p->core->consumers_live();
     st->epoch = p->core->epoch();
+    return MSI_OK;
+}
+
+msi_status msi_plan_set_timing(msi_plan *p, int enable)
+{
+    if (!p)
+        return fail(MSI_E_INVALID_ARG, "null plan");
+    p->timing = enable != 0;
+    return MSI_OK;
+}
+
+msi_status msi_plan_timings(msi_plan *p, msi_timings *out, int reset)
+{
+    if (!p || !out)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    HIP_OK(hipSetDevice(p->device));
+    p->resolve_timings();
+    for (int k = 0; k < MSI_NKERN; ++k) {
+        out->launches[k] = p->t_launches[k];
+        out->ms[k] = p->t_ms[k];
+        if (reset) {
+            p->t_launches[k] = 0;
+            p->t_ms[k] = 0.0;
+        }
+    }
     return MSI_OK;
 }
 
