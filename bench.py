@@ -92,7 +92,7 @@ def bench_decode(args, cs, side):
     ms = _run(plan, xs, dev, r, ws, out, args.steps, 0, cs, side)
     t = plan.timings()
     st = plan.stats()
-    # algorithmic bytes of each step's routed gate/up launch (one round): the
+    # algorithmic bytes of each step's gate/up launch (one round): the
     # demanded experts' Wg and Wu once, their tokens' x rows once, act written
     # once; the down launch reads Wd and act once and writes fp32 rows once
     bytes_b, down_b = [], []
@@ -100,8 +100,10 @@ def bench_decode(args, cs, side):
         plan.route(xs[b], dev["wr"], dev["bias"], r, ws, cs)
         c = r.counts.cpu().numpy()
         dem = c[c > 0]
-        bytes_b.append(len(dem) * 2 * s.I * s.d * 2 + int(dem.sum()) * (s.d * 2 + s.I * 2))
-        down_b.append(len(dem) * s.d * s.I * 2 + int(dem.sum()) * (s.I * 2 + s.d * 4))
+        # the shared expert rides in the same launches: one more object, T more rows
+        n_obj, n_rows = len(dem) + 1, int(dem.sum()) + s.T
+        bytes_b.append(n_obj * 2 * s.I * s.d * 2 + n_rows * (s.d * 2 + s.I * 2))
+        down_b.append(n_obj * s.d * s.I * 2 + n_rows * (s.I * 2 + s.d * 4))
     per_step_bytes = [bytes_b[i % len(xs)] for i in range(args.steps)]
     per_step_down = [down_b[i % len(xs)] for i in range(args.steps)]
     n_gu, ms_gu = t["gateup_stream"]

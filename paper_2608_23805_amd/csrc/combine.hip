@@ -23,14 +23,20 @@ __global__ void __launch_bounds__(256) combine_kernel(const float *__restrict__ 
         return;
     const int t = int(i / d4), c = int(i % d4) * 4;
     float4 acc = ys ? *reinterpret_cast<const float4 *>(ys + int64_t(t) * d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int k = 0; k < K; ++k) {
-        const int64_t row = inv[int64_t(t) * K + k];
-        const float4 v = *reinterpret_cast<const float4 *>(y + row * d + c);
-        acc.x += v.x;
-        acc.y += v.y;
-        acc.z += v.z;
-        acc.w += v.w;
-    }
+    // all K row loads are issued before the fixed-order sum (K <= 16)
+    float4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < K)
+            v[k] = *reinterpret_cast<const float4 *>(y + int64_t(inv[int64_t(t) * K + k]) * d + c);
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < K) {
+            acc.x += v[k].x;
+            acc.y += v[k].y;
+            acc.z += v[k].z;
+            acc.w += v[k].w;
+        }
     *reinterpret_cast<float4 *>(out + int64_t(t) * d + c) = acc;
 }
 

@@ -104,6 +104,25 @@ __device__ __forceinline__ bool slot_current(const WorkItem &it, const uint32_t 
     return false;
 }
 
+// ---- wavefront reductions (64 lanes)
+__device__ __forceinline__ float wave_max(float v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (uint64_t(1) << lane) - 1; }
+
 // Logical tile index with consecutive tiles kept on one XCD: hardware hands
 // workgroup b to XCD b % 8, so XCD x walks tiles [x*per, (x+1)*per).
 __device__ __forceinline__ int xcd_swizzle(int b, int n)

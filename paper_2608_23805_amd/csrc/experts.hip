@@ -42,6 +42,9 @@ static TileArgs tile_args(const ExpertLaunch &L, bool gateup)
     }
     p.wbase = L.wbase;
     p.wstride = L.wstride;
+    p.shared_w = L.shared_w;
+    p.a_s = reinterpret_cast<const uint16_t *>(L.act_s);
+    p.out_s = gateup ? L.act_s : static_cast<void *>(L.ys);
     p.n_valid = 1 << 30;
     p.d = L.d;
     p.I = L.I;
@@ -154,14 +157,15 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
         return;
     const int n = it.nrows;
     const int d = L.d, I = L.I, ldk = d + 8;
-    stage_rows(xs, reinterpret_cast<const uint16_t *>(L.x), L.perm, it.row0, n, d);
+    const bool sh = it.slot < 0;
+    stage_rows(xs, reinterpret_cast<const uint16_t *>(L.x), sh ? nullptr : L.perm, it.row0, n, d);
     __syncthreads();
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int i0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
     const int j = lane & 15, kg = (lane >> 4) * 8;
-    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + kg;
     const uint16_t *up = gp + int64_t(I) * d;
     const uint16_t *xr = xs + j * ldk + kg;
@@ -188,7 +192,8 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
         uint2 v;
         v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
         v.y = pack_bf16x2(silu(ag[2]) * au[2], silu(ag[3]) * au[3]);
-        uint16_t *act = reinterpret_cast<uint16_t *>(L.act) + int64_t(it.row0 + j) * I + i0 + 4 * (lane >> 4);
+        uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0 + j) * I + i0 +
+                        4 * (lane >> 4);
         *reinterpret_cast<uint2 *>(act) = v;
     }
 }
@@ -203,14 +208,15 @@ __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
         return;
     const int n = it.nrows;
     const int d = L.d, I = L.I, ldk = I + 8;
-    stage_rows(as, reinterpret_cast<const uint16_t *>(L.act), nullptr, it.row0, n, I);
+    const bool sh = it.slot < 0;
+    stage_rows(as, reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act), nullptr, it.row0, n, I);
     __syncthreads();
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int c0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
     const int j = lane & 15, kg = (lane >> 4) * 8;
-    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *wp = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0 + j) * I + kg;
     const uint16_t *ar = as + j * ldk + kg;
     const bool live = j < n;
@@ -229,9 +235,9 @@ __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
     }
     if (live) {
         const int64_t row = it.row0 + j;
-        const float w = L.row_weight ? L.row_weight[row] : 1.0f;
+        const float w = sh ? 1.0f : L.row_weight[row];
         float4 o = make_float4(acc[0] * w, acc[1] * w, acc[2] * w, acc[3] * w);
-        *reinterpret_cast<float4 *>(L.y + row * d + c0 + 4 * (lane >> 4)) = o;
+        *reinterpret_cast<float4 *>((sh ? L.ys : L.y) + row * d + c0 + 4 * (lane >> 4)) = o;
     }
 }
 
@@ -290,9 +296,10 @@ __global__ void __launch_bounds__(256) gateup_f32_kernel(ExpertLaunch L)
     if (r >= it.nrows)
         return;
     const int d = L.d;
-    const int64_t src = L.perm ? int64_t(L.perm[it.row0 + r]) : int64_t(it.row0 + r);
+    const bool sh = it.slot < 0;
+    const int64_t src = sh ? int64_t(it.row0 + r) : int64_t(L.perm[it.row0 + r]);
     const float *x = reinterpret_cast<const float *>(L.x) + src * d;
-    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const float *wg = reinterpret_cast<const float *>(base) + int64_t(c) * d;
     const float *wu = wg + int64_t(L.I) * d;
     float g = 0.f, u = 0.f;
@@ -300,7 +307,7 @@ __global__ void __launch_bounds__(256) gateup_f32_kernel(ExpertLaunch L)
         g = fmaf(x[k], wg[k], g);
         u = fmaf(x[k], wu[k], u);
     }
-    reinterpret_cast<float *>(L.act)[int64_t(it.row0 + r) * L.I + c] = silu(g) * u;
+    reinterpret_cast<float *>(sh ? L.act_s : L.act)[int64_t(it.row0 + r) * L.I + c] = silu(g) * u;
 }
 
 __global__ void __launch_bounds__(256) down_f32_kernel(ExpertLaunch L)
@@ -317,14 +324,15 @@ __global__ void __launch_bounds__(256) down_f32_kernel(ExpertLaunch L)
         return;
     const int I = L.I;
     const int64_t row = it.row0 + r;
-    const float *a = reinterpret_cast<const float *>(L.act) + row * I;
-    const uint8_t *base = L.wbase + (it.slot >= 0 ? uint64_t(it.slot) * L.wstride : 0);
+    const bool sh = it.slot < 0;
+    const float *a = reinterpret_cast<const float *>(sh ? L.act_s : L.act) + row * I;
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const float *wd = reinterpret_cast<const float *>(base) + int64_t(2) * I * L.d + int64_t(c) * I;
     float acc = 0.f;
     for (int k = 0; k < I; ++k)
         acc = fmaf(a[k], wd[k], acc);
-    const float w = L.row_weight ? L.row_weight[row] : 1.0f;
-    L.y[row * L.d + c] = acc * w;
+    const float w = sh ? 1.0f : L.row_weight[row];
+    (sh ? L.ys : L.y)[row * L.d + c] = acc * w;
 }
 
 hipError_t launch_gateup_f32(const ExpertLaunch &L, hipStream_t s)
@@ -349,11 +357,10 @@ namespace msi {
 
 hipError_t init_kernel_attributes()
 {
-    const int big = 160 * 1024;
     hipError_t e = hipSuccess;
     auto set = [&](const void *f) {
         if (e == hipSuccess)
-            e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+            e = allow_large_lds(f);
     };
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
@@ -362,6 +369,8 @@ hipError_t init_kernel_attributes()
     set(reinterpret_cast<const void *>(&stream_gateup_kernel<1>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<16>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
+    if (e == hipSuccess)
+        e = init_route_attributes();
     return e;
 }
 

@@ -55,6 +55,11 @@ struct TileArgs {
     int64_t ldo;                // elements per output row
     const float *bias;          // router bias or null
     const float *row_weight;    // gate weight per permuted row (down) or null (1.0)
+    // items with slot < 0 (gate/up, down) are the shared expert: weights at
+    // shared_w, A rows are tokens (gate/up) or rows of a_s (down), output to out_s
+    const uint8_t *shared_w;
+    const uint16_t *a_s;
+    void *out_s;
 };
 
 template <TileMode MODE>
@@ -82,6 +87,12 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
     const int m0 = (local / p.n_tiles_n) * BM;
     const int nt = local % p.n_tiles_n;
 
+    const bool sh = MODE != TileMode::Router && it.slot < 0;
+    const uint16_t *abase = (MODE == TileMode::Down && sh) ? p.a_s : p.a;
+    const int32_t *perm = sh ? nullptr : p.perm;
+    void *outp = sh ? p.out_s : p.out;
+    const float *rweight = sh ? nullptr : p.row_weight;
+
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -98,10 +109,12 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
         aval[i] = m0 + r < it.nrows;
         int64_t src = 0;
         if (aval[i])
-            src = p.perm ? int64_t(p.perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
-        aptr[i] = p.a + src * p.lda + chunk * 8;
+            src = perm ? int64_t(perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
+        aptr[i] = abase + src * p.lda + chunk * 8;
     }
-    const uint8_t *base = p.wbase + (it.slot >= 0 ? uint64_t(it.slot) * p.wstride : 0);
+    const uint8_t *base = MODE == TileMode::Router ? p.wbase
+                          : sh                     ? p.shared_w
+                                                   : p.wbase + uint64_t(it.slot) * p.wstride;
     const uint16_t *bptr[B_LOADS];
     bool bval[B_LOADS];
 #pragma unroll
@@ -204,15 +217,15 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
                 continue;
             const int64_t orow = int64_t(it.row0) + m0 + row;
             if constexpr (MODE == TileMode::GateUp) {
-                uint16_t *act = reinterpret_cast<uint16_t *>(p.out) + orow * p.ldo;
+                uint16_t *act = reinterpret_cast<uint16_t *>(outp) + orow * p.ldo;
 #pragma unroll
                 for (int nb = 0; nb < 2; ++nb) {
                     const int col = nt * 128 + wn * 64 + nb * 32 + col_l;
                     act[col] = f32_to_bf16(silu(acc[mb][nb][r]) * acc[mb][nb + 2][r]);
                 }
             } else if constexpr (MODE == TileMode::Down) {
-                float *y = reinterpret_cast<float *>(p.out) + orow * p.ldo;
-                const float w = p.row_weight ? p.row_weight[orow] : 1.0f;
+                float *y = reinterpret_cast<float *>(outp) + orow * p.ldo;
+                const float w = rweight ? rweight[orow] : 1.0f;
 #pragma unroll
                 for (int nb = 0; nb < 4; ++nb)
                     y[nt * BN + wn * 128 + nb * 32 + col_l] = acc[mb][nb][r] * w;

@@ -16,10 +16,26 @@ hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, cons
                                      int d, int E, hipStream_t s);
 // raise the dynamic LDS limit of the kernels that use more than 64 KiB
 hipError_t init_kernel_attributes();
-hipError_t launch_topk(const float *L, int32_t *idx, float *w, int T, int E, int K, hipStream_t s);
-hipError_t launch_permute(const int32_t *idx, const float *w, int32_t *counts, int32_t *offsets, int32_t *perm,
-                          int32_t *inv, float *row_weight, int32_t *blockhist, int T, int K, int E,
-                          hipStream_t s);
+
+// Let kernel f use all of the CU's 160 KiB of LDS (dynamic part = 160 KiB
+// minus its static LDS).
+inline hipError_t allow_large_lds(const void *f)
+{
+    hipFuncAttributes a{};
+    hipError_t e = hipFuncGetAttributes(&a, f);
+    if (e != hipSuccess)
+        return e;
+    return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               int(160 * 1024 - a.sharedSizeBytes));
+}
+// streaming router for T <= 16 tokens (bf16)
+hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T, int d,
+                                int E, hipStream_t s);
+// top-K + restricted softmax + permutation (one fused workgroup when T <= 256)
+hipError_t launch_route_select(const float *L, int32_t *idx, float *w, int32_t *counts, int32_t *offsets,
+                               int32_t *perm, int32_t *inv, float *row_weight, int32_t *blockhist, int T, int K,
+                               int E, hipStream_t s);
+hipError_t init_route_attributes();
 
 // ---- expert projections (experts.hip).  `items` lists the experts of one
 // launch (device memory), `n_tiles` the launch's total tile count.
@@ -28,9 +44,14 @@ struct ExpertLaunch {
     int n_items;
     int n_tiles;
     const void *x;               // [T, d] hidden states (bf16 or f32)
-    const int32_t *perm;         // gather map, null for the shared expert
-    const uint8_t *wbase;        // slot pool (routed) or shared object
+    const int32_t *perm;         // gather map of routed rows
+    const uint8_t *wbase;        // slot pool
     uint64_t wstride;
+    // items with slot < 0 are the shared expert: weights at shared_w, rows
+    // are tokens (no gather), act / y go to act_s / ys, weight 1
+    const uint8_t *shared_w;
+    void *act_s;
+    float *ys;
     const uint32_t *gen_dev;
     uint32_t *status;
     void *act;                   // [rows, I] bf16 (f32 for f32 layers)

@@ -429,16 +429,20 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
                 return launch_router_logits_f32(static_cast<const float *>(a->x),
                                                 static_cast<const float *>(a->w_router), a->bias, L, T, D, E, s);
             }));
+        else if (T <= 16)
+            HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
+                return launch_router_stream(static_cast<const uint16_t *>(a->x),
+                                            static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s);
+            }));
         else
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
                 return launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
                                                  static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s);
             }));
-        HIP_OK(p->timed_launch(MSI_K_TOPK, s, [&] { return launch_topk(L, a->r.idx, a->r.weights, T, E, K, s); }));
     }
-    HIP_OK(p->timed_launch(MSI_K_PERMUTE, s, [&] {
-        return launch_permute(a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv,
-                              a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s);
+    HIP_OK(p->timed_launch(MSI_K_TOPK, s, [&] {
+        return launch_route_select(L, a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv,
+                                   a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s);
     }));
     return MSI_OK;
 }
@@ -490,7 +494,6 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     enum Kind { GU_TILE, GU_STREAM, GU_F32, DN_TILE, DN_STREAM, DN_F32, NKIND };
     struct Launch {
         int kind;
-        bool shared;
         size_t off;
         int n_items;
         int n_tiles;
@@ -498,10 +501,10 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     std::vector<std::vector<Launch>> launches(sched.rounds.size());
     std::vector<WorkItem> table;
     const bool f32 = d.wdtype == MSI_W_F32;
-    auto add_launch = [&](size_t r, int kind, bool shared, const std::vector<WorkItem> &items) {
+    auto add_launch = [&](size_t r, int kind, const std::vector<WorkItem> &items) {
         if (items.empty())
             return;
-        Launch l{kind, shared, table.size(), int(items.size()), 0};
+        Launch l{kind, table.size(), int(items.size()), 0};
         int tiles = 0;
         for (WorkItem w : items) {
             int n;
@@ -521,26 +524,23 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         launches[r].push_back(l);
     };
     const uint32_t thr = g_stream_threshold;
-    for (size_t r = 0; r < sched.rounds.size(); ++r) {
+    const bool has_shared = a->shared_object && T > 0;
+    if (has_shared && sched.rounds.empty())
+        launches.emplace_back();
+    for (size_t r = 0; r < launches.size(); ++r) {
         std::vector<WorkItem> tile_items, stream_items;
-        for (const SchedItem &si : sched.rounds[r].items) {
+        if (r == 0 && has_shared)   // the shared expert rides in the first round's launches
+            (f32 || uint32_t(T) > thr ? tile_items : stream_items).push_back(WorkItem{-1, -1, 0u, 0, T, 0});
+        const std::vector<SchedItem> none;
+        for (const SchedItem &si : r < sched.rounds.size() ? sched.rounds[r].items : none) {
             WorkItem w{si.expert, int32_t(core.global_slot(a->layer, uint32_t(si.slot))), si.gen, offsets[si.expert],
                        counts[si.expert], 0};
             (f32 || uint32_t(w.nrows) > thr ? tile_items : stream_items).push_back(w);
         }
-        add_launch(r, f32 ? GU_F32 : GU_TILE, false, tile_items);
-        add_launch(r, GU_STREAM, false, stream_items);
-        add_launch(r, f32 ? DN_F32 : DN_TILE, false, tile_items);
-        add_launch(r, DN_STREAM, false, stream_items);
-    }
-    const bool has_shared = a->shared_object && T > 0;
-    if (has_shared) {
-        if (sched.rounds.empty())
-            launches.emplace_back();
-        const std::vector<WorkItem> sh{WorkItem{-1, -1, 0u, 0, T, 0}};
-        const bool st = !f32 && uint32_t(T) <= thr;
-        add_launch(0, f32 ? GU_F32 : (st ? GU_STREAM : GU_TILE), true, sh);
-        add_launch(0, f32 ? DN_F32 : (st ? DN_STREAM : DN_TILE), true, sh);
+        add_launch(r, f32 ? GU_F32 : GU_TILE, tile_items);
+        add_launch(r, GU_STREAM, stream_items);
+        add_launch(r, f32 ? DN_F32 : DN_TILE, tile_items);
+        add_launch(r, DN_STREAM, stream_items);
     }
     if (table.size() > p->table_cap)
         return fail(MSI_E_INVALID_ARG, "internal: schedule table overflow");
@@ -604,24 +604,18 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             L.status = p->status_dev;
             L.d = D;
             L.I = I;
-            if (l.shared) {
-                L.perm = nullptr;
-                L.wbase = static_cast<const uint8_t *>(a->shared_object);
-                L.wstride = 0;
-                L.act = wsb + ws.act_s;
-                L.y = reinterpret_cast<float *>(wsb + ws.ys);
-                L.row_weight = nullptr;
-            } else {
-                L.perm = a->r.perm;
-                L.wbase = static_cast<const uint8_t *>(d.slot_pool);
-                L.wstride = d.slot_stride;
-                L.act = wsb + ws.act;
-                L.y = reinterpret_cast<float *>(wsb + ws.y);
-                L.row_weight = a->r.row_weight;
-            }
+            L.perm = a->r.perm;
+            L.wbase = static_cast<const uint8_t *>(d.slot_pool);
+            L.wstride = d.slot_stride;
+            L.act = wsb + ws.act;
+            L.y = reinterpret_cast<float *>(wsb + ws.y);
+            L.row_weight = a->r.row_weight;
+            L.shared_w = static_cast<const uint8_t *>(a->shared_object);
+            L.act_s = wsb + ws.act_s;
+            L.ys = reinterpret_cast<float *>(wsb + ws.ys);
             static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
                                              MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32};
-            const hipError_t e = p->timed_launch(l.shared ? MSI_K_SHARED : tkind[l.kind], cs, [&] {
+            const hipError_t e = p->timed_launch(tkind[l.kind], cs, [&] {
                 switch (l.kind) {
                 case GU_TILE: return launch_gateup_tile(L, cs);
                 case GU_STREAM: return launch_gateup_stream(L, cs);
