@@ -197,7 +197,7 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=10)
     ap.add_argument("--lru-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu")
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
@@ -209,6 +209,9 @@ def main():
     cs = torch.cuda.current_stream()
     side = torch.cuda.Stream()
 
+    if "decode" in skip:            # profiling aid: prefill only
+        print(json.dumps({"prefill": bench_prefill(args, cs, side)}), flush=True)
+        return
     dec, li = bench_decode(args, cs, side)
     extra = {}
     if "lru" not in skip:

@@ -134,16 +134,31 @@ int tiles_down_stream(int nrows, int d, int I)
 }
 
 // Stage the (<= 16) B-operand rows of one expert into LDS [16][K + 8].
+// Loads are issued in batches of 8 per thread before their LDS stores, so a
+// 64 KiB staging costs two memory round trips, not sixteen.
 __device__ __forceinline__ void stage_rows(uint16_t *xs, const uint16_t *__restrict__ src, const int32_t *perm,
                                            int row0, int n, int K)
 {
     const int ldk = K + 8;
     const int chunks = K / 8;
-    for (int c = threadIdx.x; c < n * chunks; c += blockDim.x) {
-        const int j = c / chunks, q = c % chunks;
-        const int64_t r = perm ? int64_t(perm[row0 + j]) : int64_t(row0 + j);
-        *reinterpret_cast<uint4 *>(xs + j * ldk + q * 8) =
-            *reinterpret_cast<const uint4 *>(src + r * K + q * 8);
+    const int total = n * chunks;
+    for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {
+        uint4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int c = c0 + u * int(blockDim.x);
+            if (c < total) {
+                const int j = c / chunks, q = c % chunks;
+                const int64_t r = perm ? int64_t(perm[row0 + j]) : int64_t(row0 + j);
+                v[u] = *reinterpret_cast<const uint4 *>(src + r * K + q * 8);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int c = c0 + u * int(blockDim.x);
+            if (c < total)
+                *reinterpret_cast<uint4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
+        }
     }
 }
 

@@ -4,9 +4,10 @@
 // C[m, n] = sum_k A[m, k] * B[n, k]: both operands have the reduction axis
 // contiguous (x and act rows; router / expert weight rows).  A workgroup of
 // 256 threads (4 wavefronts, 2 x 2) computes a BM x BN = 128 x 256 tile; each
-// wavefront owns 64 x 128 as 2 x 4 blocks of 32 x 32.  K advances in BK = 64
-// steps through a double-buffered LDS stage, the next stage's global loads
-// held in registers while the current stage feeds the MFMAs.
+// wavefront owns 64 x 128 as 2 x 4 blocks of 32 x 32.  K advances in BK = 32
+// steps through a double-buffered LDS stage (60 KiB per workgroup, so two
+// workgroups share a CU and each SIMD interleaves two wavefronts); the next
+// stage's global loads are in flight while the current stage is computed.
 //
 // A rows are gathered through the permutation (row r of expert e's tile reads
 // token perm[row0 + r]), so the permuted copy of x is never materialised.
@@ -26,8 +27,8 @@ namespace msi {
 namespace tile {
 constexpr int BM = 128;
 constexpr int BN = 256;
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;   // 144-byte LDS row pitch: conflict-free 16-byte fragment reads
+constexpr int BK = 32;
+constexpr int LDK = BK + 8;   // 80-byte LDS row pitch: conflict-free 16-byte fragment reads
 constexpr int THREADS = 256;
 constexpr int A_LOADS = BM * (BK / 8) / THREADS;   // 16-byte loads per thread per stage
 constexpr int B_LOADS = BN * (BK / 8) / THREADS;
@@ -62,6 +63,24 @@ struct TileArgs {
     void *out_s;
 };
 
+// Stage helpers: row i of a thread's share sits THREADS / (BK / 8) rows below row i-1.
+template <int N>
+__device__ __forceinline__ void tile_load_rows(u32x4 (&r)[N], const uint16_t *base, const uint32_t (&off)[N],
+                                               uint32_t k0)
+{
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+        r[i] = *reinterpret_cast<const u32x4 *>(base + (off[i] + k0));
+}
+
+template <int N>
+__device__ __forceinline__ void tile_store_rows(const u32x4 (&r)[N], uint16_t *dst)
+{
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+        *reinterpret_cast<u32x4 *>(dst + (tile::THREADS / (tile::BK / 8)) * i * tile::LDK) = r[i];
+}
+
 template <TileMode MODE>
 __device__ __forceinline__ int wave_col_block(int wn, int nb)
 {
@@ -72,7 +91,7 @@ __device__ __forceinline__ int wave_col_block(int wn, int nb)
 }
 
 template <TileMode MODE>
-__global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
+__global__ void __launch_bounds__(tile::THREADS, 2) tile_gemm_kernel(TileArgs p)
 {
     using namespace tile;
     extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -97,69 +116,56 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int chunk = tid & 7;        // 16-byte chunk of a 128-byte stage row
-    const int rsub = tid >> 3;        // 0..31
+    constexpr int CPR = BK / 8;       // 16-byte chunks per stage row
+    const int chunk = tid % CPR;
+    const int rsub = tid / CPR;       // first row of this thread's share
 
-    // ---- per-thread A / B row pointers (fixed over K)
-    const uint16_t *aptr[A_LOADS];
-    bool aval[A_LOADS];
+    // ---- per-thread A / B row offsets (fixed over K): 32-bit element offsets
+    // from uniform bases, so the loads use the scalar-base addressing form.
+    // Rows past the tile's valid rows (or past the router's E columns) read
+    // row 0 unmasked: an MFMA output element depends only on its own A row and
+    // B column, and those outputs are never stored.  (Masking the loads would
+    // put a divergent branch, and a full memory wait, behind every load.)
+    uint32_t aoff[A_LOADS];
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-        const int r = rsub + 32 * i;
-        aval[i] = m0 + r < it.nrows;
+        const int r = rsub + (THREADS / CPR) * i;
         int64_t src = 0;
-        if (aval[i])
+        if (m0 + r < it.nrows)
             src = perm ? int64_t(perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
-        aptr[i] = abase + src * p.lda + chunk * 8;
+        aoff[i] = uint32_t(src * p.lda) + chunk * 8;
     }
+    static_assert(THREADS / CPR * A_LOADS == BM && THREADS / CPR * B_LOADS == BN, "stage rows per thread");
     const uint8_t *base = MODE == TileMode::Router ? p.wbase
                           : sh                     ? p.shared_w
                                                    : p.wbase + uint64_t(it.slot) * p.wstride;
-    const uint16_t *bptr[B_LOADS];
-    bool bval[B_LOADS];
+    const uint16_t *bbase = reinterpret_cast<const uint16_t *>(base) +
+                            (MODE == TileMode::Down ? int64_t(2) * p.I * p.d : int64_t(0));
+    uint32_t boff[B_LOADS];
 #pragma unroll
     for (int j = 0; j < B_LOADS; ++j) {
-        const int c = rsub + 32 * j;
+        const int c = rsub + (THREADS / CPR) * j;
         int64_t brow;
-        const uint16_t *mat;
-        if constexpr (MODE == TileMode::GateUp) {
-            const uint16_t *wg = reinterpret_cast<const uint16_t *>(base);
-            mat = c < 128 ? wg : wg + int64_t(p.I) * p.d;
-            brow = int64_t(nt) * 128 + (c & 127);
-            bval[j] = true;
-        } else if constexpr (MODE == TileMode::Down) {
-            mat = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * p.I * p.d;
+        if constexpr (MODE == TileMode::GateUp)
+            brow = (c < 128 ? int64_t(0) : int64_t(p.I)) + int64_t(nt) * 128 + (c & 127);   // Wu follows Wg
+        else
             brow = int64_t(nt) * BN + c;
-            bval[j] = true;
-        } else {
-            mat = reinterpret_cast<const uint16_t *>(base);
-            brow = int64_t(nt) * BN + c;
-            bval[j] = brow < p.n_valid;
-            if (!bval[j])
-                brow = 0;
-        }
-        bptr[j] = mat + brow * p.K + chunk * 8;
+        if (MODE == TileMode::Router && brow >= p.n_valid)
+            brow = 0;
+        boff[j] = uint32_t(brow * p.K) + chunk * 8;
     }
 
-    uint4 ra[A_LOADS], rb[B_LOADS];
-    auto load_stage = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < A_LOADS; ++i)
-            ra[i] = aval[i] ? *reinterpret_cast<const uint4 *>(aptr[i] + k0) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < B_LOADS; ++j)
-            rb[j] = bval[j] ? *reinterpret_cast<const uint4 *>(bptr[j] + k0) : make_uint4(0, 0, 0, 0);
-    };
-    auto store_stage = [&](int buf) {
-        uint16_t *a = As + buf * BM * LDK;
-        uint16_t *b = Bs + buf * BN * LDK;
-#pragma unroll
-        for (int i = 0; i < A_LOADS; ++i)
-            *reinterpret_cast<uint4 *>(a + (rsub + 32 * i) * LDK + chunk * 8) = ra[i];
-#pragma unroll
-        for (int j = 0; j < B_LOADS; ++j)
-            *reinterpret_cast<uint4 *>(b + (rsub + 32 * j) * LDK + chunk * 8) = rb[j];
-    };
+    u32x4 ra0[A_LOADS], rb0[B_LOADS];
+#define MSI_LOAD_STAGE(RA, RB, K0)                  \
+    do {                                            \
+        tile_load_rows(RA, abase, aoff, uint32_t(K0)); \
+        tile_load_rows(RB, bbase, boff, uint32_t(K0)); \
+    } while (0)
+#define MSI_STORE_STAGE(RA, RB, BUF)                                     \
+    do {                                                                 \
+        tile_store_rows(RA, As + (BUF) * BM * LDK + rsub * LDK + chunk * 8); \
+        tile_store_rows(RB, Bs + (BUF) * BN * LDK + rsub * LDK + chunk * 8); \
+    } while (0)
 
     f32x16 acc[2][4];
 #pragma unroll
@@ -170,17 +176,9 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
             for (int r = 0; r < 16; ++r)
                 acc[mb][nb][r] = 0.f;
 
-    const int nk = p.K / BK;
-    load_stage(0);
-    store_stage(0);
-    if (nk > 1)
-        load_stage(BK);
-    __syncthreads();
-
     const int frow = lane & 31;
     const int fk = (lane >> 5) * 8;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
+    auto compute = [&](int buf) {
         const uint16_t *a = As + buf * BM * LDK;
         const uint16_t *b = Bs + buf * BN * LDK;
 #pragma unroll
@@ -199,15 +197,59 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
                 for (int nb = 0; nb < 4; ++nb)
                     acc[mb][nb] = mfma32(af[mb], bfr[nb], acc[mb][nb]);
         }
+    };
+
+    // One register set: stage kt+1 is loaded while stage kt feeds the MFMAs
+    // and written to the other LDS buffer afterwards.  Two workgroups per CU
+    // (two wavefronts per SIMD) cover each other's load and barrier waits.
+    const int nk = p.K / BK;
+    MSI_LOAD_STAGE(ra0, rb0, 0);
+    MSI_STORE_STAGE(ra0, rb0, 0);
+    if (nk > 1)
+        MSI_LOAD_STAGE(ra0, rb0, BK);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        compute(buf);
         if (kt + 1 < nk)
-            store_stage(buf ^ 1);
+            MSI_STORE_STAGE(ra0, rb0, buf ^ 1);
         if (kt + 2 < nk)
-            load_stage((kt + 2) * BK);
+            MSI_LOAD_STAGE(ra0, rb0, (kt + 2) * BK);
         __syncthreads();
     }
+#undef MSI_LOAD_STAGE
+#undef MSI_STORE_STAGE
 
     // ---- epilogue: lane holds rows 8*(r/4) + 4*(lane/32) + r%4, column lane%32 of each block
     const int col_l = lane & 31;
+    if constexpr (MODE == TileMode::GateUp) {
+        // act = silu(gate) * up in bf16, transposed through LDS (the main loop
+        // is done with it) so that each lane stores 16 contiguous bytes
+        constexpr int EP = 64 + 8;                     // per-wave [64 rows][64 cols] bf16, padded
+        uint16_t *ep = lds + wave * 64 * EP;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rl = mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+                    ep[rl * EP + nb * 32 + col_l] = f32_to_bf16(silu(acc[mb][nb][r]) * acc[mb][nb + 2][r]);
+            }
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        uint16_t *act = reinterpret_cast<uint16_t *>(outp);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int c = lane + 64 * i;                // 512 chunks of 8 bf16
+            const int rl = c >> 3, q = c & 7;
+            const int row = wm * 64 + rl;
+            if (m0 + row < it.nrows)
+                *reinterpret_cast<uint4 *>(act + (int64_t(it.row0) + m0 + row) * p.ldo + nt * 128 + wn * 64 + q * 8) =
+                    *reinterpret_cast<const uint4 *>(ep + rl * EP + q * 8);
+        }
+        return;
+    }
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
@@ -216,14 +258,7 @@ __global__ void __launch_bounds__(tile::THREADS, 1) tile_gemm_kernel(TileArgs p)
             if (m0 + row >= it.nrows)
                 continue;
             const int64_t orow = int64_t(it.row0) + m0 + row;
-            if constexpr (MODE == TileMode::GateUp) {
-                uint16_t *act = reinterpret_cast<uint16_t *>(outp) + orow * p.ldo;
-#pragma unroll
-                for (int nb = 0; nb < 2; ++nb) {
-                    const int col = nt * 128 + wn * 64 + nb * 32 + col_l;
-                    act[col] = f32_to_bf16(silu(acc[mb][nb][r]) * acc[mb][nb + 2][r]);
-                }
-            } else if constexpr (MODE == TileMode::Down) {
+            if constexpr (MODE == TileMode::Down) {
                 float *y = reinterpret_cast<float *>(outp) + orow * p.ldo;
                 const float w = rweight ? rweight[orow] : 1.0f;
 #pragma unroll

@@ -58,9 +58,21 @@ __global__ void __launch_bounds__(256) router_stream_kernel(const uint16_t *__re
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];   // [16][d + 8]
     __shared__ float red[3][64][4];
     const int ldk = d + 8;
-    for (int c = threadIdx.x; c < T * (d / 8); c += blockDim.x) {
-        const int j = c / (d / 8), q = c % (d / 8);
-        *reinterpret_cast<uint4 *>(xs + j * ldk + q * 8) = *reinterpret_cast<const uint4 *>(x + int64_t(j) * d + q * 8);
+    const int chunks = d / 8, total = T * chunks;
+    for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {   // loads batched 8 deep
+        uint4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int c = c0 + u * int(blockDim.x);
+            if (c < total)
+                v[u] = *reinterpret_cast<const uint4 *>(x + int64_t(c / chunks) * d + (c % chunks) * 8);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int c = c0 + u * int(blockDim.x);
+            if (c < total)
+                *reinterpret_cast<uint4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
+        }
     }
     __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
