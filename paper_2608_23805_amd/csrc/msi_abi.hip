@@ -349,7 +349,8 @@ msi_status msi_plan_reset(msi_plan *p)
 {
     if (!p)
         return fail(MSI_E_INVALID_ARG, "null plan");
-    poll_fills(p);
+    // fills not yet observed are outstanding work: their completions will be
+    // judged against the new epoch and not published
     const msi_status st = p->core->reset();
     return st == MSI_OK ? st : fail(st, p->core->error());
 }
@@ -683,6 +684,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         return rst;
     if (*p->status_host & STATUS_STALE) {
         core.stats().stale_detected++;
+        core.invalidate_read_slots(a->layer, sched);
         return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
     }
     return MSI_OK;

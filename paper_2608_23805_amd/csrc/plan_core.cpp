@@ -347,6 +347,18 @@ void PlanCore::end_forward(uint32_t layer, const Schedule &s)
         }
 }
 
+void PlanCore::invalidate_read_slots(uint32_t layer, const Schedule &s)
+{
+    for (const SchedRound &r : s.rounds)
+        for (const SchedItem &it : r.items) {
+            Slot &sl = slot(layer, uint32_t(it.slot));
+            if (sl.fill_id < 0 && sl.holds == 0 && sl.consumers == 0) {
+                sl.state = SlotState::Vacant;
+                sl.expert = -1;
+            }
+        }
+}
+
 msi_status PlanCore::hold(uint32_t layer, uint32_t s)
 {
     if (layer >= n_layers_ || s >= pool_slots_) {

@@ -117,6 +117,10 @@ public:
     // Zero-cache plans then forget every object they loaded.
     void end_forward(uint32_t layer, const Schedule &s);
 
+    // After a forward that saw a stale generation: every slot it read is
+    // suspect, so none of them stays published (the next use refills).
+    void invalidate_read_slots(uint32_t layer, const Schedule &s);
+
     msi_status hold(uint32_t layer, uint32_t s);
     msi_status unhold(uint32_t layer, uint32_t s);
     msi_status reset();                        // epoch++ (MSI_E_BUSY with holds)

@@ -1,0 +1,172 @@
+"""Lifecycle fault cells through the C ABI on the GPU, after the paper's fault
+matrix (Table 5): each cell names the invariant it exercises and checks the
+required observation; every cell ends with a balanced terminal state (no fill
+in flight, no busy window, no live consumer).
+
+Faults are forced from the host (a bogus device generation word, a held
+consumer, a fill of an object outside the manifest, a reset while a fill is
+queued); no kernel is made to fault."""
+import numpy as np
+import pytest
+
+import synth
+from _gpu_helpers import device_layer, log, make_plan, run_layer
+
+pytestmark = pytest.mark.gpu
+
+WL = synth.Workload("cells_bf16", 13, synth.LayerShape(40, 256, 12, 3, 128, "bf16"),
+                    prior="dirichlet", prior_param=0.5, tau=0.4)
+
+
+@pytest.fixture(scope="module")
+def li():
+    return synth.layer_inputs(WL)
+
+
+@pytest.fixture(scope="module")
+def control(li):
+    """No-fault control: output of an all-resident plan."""
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=12, per_window=4)
+    out = run_layer(plan, dl)["out"].cpu().numpy()
+    plan.close()
+    return out
+
+
+def balanced(plan):
+    plan.poll()
+    st = plan.stats()
+    assert st["fills_in_flight"] == 0 and st["windows_busy"] == 0 and st["consumers_live"] == 0, st
+    return st
+
+
+def test_stale_generation_publishes_nothing(li, control):
+    """Stale completion / wrong version: mismatch rejected before visibility,
+    zero accepted outputs; the next forward refills and is exact."""
+    import torch
+    import paper_2608_23805_amd as msi
+    log("cell stale_generation")
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=12, per_window=4)
+    res = run_layer(plan, dl)                                   # warm: every demanded expert resident
+    demanded = np.nonzero(res["counts"])[0]
+    slot = next(s for s in range(12) if plan.query(0, s).expert == int(demanded[0]))
+    info = plan.query(0, slot)
+    plan.debug_set_device_gen(0, slot, info.generation + 1000)
+    canary = torch.full((WL.shape.T, WL.shape.d), 12345.0, device="cuda")
+    res = run_layer(plan, dl, out=canary, check=False)
+    assert res["status"] == msi.MSI_E_STALE
+    assert torch.all(canary == 12345.0), "output written despite a stale slot"
+    st = balanced(plan)
+    assert st["stale_detected"] == 1
+    res = run_layer(plan, dl)                                   # refilled, exact
+    assert res["out"].cpu().numpy().tobytes() == control.tobytes()
+    balanced(plan)
+    plan.close()
+
+
+def test_held_consumer_delays_reuse(li, control):
+    """Held consumer: no reuse before consumers finish; full control-exact
+    output and balanced release."""
+    import paper_2608_23805_amd as msi
+    log("cell held_consumer")
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=3, per_window=4)             # 3 slots < demand: rounds, evictions
+    t = plan.slot_fill(0, 5, slot=1)
+    plan.poll()
+    plan.hold(0, 1)
+    with pytest.raises(msi.MsiError) as e:
+        plan.slot_fill(0, 6, slot=1)
+    assert e.value.status == msi.MSI_E_BUSY
+    out = run_layer(plan, dl)["out"].cpu().numpy()
+    assert out.tobytes() == control.tobytes()
+    info = plan.query(0, 1)
+    assert info.expert == 5 and info.generation == t.generation and info.holds == 1   # never reused
+    with pytest.raises(msi.MsiError) as e:
+        plan.reset()                                            # reset with a live consumer
+    assert e.value.status == msi.MSI_E_BUSY
+    assert plan.destroy_status() == msi.MSI_E_BUSY              # shutdown with a live consumer
+    plan.unhold(0, 1)
+    balanced(plan)
+    plan.close()
+
+
+def test_wrong_object_rejected(li):
+    """Wrong object: a request outside the manifest is rejected, and a forward
+    demanding an object with no extent publishes nothing."""
+    import torch
+    import paper_2608_23805_amd as msi
+    log("cell wrong_object")
+    dl = device_layer(li)
+    counts = run_layer(make_plan(li, capacity=12, per_window=4), dl)["counts"]
+    missing = int(np.argmax(counts))                            # a demanded expert
+    keep = [e for e in range(WL.shape.E) if e != missing]
+    plan = make_plan(li, capacity=12, per_window=4, experts=keep)
+    with pytest.raises(msi.MsiError) as e:
+        plan.slot_fill(0, missing)
+    assert e.value.status == msi.MSI_E_WRONG_OBJECT
+    with pytest.raises(msi.MsiError) as e:
+        plan.slot_fill(0, keep[0], slot=99)
+    assert e.value.status == msi.MSI_E_WRONG_OBJECT
+    canary = torch.full((WL.shape.T, WL.shape.d), -7.0, device="cuda")
+    res = run_layer(plan, dl, out=canary, check=False)
+    assert res["status"] == msi.MSI_E_WRONG_OBJECT
+    assert torch.all(canary == -7.0)
+    balanced(plan)
+    plan.close()
+
+
+def test_reset_with_inflight_fill(li, control):
+    """Reset with outstanding work: the late completion does not publish; the
+    next forward refills and is exact."""
+    import torch
+    log("cell reset_inflight")
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=12, per_window=4)
+    side = torch.cuda.Stream()
+    t = plan.slot_fill(0, 2, side_stream=side)                  # queued, not yet observed
+    plan.reset()
+    torch.cuda.synchronize()
+    plan.poll()
+    info = plan.query(0, t.slot)
+    assert info.state == 0 and info.expert == -1                # Vacant: never published
+    st = plan.stats()
+    assert st["fills_discarded"] == 1 and st["epoch"] == 1
+    assert run_layer(plan, dl)["out"].cpu().numpy().tobytes() == control.tobytes()
+    balanced(plan)
+    plan.close()
+
+
+def test_out_of_order_fills_exact(li, control):
+    """Valid out-of-order completion: fills on two side streams in opposite
+    orders complete in any order and the output stays control-exact."""
+    import torch
+    log("cell out_of_order")
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=12, per_window=4)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for e in range(WL.shape.E):
+        plan.slot_fill(0, e, side_stream=s1 if e % 2 else s2)
+    torch.cuda.synchronize()
+    plan.poll()
+    st = plan.stats()
+    assert st["fills_published"] == WL.shape.E
+    out = run_layer(plan, dl)["out"].cpu().numpy()
+    assert out.tobytes() == control.tobytes()
+    assert plan.stats()["fills"] == WL.shape.E                  # everything was a hit
+    balanced(plan)
+    plan.close()
+
+
+def test_explicit_fill_hit_keeps_generation(li):
+    log("cell fill_hit")
+    plan = make_plan(li, capacity=4, per_window=4)
+    a = plan.slot_fill(0, 3)
+    b = plan.slot_fill(0, 3)
+    assert b.hit == 1 and b.slot == a.slot and b.generation == a.generation
+    c = plan.slot_fill(0, 3, slot=(a.slot + 1) % 4)             # forced elsewhere: a new version
+    assert c.hit == 0 and c.generation >= 1
+    import torch
+    torch.cuda.synchronize()
+    balanced(plan)
+    plan.close()
