@@ -140,9 +140,9 @@ def bench_decode_lru(args, cs, side):
     return res
 
 
-def bench_prefill(args, cs, side):
+def bench_prefill(args, cs, side, name="prefill_bf16"):
     import synth
-    wl = synth.WORKLOADS["prefill_bf16"]
+    wl = synth.WORKLOADS[name]
     s = wl.shape
     li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=1)
     plan.set_timing(True)
@@ -157,16 +157,30 @@ def bench_prefill(args, cs, side):
     achieved = flops_gu / (avg_gu * 1e-3) / 1e12
     kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 1)} for k, (n, v) in t.items() if n}
     plan.close()
-    res = dict(value=round(s.T / (ms * 1e-3), 1), unit="routed tokens/s per layer", ms_per_step=round(ms, 3),
+    res = dict(workload=name, value=round(s.T / (ms * 1e-3), 1), unit="routed tokens/s per layer",
+               ms_per_step=round(ms, 3),
                T=s.T, layer_tflops=round(layer_flops / (ms * 1e-3) / 1e12, 1),
                layer_mfma_frac=round(layer_flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
                roofline={"bound": "mfma", "kernel": "tile_gemm_kernel<GateUp>", "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
-                         "flops_per_launch": flops_gu, "avg_launch_us": round(avg_gu * 1e3, 1)},
+                         "flops_per_launch": flops_gu, "avg_launch_us": round(avg_gu * 1e3, 1),
+                         "note": "int4 weights unpacked to bf16 MFMA operands" if s.wdtype == "q4b32" else ""},
                kernels=kernels)
     log(f"[bench] prefill: {ms:.3f} ms/step, {res['value']:.0f} tok/s, layer {res['layer_tflops']} TFLOP/s, "
         f"gate/up {avg_gu * 1e3:.0f} us = {achieved:.0f} TFLOP/s")
+    return res
+
+
+def bench_decode_q4(args, cs, side):
+    """T = 1 decode with 4-bit experts: ~21 MB of weights per step, launch-bound."""
+    import synth
+    wl = synth.WORKLOADS["decode_q4"]
+    li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=16)
+    ms = _run(plan, xs, dev, r, ws, out, args.steps, args.warmup, cs, side)
+    plan.close()
+    res = dict(workload="decode_q4", ms=round(ms, 4), tokens_per_s=round(wl.shape.T / (ms * 1e-3), 1))
+    log(f"[bench] decode_q4: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s")
     return res
 
 
@@ -197,7 +211,7 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=10)
     ap.add_argument("--lru-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode")
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
@@ -218,6 +232,9 @@ def main():
         extra["decode_lru64"] = bench_decode_lru(args, cs, side)
     if "prefill" not in skip:
         extra["prefill"] = bench_prefill(args, cs, side)
+    if "q4" not in skip:
+        extra["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
+        extra["decode_q4"] = bench_decode_q4(args, cs, side)
     cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds)
 
     s = li.wl.shape

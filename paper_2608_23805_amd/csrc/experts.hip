@@ -386,6 +386,8 @@ hipError_t init_kernel_attributes()
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
     if (e == hipSuccess)
         e = init_route_attributes();
+    if (e == hipSuccess)
+        e = init_q4_attributes();
     return e;
 }
 

@@ -75,6 +75,17 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_gateup_f32(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_down_f32(const ExpertLaunch &L, hipStream_t s);
 
+// 4-bit block-quantized experts (experts_q4.hip)
+int tiles_gateup_q4_stream(int nrows, int d, int I);
+int tiles_down_q4_stream(int nrows, int d, int I);
+int tiles_gateup_q4_tile(int nrows, int d, int I);
+int tiles_down_q4_tile(int nrows, int d, int I);
+hipError_t launch_gateup_q4_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t init_q4_attributes();
+
 // ---- combine / publication and slot generation words (combine.hip)
 hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,
                           int T, int K, int d, hipStream_t s);

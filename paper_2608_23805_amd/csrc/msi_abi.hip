@@ -492,7 +492,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         return fail(sst, core.error());
 
     // ---- work tables: per round, gate/up and down launches of each path
-    enum Kind { GU_TILE, GU_STREAM, GU_F32, DN_TILE, DN_STREAM, DN_F32, NKIND };
+    enum Kind { GU_TILE, GU_STREAM, GU_F32, DN_TILE, DN_STREAM, DN_F32, GU_Q4T, GU_Q4S, DN_Q4T, DN_Q4S, NKIND };
     struct Launch {
         int kind;
         size_t off;
@@ -502,6 +502,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     std::vector<std::vector<Launch>> launches(sched.rounds.size());
     std::vector<WorkItem> table;
     const bool f32 = d.wdtype == MSI_W_F32;
+    const bool q4 = d.wdtype == MSI_W_Q4B32;
     auto add_launch = [&](size_t r, int kind, const std::vector<WorkItem> &items) {
         if (items.empty())
             return;
@@ -515,7 +516,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             case GU_F32: n = tiles_gateup_f32(w.nrows, D, I); break;
             case DN_TILE: n = tiles_down_tile(w.nrows, D, I); break;
             case DN_STREAM: n = tiles_down_stream(w.nrows, D, I); break;
-            default: n = tiles_down_f32(w.nrows, D, I); break;
+            case DN_F32: n = tiles_down_f32(w.nrows, D, I); break;
+            case GU_Q4T: n = tiles_gateup_q4_tile(w.nrows, D, I); break;
+            case GU_Q4S: n = tiles_gateup_q4_stream(w.nrows, D, I); break;
+            case DN_Q4T: n = tiles_down_q4_tile(w.nrows, D, I); break;
+            default: n = tiles_down_q4_stream(w.nrows, D, I); break;
             }
             w.tile0 = tiles;
             tiles += n;
@@ -538,10 +543,10 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
                        counts[si.expert], 0};
             (f32 || uint32_t(w.nrows) > thr ? tile_items : stream_items).push_back(w);
         }
-        add_launch(r, f32 ? GU_F32 : GU_TILE, tile_items);
-        add_launch(r, GU_STREAM, stream_items);
-        add_launch(r, f32 ? DN_F32 : DN_TILE, tile_items);
-        add_launch(r, DN_STREAM, stream_items);
+        add_launch(r, f32 ? GU_F32 : q4 ? GU_Q4T : GU_TILE, tile_items);
+        add_launch(r, q4 ? GU_Q4S : GU_STREAM, stream_items);
+        add_launch(r, f32 ? DN_F32 : q4 ? DN_Q4T : DN_TILE, tile_items);
+        add_launch(r, q4 ? DN_Q4S : DN_STREAM, stream_items);
     }
     if (table.size() > p->table_cap)
         return fail(MSI_E_INVALID_ARG, "internal: schedule table overflow");
@@ -615,7 +620,9 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             L.act_s = wsb + ws.act_s;
             L.ys = reinterpret_cast<float *>(wsb + ws.ys);
             static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
-                                             MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32};
+                                             MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32,
+                                             MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_DOWN_TILE,
+                                             MSI_K_DOWN_STREAM};
             const hipError_t e = p->timed_launch(tkind[l.kind], cs, [&] {
                 switch (l.kind) {
                 case GU_TILE: return launch_gateup_tile(L, cs);
@@ -623,7 +630,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
                 case GU_F32: return launch_gateup_f32(L, cs);
                 case DN_TILE: return launch_down_tile(L, cs);
                 case DN_STREAM: return launch_down_stream(L, cs);
-                default: return launch_down_f32(L, cs);
+                case DN_F32: return launch_down_f32(L, cs);
+                case GU_Q4T: return launch_gateup_q4_tile(L, cs);
+                case GU_Q4S: return launch_gateup_q4_stream(L, cs);
+                case DN_Q4T: return launch_down_q4_tile(L, cs);
+                default: return launch_down_q4_stream(L, cs);
                 }
             });
             if (e != hipSuccess) {

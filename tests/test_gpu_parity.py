@@ -216,3 +216,72 @@ def test_prefill_full_sampled(o):
     log(f"prefill sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
     _check_weights(res, ora, toks)
     plan.close()
+
+
+# ------------------------------------------------------------------ 4-bit block-quantized experts
+
+SMALL_Q4 = synth.Workload("small_q4", 14, synth.LayerShape(260, 512, 24, 4, 256, "q4b32"),
+                          prior="zipf", prior_param=1.5, tau=0.3)
+
+
+@pytest.fixture(scope="module")
+def small_q4():
+    return synth.layer_inputs(SMALL_Q4)
+
+
+def test_small_q4_layer_and_capacities(o, small_q4):
+    dl = device_layer(small_q4)
+    ref = None
+    for cap in (24, 6, 0):
+        log(f"case small_q4 capacity={cap}")
+        plan = make_plan(small_q4, capacity=cap, transient=4)
+        res = run_layer(plan, dl)
+        if ref is None:
+            counts = res["counts"]
+            log(f"small_q4 counts min={counts.min()} max={counts.max()} "
+                f"stream={((counts > 0) & (counts <= 16)).sum()} tile={(counts > 16).sum()}")
+            assert (counts > 128).any() and ((counts > 0) & (counts <= 16)).any()
+            toks = list(range(SMALL_Q4.shape.T))
+            err, near, ora = oracle_compare(o, small_q4, res, toks, TOL_BF16)
+            log(f"small_q4 err={err:.3e} near_ties={len(near)}")
+            _check_permutation(o, res, SMALL_Q4.shape.E)
+            ref = res["out"].cpu().numpy()
+        else:
+            assert res["out"].cpu().numpy().tobytes() == ref.tobytes(), cap
+        plan.close()
+
+
+def test_decode_q4_full(o):
+    wl = synth.WORKLOADS["decode_q4"]
+    li = synth.layer_inputs(wl)
+    dl = device_layer(li)
+    log("case decode_q4 T=1")
+    outs = []
+    for cap in (512, 0):
+        plan = make_plan(li, capacity=cap)
+        res = run_layer(plan, dl)
+        if cap == 512:
+            err, near, _ = oracle_compare(o, li, res, [0], TOL_BF16)
+            log(f"decode_q4 err={err:.3e} near_ties={len(near)}")
+        outs.append(res["out"].cpu().numpy())
+        plan.close()
+    assert outs[0].tobytes() == outs[1].tobytes()
+
+
+def test_prefill_q4_full_sampled(o):
+    wl = synth.WORKLOADS["prefill_q4"]
+    li = synth.layer_inputs(wl)
+    dl = device_layer(li)
+    log("case prefill_q4 T=32768 capacity=512")
+    plan = make_plan(li, capacity=512)
+    res = run_layer(plan, dl)
+    counts = res["counts"]
+    log(f"prefill_q4 counts min={counts.min()} max={counts.max()} zero={(counts == 0).sum()}")
+    _check_permutation(o, res, wl.shape.E)
+    g = np.random.default_rng(8)
+    busy = int(np.argmax(counts))
+    toks = sorted(set([0, wl.shape.T - 1] + g.choice(wl.shape.T, 30, replace=False).tolist()
+                      + res["perm"][res["offsets"][busy]:res["offsets"][busy] + 4].tolist()))
+    err, near, _ = oracle_compare(o, li, res, toks, TOL_BF16)
+    log(f"prefill_q4 sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
+    plan.close()
