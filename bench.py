@@ -184,6 +184,38 @@ def bench_decode_q4(args, cs, side):
     return res
 
 
+def bench_stack(args, cs, side):
+    """48-layer stack, T = 4096: one pass at capacities 0 and 64 (fills over
+    PCIe every layer), a cold and a warm pass at 512 (all resident)."""
+    import time as _t
+    import torch
+    import synth
+    from _stack import Stack
+    wl = synth.WORKLOADS["stack_bf16"]
+    pool = synth.layer_inputs(wl, layer=0)
+    res = {"workload": "stack_bf16 (48 layers, T=4096, Zipf(1.1), windows of 8 experts)"}
+    for cap in (0, 64, 512):
+        st = Stack(wl, capacity=cap, pool=pool)
+        passes = 2 if cap == 512 else 1
+        for p in range(passes):
+            torch.cuda.synchronize()
+            before = st.plan.stats()
+            t0 = _t.perf_counter()
+            st.run(compute=cs, side=side)
+            dt = _t.perf_counter() - t0
+            after = st.plan.stats()
+            h2d = after["h2d_bytes"] - before["h2d_bytes"]
+            key = f"capacity_{cap}" + ("_warm" if p == 1 else "")
+            res[key] = {"ms": round(dt * 1e3, 1), "tokens_per_s_per_layer": round(wl.shape.T * st.L / dt, 1),
+                        "fills": after["fills"] - before["fills"], "h2d_GB": round(h2d / 1e9, 2),
+                        "h2d_GBs": round(h2d / dt / 1e9, 1)}
+            log(f"[bench] stack {key}: {dt * 1e3:.0f} ms, H2D {h2d / dt / 1e9:.1f} GB/s")
+        st.close()
+        del st
+        torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(li, budget_s):
     """The fp64 oracle, as it stands, on the decode batch 0 (16 tokens), repeated
     until about budget_s seconds of wall time."""
@@ -211,7 +243,7 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=10)
     ap.add_argument("--lru-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4")
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4,stack")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
@@ -235,6 +267,8 @@ def main():
     if "q4" not in skip:
         extra["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
         extra["decode_q4"] = bench_decode_q4(args, cs, side)
+    if "stack" not in skip:
+        extra["stack"] = bench_stack(args, cs, side)
     cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds)
 
     s = li.wl.shape

@@ -297,6 +297,18 @@ msi_status msi_plan_stats(const msi_plan *plan, msi_stats *stats);
 msi_status msi_plan_set_timing(msi_plan *plan, int enable);
 msi_status msi_plan_timings(msi_plan *plan, msi_timings *out, int reset);
 
+/* Residual stream between stacked layers (attention omitted), row-major
+ * [rows, cols]: msi_residual_init sets h = float(x0); msi_residual_add does
+ * h += out.  Both then write the next layer's input x = bf16_rne(h / rms(h))
+ * per row, rms(h) = sqrt(mean(h^2) + 1e-6) summed in fp32 in a fixed order
+ * (an unweighted RMSNorm, as a transformer block normalizes its input; without
+ * it the gated FFN's quadratic response overflows a deep stack).  x0 and x
+ * may alias.  Device pointers, on `stream`. */
+msi_status msi_residual_init(const uint16_t *x0_bf16, float *h, uint16_t *x_bf16, uint32_t rows, uint32_t cols,
+                             void *stream);
+msi_status msi_residual_add(const float *out, float *h, uint16_t *x_bf16, uint32_t rows, uint32_t cols,
+                            void *stream);
+
 /* Test hook: overwrite one slot's device generation word (synchronously). */
 msi_status msi_debug_set_device_gen(msi_plan *plan, uint32_t layer, uint32_t slot, uint32_t gen);
 

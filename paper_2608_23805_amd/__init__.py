@@ -91,7 +91,7 @@ class msi_timings(ctypes.Structure):
     _fields_ = [("launches", _u64 * len(KERNEL_KINDS)), ("ms", ctypes.c_double * len(KERNEL_KINDS))]
 
 
-EXPORTS = ["msi_plan_set_timing", "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy", "msi_plan_reset",
+EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy", "msi_plan_reset",
            "msi_workspace_size", "msi_slot_fill", "msi_plan_poll", "msi_route", "msi_moe_forward",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
            "msi_debug_set_device_gen", "msi_stream_threshold"]
@@ -124,6 +124,8 @@ def _load():
     L.msi_plan_stats.argtypes = [_vp, P(msi_stats)]
     L.msi_debug_set_device_gen.argtypes = [_vp, _u32, _u32, _u32]
     L.msi_plan_set_timing.argtypes = [_vp, ctypes.c_int]
+    L.msi_residual_init.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
+    L.msi_residual_add.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
     L.msi_plan_timings.argtypes = [_vp, P(msi_timings), ctypes.c_int]
     L.msi_stream_threshold.argtypes = [_u32]
     L.msi_stream_threshold.restype = _u32
@@ -149,6 +151,16 @@ def last_error() -> str:
 
 def stream_threshold(v: int = 0) -> int:
     return int(lib.msi_stream_threshold(v))
+
+
+def residual_init(x0_bf16, h, x_bf16, stream=None):
+    """h = float(x0); x = bf16(rmsnorm(h)) per row (bf16 bits in int16 tensors, h float32 [rows, cols])."""
+    _check(lib.msi_residual_init(_ptr(x0_bf16), _ptr(h), _ptr(x_bf16), h.shape[0], h.shape[1], _stream(stream)))
+
+
+def residual_add(out, h, x_bf16, stream=None):
+    """h += out; x = bf16(rmsnorm(h)) per row."""
+    _check(lib.msi_residual_add(_ptr(out), _ptr(h), _ptr(x_bf16), h.shape[0], h.shape[1], _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -50,6 +50,42 @@ hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, f
     return hipGetLastError();
 }
 
+// Residual stream of a layer stack: h = float(x0) or h += out, then
+// x = bf16(h / sqrt(mean(h^2) + eps)) per row.  One 256-thread workgroup per
+// row; the sum of squares is reduced in a fixed order (per-thread strided
+// partial sums, then a wavefront tree, then the four wavefronts in order).
+__global__ void __launch_bounds__(256) residual_kernel(const uint16_t *__restrict__ x0,
+                                                       const float *__restrict__ out, float *__restrict__ h,
+                                                       uint16_t *__restrict__ x, int cols)
+{
+    __shared__ float part[4];
+    const int64_t row = blockIdx.x;
+    float *hr = h + row * cols;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < cols; c += blockDim.x) {
+        const float v = x0 ? bf16_to_f32(x0[row * cols + c]) : hr[c] + out[row * cols + c];
+        hr[c] = v;
+        ss = fmaf(v, v, ss);
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0)
+        part[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float ms = (((part[0] + part[1]) + part[2]) + part[3]) / float(cols);
+    const float inv = 1.0f / sqrtf(ms + 1e-6f);
+    for (int c = threadIdx.x; c < cols; c += blockDim.x)
+        x[row * cols + c] = f32_to_bf16(hr[c] * inv);
+}
+
+hipError_t launch_residual(const uint16_t *x0, const float *out, float *h, uint16_t *x, int rows, int cols,
+                           hipStream_t s)
+{
+    if (rows == 0 || cols == 0)
+        return hipSuccess;
+    residual_kernel<<<unsigned(rows), 256, 0, s>>>(x0, out, h, x, cols);
+    return hipGetLastError();
+}
+
 // Generation words are written with vector stores from one lane per entry.
 __global__ void set_gens_kernel(uint32_t *gen_dev, GenBatch b)
 {

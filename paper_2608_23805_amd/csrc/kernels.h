@@ -96,6 +96,9 @@ struct GenBatch {
     uint32_t value[GEN_BATCH];
 };
 hipError_t launch_set_gens(uint32_t *gen_dev, const GenBatch &b, hipStream_t s);
+// x0 != null: h = float(x0); else h += out.  Then x = bf16(rmsnorm(h)) per row.
+hipError_t launch_residual(const uint16_t *x0, const float *out, float *h, uint16_t *x, int rows, int cols,
+                           hipStream_t s);
 hipError_t launch_clear_word(uint32_t *word, hipStream_t s);
 
 }  // namespace msi

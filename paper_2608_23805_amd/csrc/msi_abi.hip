@@ -765,6 +765,23 @@ msi_status msi_plan_timings(msi_plan *p, msi_timings *out, int reset)
     return MSI_OK;
 }
 
+msi_status msi_residual_init(const uint16_t *x0, float *h, uint16_t *x, uint32_t rows, uint32_t cols,
+                             void *stream)
+{
+    if (uint64_t(rows) * cols && (!x0 || !h || !x))
+        return fail(MSI_E_INVALID_ARG, "null pointer");
+    HIP_OK(launch_residual(x0, nullptr, h, x, int(rows), int(cols), static_cast<hipStream_t>(stream)));
+    return MSI_OK;
+}
+
+msi_status msi_residual_add(const float *out, float *h, uint16_t *x, uint32_t rows, uint32_t cols, void *stream)
+{
+    if (uint64_t(rows) * cols && (!out || !h || !x))
+        return fail(MSI_E_INVALID_ARG, "null pointer");
+    HIP_OK(launch_residual(nullptr, out, h, x, int(rows), int(cols), static_cast<hipStream_t>(stream)));
+    return MSI_OK;
+}
+
 msi_status msi_debug_set_device_gen(msi_plan *p, uint32_t layer, uint32_t slot, uint32_t gen)
 {
     if (!p)

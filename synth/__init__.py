@@ -203,6 +203,16 @@ def router_weight(wl: Workload, layer: int = 0) -> np.ndarray:
     return encode_dense(g.standard_normal((s.E, s.d), dtype=np.float32) * np.float32(0.02), s.xdtype)
 
 
+def stack_expert_map(wl: Workload, layer: int) -> np.ndarray:
+    """Layer stacks draw their routed-expert objects from one pool of E
+    distinct seeded objects (pool object i = ``expert_object(wl, 0, i)``):
+    expert e of layer l is pool object map[e], with map a seeded permutation
+    per layer.  Host windows then hold E objects instead of n_layers * E."""
+    if layer == 0:
+        return np.arange(wl.shape.E)
+    return rng(wl.wid, layer, KIND_PERM, 1).permutation(wl.shape.E)
+
+
 def popularity_prior(wl: Workload, layer: int = 0) -> Optional[np.ndarray]:
     """Per-expert popularity p (sums to 1) or None for the unbiased workloads."""
     E = wl.shape.E
