@@ -207,7 +207,8 @@ typedef enum {
     MSI_K_SHARED = 8,          /* shared expert, gate/up and down                 */
     MSI_K_COMBINE = 9,
     MSI_K_FILL = 10,           /* one batch of slot fills on the side stream      */
-    MSI_NKERN = 11
+    MSI_K_WORKLIST = 11,       /* device-built work list of a forward             */
+    MSI_NKERN = 12
 } msi_kernel_kind;
 
 typedef struct {
@@ -290,7 +291,8 @@ msi_status msi_slot_unhold(msi_plan *plan, uint32_t layer, uint32_t slot);
 msi_status msi_slot_query(const msi_plan *plan, uint32_t layer, uint32_t slot, msi_slot_info *info);
 msi_status msi_plan_stats(const msi_plan *plan, msi_stats *stats);
 
-/* Telemetry: when enabled, every kernel launch of route/forward/fill on this
+/* Telemetry: enable = 0 off, 1 every kernel kind, otherwise a bit mask of
+ * (1 << msi_kernel_kind).  Each selected launch of route/forward/fill on this
  * plan is bracketed by two HIP events on its own stream; msi_plan_timings
  * waits for the recorded events, accumulates the elapsed times per kernel
  * kind into *out and, if reset != 0, clears the accumulators. */

@@ -84,7 +84,7 @@ class msi_stats(ctypes.Structure):
 
 
 KERNEL_KINDS = ["router_logits", "topk", "permute", "gateup_tile", "gateup_stream", "down_tile",
-                "down_stream", "expert_f32", "shared", "combine", "fill"]
+                "down_stream", "expert_f32", "shared", "combine", "fill", "worklist"]
 
 
 class msi_timings(ctypes.Structure):
@@ -327,8 +327,16 @@ class Plan:
         _check(lib.msi_plan_stats(self.h, ctypes.byref(s)))
         return {n: getattr(s, n) for n, _ in msi_stats._fields_ if n != "reserved"}
 
-    def set_timing(self, enable: bool):
-        _check(lib.msi_plan_set_timing(self.h, int(bool(enable))))
+    def set_timing(self, enable=True, kinds=None):
+        """Telemetry on/off; ``kinds`` (names of KERNEL_KINDS) restricts it."""
+        v = int(bool(enable))
+        if enable and kinds:
+            v = 0
+            for k in kinds:
+                v |= 1 << KERNEL_KINDS.index(k)
+            if v == 1:                      # kind 0 alone would read as "all"
+                v |= 1 << 31
+        _check(lib.msi_plan_set_timing(self.h, v))
 
     def timings(self, reset: bool = False) -> dict:
         """{kind: (launches, total_ms)} of the timing telemetry."""

@@ -25,7 +25,8 @@ struct alignas(16) u16x8 {
 constexpr int PERM_BLOCK = 256;
 
 // status word bits written by kernels that detect a problem
-constexpr uint32_t STATUS_STALE = 1u;
+constexpr uint32_t STATUS_STALE = 1u;   // a tile saw a slot generation it did not expect
+constexpr uint32_t STATUS_MISS = 2u;    // a demanded expert had no published slot (device work list)
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
@@ -122,6 +123,18 @@ __device__ __forceinline__ float wave_sum(float v)
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (uint64_t(1) << lane) - 1; }
+
+// Inclusive scan of part[0..1023] by a 1024-thread workgroup.
+__device__ __forceinline__ void block_scan_1024(int32_t *part)
+{
+    const int e = threadIdx.x;
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int v = e >= off ? part[e - off] : 0;
+        __syncthreads();
+        part[e] += v;
+        __syncthreads();
+    }
+}
 
 // Logical tile index with consecutive tiles kept on one XCD: hardware hands
 // workgroup b to XCD b % 8, so XCD x walks tiles [x*per, (x+1)*per).

@@ -166,9 +166,14 @@ template <int U>
 __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
-    if (!slot_current(it, L.gen_dev, L.status))
+    // with a device-built work list the grid is an upper bound: workgroups
+    // past the real tile count exit, and the XCD spread uses the real count
+    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
+    if (int(blockIdx.x) >= ntiles)
+        return;
+    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
+    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows;
     const int d = L.d, I = L.I, ldk = d + 8;
@@ -217,9 +222,14 @@ template <int U>
 __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t as[];
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
-    if (!slot_current(it, L.gen_dev, L.status))
+    // with a device-built work list the grid is an upper bound: workgroups
+    // past the real tile count exit, and the XCD spread uses the real count
+    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
+    if (int(blockIdx.x) >= ntiles)
+        return;
+    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
+    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows;
     const int d = L.d, I = L.I, ldk = I + 8;
@@ -277,6 +287,61 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
         stream_down_kernel<16><<<L.n_tiles, 256, lds, s>>>(L);
     else
         stream_down_kernel<4><<<L.n_tiles, 256, lds, s>>>(L);
+    return hipGetLastError();
+}
+
+// ============================================================== device work list
+
+__global__ void __launch_bounds__(1024) fast_worklist_kernel(const int32_t *__restrict__ counts,
+                                                             const int32_t *__restrict__ offsets,
+                                                             const int32_t *__restrict__ slot_of,
+                                                             const uint32_t *__restrict__ gen_of, int E, int T,
+                                                             int has_shared, int tpg, int tpd, WorkItem *gu,
+                                                             WorkItem *dn, int32_t *info, uint32_t *tail)
+{
+    __shared__ int32_t part[1024];
+    const int e = threadIdx.x;
+    const int c = e < E ? counts[e] : 0;
+    part[e] = c > 0 ? 1 : 0;
+    __syncthreads();
+    block_scan_1024(part);
+    const int base = has_shared ? 1 : 0;
+    bool miss = false;
+    if (c > 0) {
+        const int pos = base + part[e] - 1;
+        int32_t s = slot_of[e];
+        uint32_t g = gen_of[e];
+        int n = c;
+        if (s < 0) {            // not published: this forward will not publish; the item writes nothing
+            miss = true;
+            n = 0;
+        }
+        gu[pos] = WorkItem{e, s, g, offsets[e], n, pos * tpg};
+        dn[pos] = WorkItem{e, s, g, offsets[e], n, pos * tpd};
+    }
+    if (e == 0 && has_shared) {
+        gu[0] = WorkItem{-1, -1, 0u, 0, T, 0};
+        dn[0] = WorkItem{-1, -1, 0u, 0, T, 0};
+    }
+    const int any_miss = __syncthreads_or(miss ? 1 : 0);
+    if (e == 0) {
+        const int n = base + part[1023];
+        info[0] = n;
+        info[1] = n * tpg;
+        info[2] = n;
+        info[3] = n * tpd;
+        __hip_atomic_store(tail, any_miss ? STATUS_MISS : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (e < E)
+        tail[1 + e] = uint32_t(c);
+}
+
+hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
+                                const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
+                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s)
+{
+    fast_worklist_kernel<<<1, 1024, 0, s>>>(counts, offsets, slot_of, gen_of, E, T, has_shared, tpg, tpd, gu, dn,
+                                            info, tail);
     return hipGetLastError();
 }
 

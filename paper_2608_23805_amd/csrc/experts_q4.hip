@@ -119,9 +119,14 @@ __device__ __forceinline__ void q4_rows_dot(const uint8_t *__restrict__ nib, con
 __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
-    if (!slot_current(it, L.gen_dev, L.status))
+    // with a device-built work list the grid is an upper bound: workgroups
+    // past the real tile count exit, and the XCD spread uses the real count
+    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
+    if (int(blockIdx.x) >= ntiles)
+        return;
+    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
+    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8;
     const bool sh = it.slot < 0;
@@ -148,9 +153,14 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
 __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t as[];
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
-    if (!slot_current(it, L.gen_dev, L.status))
+    // with a device-built work list the grid is an upper bound: workgroups
+    // past the real tile count exit, and the XCD spread uses the real count
+    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
+    if (int(blockIdx.x) >= ntiles)
+        return;
+    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
+    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8;
     const bool sh = it.slot < 0;

@@ -58,6 +58,9 @@ struct ExpertLaunch {
     float *y;                    // [rows, d]
     const float *row_weight;     // per permuted row, or null (1.0)
     int d, I;
+    // device-built work list: {n_items, n_tiles} read by the kernel (the
+    // grid is an upper bound; workgroups past n_tiles exit), or null
+    const int32_t *dev_counts;
 };
 
 // tiles per item of each launch kind
@@ -85,6 +88,15 @@ hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t init_q4_attributes();
+
+// Device-built stream-path work list of one forward whose demanded experts
+// are all published (one workgroup): shared expert first, then demanded
+// experts in ascending id; a demanded expert without a published slot sets
+// STATUS_MISS and gets an item that writes nothing.  info = {n_gu, tiles_gu,
+// n_dn, tiles_dn}; tail = [status, counts[E]] for the host.
+hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
+                                const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
+                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s);
 
 // ---- combine / publication and slot generation words (combine.hip)
 hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,

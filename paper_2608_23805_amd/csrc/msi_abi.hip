@@ -91,7 +91,7 @@ struct msi_plan {
     PlanCore *core = nullptr;
     int device = 0;
     uint32_t *gen_dev = nullptr;        // [n_layers * pool_slots]
-    uint32_t *status_dev = nullptr;
+    uint32_t *status_dev = nullptr;     // [status, counts copy [E]] (device work-list path)
     WorkItem *table_dev = nullptr;
     WorkItem *table_host = nullptr;     // pinned staging
     size_t table_cap = 0;
@@ -103,12 +103,21 @@ struct msi_plan {
     std::vector<int64_t> fill_ev_id;    // fill id the pending event completes
     std::vector<hipEvent_t> release_ev; // per global slot: last round reading it (current forward)
     std::vector<uint8_t> fill_ev_shared;// event shared by a round batch (not owned per slot)
+    // device work-list path (all demanded experts published)
+    int32_t *res_slot_dev = nullptr;    // [n_layers][E] published global slot or -1
+    uint32_t *res_gen_dev = nullptr;    // [n_layers][E]
+    int32_t *res_host = nullptr;        // pinned staging [2 * E]
+    int32_t *info_dev = nullptr;        // {n_gu, tiles_gu, n_dn, tiles_dn}
+    uint32_t *tail_host = nullptr;      // pinned [1 + E]
+    std::vector<uint64_t> res_version;  // per layer: layer version uploaded
+    std::vector<uint8_t> direct_ok;     // per layer: last forward needed no fill
     // timing telemetry
     struct Timed {
         int kind;
         hipEvent_t a, b;
     };
     bool timing = false;
+    uint32_t timing_mask = 0;           // kernel kinds bracketed by events
     std::vector<Timed> timed;
     std::vector<hipEvent_t> tfree;
     uint64_t t_launches[MSI_NKERN] = {};
@@ -132,8 +141,10 @@ struct msi_plan {
     template <typename F>
     hipError_t timed_launch(int kind, hipStream_t s, F &&launch)
     {
-        if (!timing)
+        if (!timing || !(timing_mask & (1u << kind)))
             return launch();
+        if (timed.size() >= 8192)
+            resolve_timings();
         hipEvent_t a = get_tevent(), b = get_tevent();
         if (!a || !b)
             return hipErrorOutOfMemory;
@@ -295,16 +306,25 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         return cleanup(MSI_E_DEVICE, "no HIP device");
     if (init_kernel_attributes() != hipSuccess)
         return cleanup(MSI_E_DEVICE, "hipFuncSetAttribute failed");
+    const size_t E = desc->n_experts, NL = desc->n_layers;
+    p->res_version.assign(NL, 0);
+    p->direct_ok.assign(NL, 0);
     if (hipMalloc(&p->gen_dev, nslots * sizeof(uint32_t)) != hipSuccess ||
-        hipMalloc(&p->status_dev, 256) != hipSuccess ||
+        hipMalloc(&p->status_dev, sizeof(uint32_t) * (E + 64)) != hipSuccess ||
+        hipMalloc(&p->res_slot_dev, sizeof(int32_t) * E * NL) != hipSuccess ||
+        hipMalloc(&p->res_gen_dev, sizeof(uint32_t) * E * NL) != hipSuccess ||
+        hipMalloc(&p->info_dev, 64) != hipSuccess ||
         hipMalloc(&p->table_dev, p->table_cap * sizeof(WorkItem)) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "device allocation failed");
     if (hipHostMalloc(&p->table_host, p->table_cap * sizeof(WorkItem), hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc(&p->counts_host, sizeof(int32_t) * desc->n_experts, hipHostMallocDefault) != hipSuccess ||
-        hipHostMalloc(&p->status_host, 256, hipHostMallocDefault) != hipSuccess)
+        hipHostMalloc(&p->status_host, 256, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->res_host, sizeof(int32_t) * 2 * E, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->tail_host, sizeof(uint32_t) * (E + 1), hipHostMallocDefault) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "pinned host allocation failed");
     if (hipMemset(p->gen_dev, 0, nslots * sizeof(uint32_t)) != hipSuccess ||
-        hipMemset(p->status_dev, 0, 256) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+        hipMemset(p->status_dev, 0, sizeof(uint32_t) * (E + 64)) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess)
         return cleanup(MSI_E_DEVICE, "device initialisation failed");
     *out = p;
     return MSI_OK;
@@ -334,6 +354,16 @@ msi_status msi_plan_destroy(msi_plan *p)
         (void)hipFree(p->status_dev);
     if (p->table_dev)
         (void)hipFree(p->table_dev);
+    if (p->res_slot_dev)
+        (void)hipFree(p->res_slot_dev);
+    if (p->res_gen_dev)
+        (void)hipFree(p->res_gen_dev);
+    if (p->info_dev)
+        (void)hipFree(p->info_dev);
+    if (p->res_host)
+        (void)hipHostFree(p->res_host);
+    if (p->tail_host)
+        (void)hipHostFree(p->tail_host);
     if (p->table_host)
         (void)hipHostFree(p->table_host);
     if (p->counts_host)
@@ -469,6 +499,86 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     hipStream_t side = static_cast<hipStream_t>(side_stream);
     uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
     poll_fills(p);
+
+    // ---- layer entry, device work list: when the layer's last forward needed
+    // no fill and every expert takes the stream path (T <= threshold), the
+    // work list is built on the device from the counts and the published
+    // residency table, with no host round trip before the expert launches.
+    // A demanded expert without a published slot makes the attempt publish
+    // nothing (STATUS_MISS) and the forward continues on the scheduled path.
+    const bool f32w = d.wdtype == MSI_W_F32;
+    if (!core.zero_cache() && !f32w && T > 0 && uint32_t(T) <= g_stream_threshold && p->direct_ok[a->layer]) {
+        const uint32_t L0 = a->layer;
+        if (p->res_version[L0] != core.layer_version(L0)) {
+            core.published_map(L0, p->res_host, reinterpret_cast<uint32_t *>(p->res_host + E));
+            HIP_OK(hipMemcpyAsync(p->res_slot_dev + size_t(L0) * E, p->res_host, sizeof(int32_t) * E,
+                                  hipMemcpyHostToDevice, cs));
+            HIP_OK(hipMemcpyAsync(p->res_gen_dev + size_t(L0) * E, p->res_host + E, sizeof(uint32_t) * E,
+                                  hipMemcpyHostToDevice, cs));
+            p->res_version[L0] = core.layer_version(L0);
+        }
+        const bool q4w = d.wdtype == MSI_W_Q4B32;
+        const int tpg = q4w ? tiles_gateup_q4_stream(1, D, I) : tiles_gateup_stream(1, D, I);
+        const int tpd = q4w ? tiles_down_q4_stream(1, D, I) : tiles_down_stream(1, D, I);
+        const int has_sh = a->shared_object ? 1 : 0;
+        const int max_items = std::min(E, T * K) + has_sh;
+        WorkItem *gu = p->table_dev, *dn = p->table_dev + (E + 1);
+        HIP_OK(p->timed_launch(MSI_K_WORKLIST, cs, [&] {
+            return launch_fast_worklist(a->r.counts, a->r.offsets, p->res_slot_dev + size_t(L0) * E,
+                                        p->res_gen_dev + size_t(L0) * E, E, T, has_sh, tpg, tpd, gu, dn,
+                                        p->info_dev, p->status_dev, cs);
+        }));
+        ExpertLaunch X{};
+        X.x = a->x;
+        X.perm = a->r.perm;
+        X.wbase = static_cast<const uint8_t *>(d.slot_pool);
+        X.wstride = d.slot_stride;
+        X.gen_dev = p->gen_dev;
+        X.status = p->status_dev;
+        X.act = wsb + ws.act;
+        X.y = reinterpret_cast<float *>(wsb + ws.y);
+        X.row_weight = a->r.row_weight;
+        X.shared_w = static_cast<const uint8_t *>(a->shared_object);
+        X.act_s = wsb + ws.act_s;
+        X.ys = reinterpret_cast<float *>(wsb + ws.ys);
+        X.d = D;
+        X.I = I;
+        ExpertLaunch G = X, Dn = X;
+        G.items = gu;
+        G.n_tiles = max_items * tpg;
+        G.dev_counts = p->info_dev;
+        Dn.items = dn;
+        Dn.n_tiles = max_items * tpd;
+        Dn.dev_counts = p->info_dev + 2;
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs,
+                               [&] { return q4w ? launch_gateup_q4_stream(G, cs) : launch_gateup_stream(G, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
+                               [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
+            return launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
+                                  has_sh ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv, a->out,
+                                  p->status_dev, T, K, D, cs);
+        }));
+        HIP_OK(hipMemcpyAsync(p->tail_host, p->status_dev, sizeof(uint32_t) * (E + 1), hipMemcpyDeviceToHost, cs));
+        HIP_OK(hipStreamSynchronize(cs));
+        const uint32_t st = p->tail_host[0];
+        if (!(st & STATUS_MISS)) {
+            std::vector<int32_t> dem;
+            for (int e = 0; e < E; ++e)
+                if (p->tail_host[1 + e])
+                    dem.push_back(e);
+            if (st & STATUS_STALE) {
+                core.stats().stale_detected++;
+                core.stats().forwards++;
+                core.invalidate_experts(L0, dem);
+                p->direct_ok[L0] = 0;
+                return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
+            }
+            core.note_direct_hits(L0, dem);
+            return MSI_OK;
+        }
+        p->direct_ok[L0] = 0;       // a demanded expert was not resident: schedule it
+    }
 
     // ---- layer entry: the demanded set (one device-to-host read of the counts)
     HIP_OK(hipMemcpyAsync(p->counts_host, a->r.counts, sizeof(int32_t) * E, hipMemcpyDeviceToHost, cs));
@@ -689,13 +799,18 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     for (hipEvent_t e : round_events)
         p->free_events.push_back(e);
     core.end_forward(a->layer, sched);
-    if (p->timing)
-        p->resolve_timings();
+    {
+        bool filled = false;
+        for (const SchedRound &round : sched.rounds)
+            filled |= !round.fills.empty();
+        p->direct_ok[a->layer] = filled ? 0 : 1;
+    }
     if (rst != MSI_OK)
         return rst;
     if (*p->status_host & STATUS_STALE) {
         core.stats().stale_detected++;
         core.invalidate_read_slots(a->layer, sched);
+        p->direct_ok[a->layer] = 0;
         return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
     }
     return MSI_OK;
@@ -745,6 +860,7 @@ msi_status msi_plan_set_timing(msi_plan *p, int enable)
     if (!p)
         return fail(MSI_E_INVALID_ARG, "null plan");
     p->timing = enable != 0;
+    p->timing_mask = enable == 1 ? ~0u : uint32_t(enable);
     return MSI_OK;
 }
 

@@ -67,6 +67,54 @@ PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
     }
     slots_.assign(size_t(n_layers_) * pool_slots_, Slot{});
     window_busy_.assign(d.n_windows, 0);
+    layer_version_.assign(n_layers_, 1);
+}
+
+void PlanCore::published_map(uint32_t layer, int32_t *slot_of, uint32_t *gen_of) const
+{
+    for (uint32_t e = 0; e < n_experts_; ++e) {
+        slot_of[e] = -1;
+        gen_of[e] = 0;
+    }
+    if (zero_cache_)
+        return;
+    for (uint32_t s = 0; s < pool_slots_; ++s) {
+        const Slot &sl = slot(layer, s);
+        if (sl.expert < 0 || sl.fill_id >= 0)
+            continue;
+        if (sl.state == SlotState::DeviceReady || sl.state == SlotState::InUse ||
+            sl.state == SlotState::Recyclable) {
+            slot_of[sl.expert] = int32_t(global_slot(layer, s));
+            gen_of[sl.expert] = sl.gen;
+        }
+    }
+}
+
+void PlanCore::invalidate_experts(uint32_t layer, const std::vector<int32_t> &experts)
+{
+    for (int32_t e : experts) {
+        const int32_t s = resident_slot(layer, uint32_t(e));
+        if (s < 0)
+            continue;
+        Slot &sl = slot(layer, uint32_t(s));
+        if (sl.fill_id < 0 && sl.holds == 0 && sl.consumers == 0) {
+            sl.state = SlotState::Vacant;
+            sl.expert = -1;
+        }
+    }
+    layer_version_[layer]++;
+}
+
+void PlanCore::note_direct_hits(uint32_t layer, const std::vector<int32_t> &demanded)
+{
+    for (int32_t e : demanded) {
+        const int32_t s = resident_slot(layer, uint32_t(e));
+        if (s >= 0)
+            slot(layer, uint32_t(s)).last_use = ++tick_;
+        stats_.hits++;
+    }
+    stats_.rounds++;
+    stats_.forwards++;
 }
 
 const ObjectInfo *PlanCore::object(uint32_t layer, uint32_t expert) const
@@ -158,6 +206,7 @@ int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
     sl.epoch = epoch_;
     sl.state = SlotState::Loading;
     sl.fill_id = r.id;
+    layer_version_[layer]++;
     sl.last_use = ++tick_;
     window_busy_[o.window]++;
     stats_.fills++;
@@ -217,6 +266,7 @@ msi_status PlanCore::request_fill(uint32_t layer, uint32_t expert, int32_t force
             sl.fill_id < 0) {
             sl.state = SlotState::Vacant;
             sl.expert = -1;
+            layer_version_[layer]++;
         }
     }
     stats_.misses++;
@@ -238,6 +288,7 @@ void PlanCore::complete_fill(int64_t id)
     if (sl.fill_id != id)
         return;
     sl.fill_id = -1;
+    layer_version_[rec.layer]++;
     if (sl.state == SlotState::Loading && sl.gen == rec.gen && rec.epoch == epoch_) {
         publish_state(sl);
         stats_.fills_published++;
@@ -337,6 +388,7 @@ void PlanCore::end_forward(uint32_t layer, const Schedule &s)
                 (sl.state == SlotState::InUse || sl.state == SlotState::DeviceReady))
                 sl.state = SlotState::Recyclable;
         }
+    layer_version_[layer]++;
     if (zero_cache_)
         for (uint32_t s2 = 0; s2 < pool_slots_; ++s2) {
             Slot &sl = slot(layer, s2);
@@ -349,6 +401,7 @@ void PlanCore::end_forward(uint32_t layer, const Schedule &s)
 
 void PlanCore::invalidate_read_slots(uint32_t layer, const Schedule &s)
 {
+    layer_version_[layer]++;
     for (const SchedRound &r : s.rounds)
         for (const SchedItem &it : r.items) {
             Slot &sl = slot(layer, uint32_t(it.slot));

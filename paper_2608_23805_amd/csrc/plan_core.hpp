@@ -131,6 +131,18 @@ public:
 
     void set_error(msi_status st, const std::string &msg) { status_ = st; err_ = msg; }
 
+    // Bumped whenever a slot of the layer changes what it publishes.
+    uint64_t layer_version(uint32_t layer) const { return layer_version_[layer]; }
+    // Published (expert -> global slot, generation) of a layer: slot -1 when
+    // the expert has no published version (Loading versions are excluded).
+    void published_map(uint32_t layer, int32_t *slot_of, uint32_t *gen_of) const;
+    // A forward served entirely by published slots: count the hits and
+    // refresh the LRU ticks of the demanded experts' slots.
+    void note_direct_hits(uint32_t layer, const std::vector<int32_t> &demanded);
+    // After a stale generation seen on published slots: forget the listed
+    // experts' versions (the next use refills).
+    void invalidate_experts(uint32_t layer, const std::vector<int32_t> &experts);
+
 private:
     int64_t new_fill(uint32_t layer, uint32_t s, uint32_t expert);
     void publish_state(Slot &sl);
@@ -146,6 +158,7 @@ private:
     std::vector<uint8_t> has_object_;
     std::vector<uint32_t> window_busy_;
     std::unordered_map<int64_t, FillRecord> fills_;   // unobserved fills
+    std::vector<uint64_t> layer_version_;
     int64_t next_fill_ = 0;
     msi_stats stats_{};
 };

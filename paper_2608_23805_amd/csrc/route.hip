@@ -245,18 +245,6 @@ __device__ __forceinline__ int rank_below(const uint32_t *row, int tl)
     return n + __popc(row[tl >> 5] & m);
 }
 
-// Inclusive scan of part[0..1023] by a 1024-thread workgroup.
-__device__ __forceinline__ void block_scan_1024(int32_t *part)
-{
-    const int e = threadIdx.x;
-    for (int off = 1; off < 1024; off <<= 1) {
-        const int v = e >= off ? part[e - off] : 0;
-        __syncthreads();
-        part[e] += v;
-        __syncthreads();
-    }
-}
-
 __global__ void __launch_bounds__(256) perm_hist_kernel(const int32_t *__restrict__ idx,
                                                         int32_t *__restrict__ blockhist, int T, int K, int E)
 {

@@ -158,6 +158,34 @@ def test_out_of_order_fills_exact(li, control):
     plan.close()
 
 
+def test_stale_generation_on_device_work_list(li, control):
+    """The same cell when the forward takes the device-built work list (all
+    demanded experts published): nothing is published, then recovery."""
+    import torch
+    import paper_2608_23805_amd as msi
+    log("cell stale_generation_direct")
+    T = 12                                              # <= 16 tokens: stream path, device work list
+    dl = device_layer(li)
+    dl.x = dl.x[:T]
+    plan = make_plan(li, capacity=12, per_window=4)
+    ref = run_layer(plan, dl, T=T)                      # fills
+    run_layer(plan, dl, T=T)                            # no fill: the next forward is eligible
+    before = plan.stats()["hits"]
+    res = run_layer(plan, dl, T=T)
+    assert res["out"].cpu().numpy().tobytes() == ref["out"].cpu().numpy().tobytes()
+    demanded = np.nonzero(res["counts"])[0]
+    slot = next(s for s in range(12) if plan.query(0, s).expert == int(demanded[-1]))
+    plan.debug_set_device_gen(0, slot, plan.query(0, slot).generation + 77)
+    canary = torch.full((T, WL.shape.d), 3.5, device="cuda")
+    bad = run_layer(plan, dl, T=T, out=canary, check=False)
+    assert bad["status"] == msi.MSI_E_STALE and torch.all(canary == 3.5)
+    again = run_layer(plan, dl, T=T)
+    assert again["out"].cpu().numpy().tobytes() == ref["out"].cpu().numpy().tobytes()
+    assert plan.stats()["hits"] > before
+    balanced(plan)
+    plan.close()
+
+
 def test_explicit_fill_hit_keeps_generation(li):
     log("cell fill_hit")
     plan = make_plan(li, capacity=4, per_window=4)

@@ -174,9 +174,10 @@ def test_decode_full_parity_and_capacities(o, dec):
         log(f"case decode_bf16 capacity={cap}")
         plan = make_plan(dec, capacity=cap)
         res = run_layer(plan, dl)
-        res2 = run_layer(plan, dl)
         outs[cap] = res["out"].cpu().numpy()
-        assert res2["out"].cpu().numpy().tobytes() == outs[cap].tobytes()
+        for _ in range(2):      # warm calls: at capacity 512 the last one runs the device work list
+            again = run_layer(plan, dl)
+            assert again["out"].cpu().numpy().tobytes() == outs[cap].tobytes()
         if cap == 512:
             toks = list(range(DEC.shape.T))
             err, near, ora = oracle_compare(o, dec, res, toks, TOL_BF16)
