@@ -207,9 +207,17 @@ class Routing:
                        perm=torch.empty(T * K, **i32), inv=torch.empty((T, K), **i32),
                        row_weight=torch.empty(T * K, **f32))
 
+    def __setattr__(self, name, value):
+        object.__setattr__(self, name, value)
+        if name != "_c":
+            object.__setattr__(self, "_c", None)     # arrays changed: marshal again
+
     def c(self) -> msi_routing:
-        return msi_routing(_ptr(self.idx), _ptr(self.weights), _ptr(self.counts), _ptr(self.offsets),
-                           _ptr(self.perm), _ptr(self.inv), _ptr(self.row_weight))
+        if getattr(self, "_c", None) is None:
+            object.__setattr__(self, "_c", msi_routing(
+                _ptr(self.idx), _ptr(self.weights), _ptr(self.counts), _ptr(self.offsets),
+                _ptr(self.perm), _ptr(self.inv), _ptr(self.row_weight)))
+        return self._c
 
 
 class Plan:

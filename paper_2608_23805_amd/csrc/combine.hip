@@ -11,9 +11,10 @@
 
 namespace msi {
 
-__global__ void __launch_bounds__(256) combine_kernel(const float *__restrict__ y, const float *__restrict__ ys,
-                                                      const int32_t *__restrict__ inv, float *__restrict__ out,
-                                                      const uint32_t *__restrict__ status, int T, int K, int d)
+// fp32 layers: y and ys in fp32, four columns per thread.
+__global__ void __launch_bounds__(256) combine_f32_kernel(const float *__restrict__ y, const float *__restrict__ ys,
+                                                          const int32_t *__restrict__ inv, float *__restrict__ out,
+                                                          const uint32_t *__restrict__ status, int T, int K, int d)
 {
     if (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
         return;
@@ -24,29 +25,86 @@ __global__ void __launch_bounds__(256) combine_kernel(const float *__restrict__ 
     const int t = int(i / d4), c = int(i % d4) * 4;
     float4 acc = ys ? *reinterpret_cast<const float4 *>(ys + int64_t(t) * d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
     // all K row loads are issued before the fixed-order sum (K <= 16)
-    float4 v[16];
+    f32x4 v[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k)
         if (k < K)
-            v[k] = *reinterpret_cast<const float4 *>(y + int64_t(inv[int64_t(t) * K + k]) * d + c);
+            v[k] = *reinterpret_cast<const f32x4 *>(y + int64_t(inv[int64_t(t) * K + k]) * d + c);
 #pragma unroll
     for (int k = 0; k < 16; ++k)
         if (k < K) {
-            acc.x += v[k].x;
-            acc.y += v[k].y;
-            acc.z += v[k].z;
-            acc.w += v[k].w;
+            acc.x += v[k][0];
+            acc.y += v[k][1];
+            acc.z += v[k][2];
+            acc.w += v[k][3];
         }
     *reinterpret_cast<float4 *>(out + int64_t(t) * d + c) = acc;
 }
 
-hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,
-                          int T, int K, int d, hipStream_t s)
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// bf16 y and ys, eight columns per thread; the sum is in fp32 in the same
+// fixed order (shared expert, then the K routed rows in selection order).
+__global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict__ y, const uint16_t *__restrict__ ys,
+                                                      const int32_t *__restrict__ inv, float *__restrict__ out,
+                                                      const uint32_t *__restrict__ status, int T, int K, int d)
 {
-    const int64_t n = int64_t(T) * (d / 4);
-    if (n == 0)
-        return hipSuccess;
-    combine_kernel<<<unsigned((n + 255) / 256), 256, 0, s>>>(y, ys, inv, out, status, T, K, d);
+    if (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+        return;
+    const int d8 = d / 8;
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(T) * d8)
+        return;
+    const int t = int(i / d8), c = int(i % d8) * 8;
+    float a[8];
+    if (ys) {
+        const u32x4 s = *reinterpret_cast<const u32x4 *>(ys + int64_t(t) * d + c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            a[2 * q] = bf16_lo(s[q]);
+            a[2 * q + 1] = bf16_hi(s[q]);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            a[q] = 0.f;
+    }
+    u32x4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < K)
+            v[k] = *reinterpret_cast<const u32x4 *>(y + int64_t(inv[int64_t(t) * K + k]) * d + c);
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < K) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                a[2 * q] += bf16_lo(v[k][q]);
+                a[2 * q + 1] += bf16_hi(v[k][q]);
+            }
+        }
+    float4 *o = reinterpret_cast<float4 *>(out + int64_t(t) * d + c);
+    o[0] = make_float4(a[0], a[1], a[2], a[3]);
+    o[1] = make_float4(a[4], a[5], a[6], a[7]);
+}
+
+hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
+                          const uint32_t *status, int T, int K, int d, hipStream_t s)
+{
+    if (f32) {
+        const int64_t n = int64_t(T) * (d / 4);
+        if (n == 0)
+            return hipSuccess;
+        launch_k(combine_f32_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const float *>(y),
+                 static_cast<const float *>(ys), inv, out, status, T, K, d);
+    } else {
+        const int64_t n = int64_t(T) * (d / 8);
+        if (n == 0)
+            return hipSuccess;
+        launch_k(combine_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const uint16_t *>(y),
+                 static_cast<const uint16_t *>(ys), inv, out, status, T, K, d);
+    }
     return hipGetLastError();
 }
 
@@ -82,7 +140,7 @@ hipError_t launch_residual(const uint16_t *x0, const float *out, float *h, uint1
 {
     if (rows == 0 || cols == 0)
         return hipSuccess;
-    residual_kernel<<<unsigned(rows), 256, 0, s>>>(x0, out, h, x, cols);
+    launch_k(residual_kernel, unsigned(rows), 256, 0, s, x0, out, h, x, cols);
     return hipGetLastError();
 }
 
@@ -98,7 +156,7 @@ hipError_t launch_set_gens(uint32_t *gen_dev, const GenBatch &b, hipStream_t s)
 {
     if (b.n == 0)
         return hipSuccess;
-    set_gens_kernel<<<1, GEN_BATCH, 0, s>>>(gen_dev, b);
+    launch_k(set_gens_kernel, 1, GEN_BATCH, 0, s, gen_dev, b);
     return hipGetLastError();
 }
 
@@ -110,7 +168,7 @@ __global__ void clear_word_kernel(uint32_t *w)
 
 hipError_t launch_clear_word(uint32_t *word, hipStream_t s)
 {
-    clear_word_kernel<<<1, 64, 0, s>>>(word);
+    launch_k(clear_word_kernel, 1, 64, 0, s, word);
     return hipGetLastError();
 }
 

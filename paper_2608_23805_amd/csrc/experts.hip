@@ -10,7 +10,8 @@
 //
 // Every workgroup checks the slot generation first and writes nothing on a
 // mismatch (fail closed).  Outputs: act[row, I] = silu(x Wg^T) * (x Wu^T) and
-// y[row, d] = row_weight * (act Wd^T), rows in permuted order.
+// y[row, d] = row_weight * (act Wd^T), rows in permuted order, both rounded
+// to bf16 once (fp32 throughout for fp32 layers).
 #include "common.h"
 #include "gemm_tile.h"
 #include "kernels.h"
@@ -44,7 +45,7 @@ static TileArgs tile_args(const ExpertLaunch &L, bool gateup)
     p.wstride = L.wstride;
     p.shared_w = L.shared_w;
     p.a_s = reinterpret_cast<const uint16_t *>(L.act_s);
-    p.out_s = gateup ? L.act_s : static_cast<void *>(L.ys);
+    p.out_s = gateup ? L.act_s : L.ys;
     p.n_valid = 1 << 30;
     p.d = L.d;
     p.I = L.I;
@@ -71,7 +72,7 @@ hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    tile_gemm_kernel<TileMode::GateUp><<<L.n_tiles, tile::THREADS, tile::LDS_BYTES, s>>>(tile_args(L, true));
+    launch_k(tile_gemm_kernel<TileMode::GateUp>, L.n_tiles, tile::THREADS, tile::LDS_BYTES, s, tile_args(L, true));
     return hipGetLastError();
 }
 
@@ -79,7 +80,7 @@ hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    tile_gemm_kernel<TileMode::Down><<<L.n_tiles, tile::THREADS, tile::LDS_BYTES, s>>>(tile_args(L, false));
+    launch_k(tile_gemm_kernel<TileMode::Down>, L.n_tiles, tile::THREADS, tile::LDS_BYTES, s, tile_args(L, false));
     return hipGetLastError();
 }
 
@@ -107,7 +108,7 @@ hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, cons
     p.ldo = E;
     p.bias = bias;
     const int tiles = ((T + tile::BM - 1) / tile::BM) * p.n_tiles_n;
-    tile_gemm_kernel<TileMode::Router><<<tiles, tile::THREADS, tile::LDS_BYTES, s>>>(p);
+    launch_k(tile_gemm_kernel<TileMode::Router>, tiles, tile::THREADS, tile::LDS_BYTES, s, p);
     return hipGetLastError();
 }
 
@@ -143,21 +144,21 @@ __device__ __forceinline__ void stage_rows(uint16_t *xs, const uint16_t *__restr
     const int chunks = K / 8;
     const int total = n * chunks;
     for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {
-        uint4 v[8];
+        u32x4 v[8];     // ext-vector array: stays in registers
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int c = c0 + u * int(blockDim.x);
             if (c < total) {
                 const int j = c / chunks, q = c % chunks;
                 const int64_t r = perm ? int64_t(perm[row0 + j]) : int64_t(row0 + j);
-                v[u] = *reinterpret_cast<const uint4 *>(src + r * K + q * 8);
+                v[u] = *reinterpret_cast<const u32x4 *>(src + r * K + q * 8);
             }
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int c = c0 + u * int(blockDim.x);
             if (c < total)
-                *reinterpret_cast<uint4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
+                *reinterpret_cast<u32x4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
         }
     }
 }
@@ -261,8 +262,8 @@ __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
     if (live) {
         const int64_t row = it.row0 + j;
         const float w = sh ? 1.0f : L.row_weight[row];
-        float4 o = make_float4(acc[0] * w, acc[1] * w, acc[2] * w, acc[3] * w);
-        *reinterpret_cast<float4 *>((sh ? L.ys : L.y) + row * d + c0 + 4 * (lane >> 4)) = o;
+        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * (lane >> 4)) =
+            make_uint2(pack_bf16x2(acc[0] * w, acc[1] * w), pack_bf16x2(acc[2] * w, acc[3] * w));
     }
 }
 
@@ -272,9 +273,9 @@ hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     const size_t lds = size_t(stream::MAXN) * (L.d + 8) * sizeof(uint16_t);
     if (L.d % 256 == 0)
-        stream_gateup_kernel<8><<<L.n_tiles, 256, lds, s>>>(L);
+        launch_k(stream_gateup_kernel<8>, L.n_tiles, 256, lds, s, L);
     else
-        stream_gateup_kernel<1><<<L.n_tiles, 256, lds, s>>>(L);
+        launch_k(stream_gateup_kernel<1>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -284,9 +285,9 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     const size_t lds = size_t(stream::MAXN) * (L.I + 8) * sizeof(uint16_t);
     if (L.I % 512 == 0)
-        stream_down_kernel<16><<<L.n_tiles, 256, lds, s>>>(L);
+        launch_k(stream_down_kernel<16>, L.n_tiles, 256, lds, s, L);
     else
-        stream_down_kernel<4><<<L.n_tiles, 256, lds, s>>>(L);
+        launch_k(stream_down_kernel<4>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -340,8 +341,8 @@ hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, c
                                 const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
                                 WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s)
 {
-    fast_worklist_kernel<<<1, 1024, 0, s>>>(counts, offsets, slot_of, gen_of, E, T, has_shared, tpg, tpd, gu, dn,
-                                            info, tail);
+    launch_k(fast_worklist_kernel, 1, 1024, 0, s, counts, offsets, slot_of, gen_of, E, T, has_shared, tpg, tpd,
+             gu, dn, info, tail);
     return hipGetLastError();
 }
 
@@ -412,14 +413,14 @@ __global__ void __launch_bounds__(256) down_f32_kernel(ExpertLaunch L)
     for (int k = 0; k < I; ++k)
         acc = fmaf(a[k], wd[k], acc);
     const float w = sh ? 1.0f : L.row_weight[row];
-    (sh ? L.ys : L.y)[row * L.d + c] = acc * w;
+    static_cast<float *>(sh ? L.ys : L.y)[row * L.d + c] = acc * w;
 }
 
 hipError_t launch_gateup_f32(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    gateup_f32_kernel<<<L.n_tiles, 256, 0, s>>>(L);
+    launch_k(gateup_f32_kernel, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -427,7 +428,7 @@ hipError_t launch_down_f32(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    down_f32_kernel<<<L.n_tiles, 256, 0, s>>>(L);
+    launch_k(down_f32_kernel, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 

@@ -176,8 +176,8 @@ __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
     if (j < n) {
         const int64_t row = it.row0 + j;
         const float w = sh ? 1.0f : L.row_weight[row];
-        *reinterpret_cast<float4 *>((sh ? L.ys : L.y) + row * d + c0 + 4 * g) =
-            make_float4(acc[0] * w, acc[1] * w, acc[2] * w, acc[3] * w);
+        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * g) =
+            make_uint2(pack_bf16x2(acc[0] * w, acc[1] * w), pack_bf16x2(acc[2] * w, acc[3] * w));
     }
 }
 
@@ -185,7 +185,7 @@ hipError_t launch_gateup_q4_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    stream_gateup_q4_kernel<<<L.n_tiles, 256, size_t(16) * (L.d + 8) * 2, s>>>(L);
+    launch_k(stream_gateup_q4_kernel, L.n_tiles, 256, size_t(16) * (L.d + 8) * 2, s, L);
     return hipGetLastError();
 }
 
@@ -193,7 +193,7 @@ hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    stream_down_q4_kernel<<<L.n_tiles, 256, size_t(16) * (L.I + 8) * 2, s>>>(L);
+    launch_k(stream_down_q4_kernel, L.n_tiles, 256, size_t(16) * (L.I + 8) * 2, s, L);
     return hipGetLastError();
 }
 
@@ -372,11 +372,11 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
                     act[nt * 64 + wn * 32 + nb * 16 + r16] =
                         f32_to_bf16(silu(acc[mb][nb][rr]) * acc[mb][nb + 2][rr]);
             } else {
-                float *y = (sh ? L.ys : L.y) + orow * d;
+                uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + orow * d;
                 const float w = sh ? 1.0f : L.row_weight[orow];
 #pragma unroll
                 for (int nb = 0; nb < 4; ++nb)
-                    y[nt * BN + wn * 64 + nb * 16 + r16] = acc[mb][nb][rr] * w;
+                    y[nt * BN + wn * 64 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * w);
             }
         }
 }
@@ -385,7 +385,7 @@ hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    tile_q4_kernel<true><<<L.n_tiles, q4t::THREADS, q4t::LDS_BYTES, s>>>(L);
+    launch_k(tile_q4_kernel<true>, L.n_tiles, q4t::THREADS, q4t::LDS_BYTES, s, L);
     return hipGetLastError();
 }
 
@@ -393,7 +393,7 @@ hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    tile_q4_kernel<false><<<L.n_tiles, q4t::THREADS, q4t::LDS_BYTES, s>>>(L);
+    launch_k(tile_q4_kernel<false>, L.n_tiles, q4t::THREADS, q4t::LDS_BYTES, s, L);
     return hipGetLastError();
 }
 

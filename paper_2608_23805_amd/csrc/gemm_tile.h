@@ -52,7 +52,7 @@ struct TileArgs {
     WorkItem single;
     const uint32_t *gen_dev;
     uint32_t *status;
-    void *out;                  // L (fp32), act (bf16) or Y (fp32)
+    void *out;                  // L (fp32), act (bf16) or Y (bf16)
     int64_t ldo;                // elements per output row
     const float *bias;          // router bias or null
     const float *row_weight;    // gate weight per permuted row (down) or null (1.0)
@@ -250,6 +250,48 @@ __global__ void __launch_bounds__(tile::THREADS, 2) tile_gemm_kernel(TileArgs p)
         }
         return;
     }
+    if constexpr (MODE == TileMode::Down) {
+        // y = row_weight * acc in bf16, transposed through LDS in two halves
+        // of 64 columns so that each lane stores 16 contiguous bytes
+        constexpr int EP = 64 + 8;
+        uint16_t *ep = lds + wave * 64 * EP;
+        uint16_t *y = reinterpret_cast<uint16_t *>(outp);
+        float wrow[2][16];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                wrow[mb][r] = !rweight ? 1.0f : (m0 + row < it.nrows ? rweight[int64_t(it.row0) + m0 + row] : 0.f);
+            }
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int rl = mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+                    for (int nb = 0; nb < 2; ++nb)
+                        ep[rl * EP + nb * 32 + col_l] = f32_to_bf16(acc[mb][half * 2 + nb][r] * wrow[mb][r]);
+                }
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = lane + 64 * i;            // 512 chunks of 8 bf16
+                const int rl = c >> 3, q = c & 7;
+                const int row = wm * 64 + rl;
+                if (m0 + row < it.nrows)
+                    *reinterpret_cast<uint4 *>(y + (int64_t(it.row0) + m0 + row) * p.ldo + nt * BN + wn * 128 +
+                                               half * 64 + q * 8) =
+                        *reinterpret_cast<const uint4 *>(ep + rl * EP + q * 8);
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+        }
+        return;
+    }
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
@@ -258,20 +300,12 @@ __global__ void __launch_bounds__(tile::THREADS, 2) tile_gemm_kernel(TileArgs p)
             if (m0 + row >= it.nrows)
                 continue;
             const int64_t orow = int64_t(it.row0) + m0 + row;
-            if constexpr (MODE == TileMode::Down) {
-                float *y = reinterpret_cast<float *>(outp) + orow * p.ldo;
-                const float w = rweight ? rweight[orow] : 1.0f;
+            float *L = reinterpret_cast<float *>(p.out) + orow * p.ldo;
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb)
-                    y[nt * BN + wn * 128 + nb * 32 + col_l] = acc[mb][nb][r] * w;
-            } else {
-                float *L = reinterpret_cast<float *>(p.out) + orow * p.ldo;
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    const int col = nt * BN + wn * 128 + nb * 32 + col_l;
-                    if (col < p.n_valid)
-                        L[col] = acc[mb][nb][r] + (p.bias ? p.bias[col] : 0.f);
-                }
+            for (int nb = 0; nb < 4; ++nb) {
+                const int col = nt * BN + wn * 128 + nb * 32 + col_l;
+                if (col < p.n_valid)
+                    L[col] = acc[mb][nb][r] + (p.bias ? p.bias[col] : 0.f);
             }
         }
     }

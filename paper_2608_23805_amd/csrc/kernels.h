@@ -2,12 +2,42 @@
 // given stream; they return the launch error, if any).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <utility>
 
 #include "common.h"
 
 namespace msi {
+
+// Per-launch telemetry: while `stop` is set, kernels launched through
+// launch_k carry HIP events that the runtime records at the first kernel's
+// start and at each kernel's end (the last one's end is the one that stays),
+// so the measured span is the kernels' own execution, not the host's
+// enqueue gaps.
+struct LaunchTiming {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+inline LaunchTiming &launch_timing()
+{
+    static thread_local LaunchTiming t;
+    return t;
+}
+
+template <typename... KArgs, typename... Args>
+inline void launch_k(void (*k)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t s, Args &&...args)
+{
+    LaunchTiming &t = launch_timing();
+    if (t.stop) {
+        hipExtLaunchKernelGGL<KArgs...>(k, grid, block, uint32_t(lds), s, t.start, t.stop, 0u,
+                                        static_cast<KArgs>(std::forward<Args>(args))...);
+        t.start = nullptr;
+    } else {
+        k<<<grid, block, lds, s>>>(std::forward<Args>(args)...);
+    }
+}
 
 // ---- router and permutation (route.hip)
 hipError_t launch_router_logits_f32(const float *x, const float *wr, const float *bias, float *L, int T, int d,
@@ -28,13 +58,17 @@ inline hipError_t allow_large_lds(const void *f)
     return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                int(160 * 1024 - a.sharedSizeBytes));
 }
-// streaming router for T <= 16 tokens (bf16)
-hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T, int d,
-                                int E, hipStream_t s);
-// top-K + restricted softmax + permutation (one fused workgroup when T <= 256)
-hipError_t launch_route_select(const float *L, int32_t *idx, float *w, int32_t *counts, int32_t *offsets,
-                               int32_t *perm, int32_t *inv, float *row_weight, int32_t *blockhist, int T, int K,
-                               int E, hipStream_t s);
+// streaming router for 1 <= T <= 16 tokens (bf16): partial logits
+// P[ROUTER_SPLIT][T][E] without the bias
+constexpr int ROUTER_SPLIT = 4;
+hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, float *P, int T, int d, int E,
+                                hipStream_t s);
+// top-K + restricted softmax + permutation (one fused workgroup when T <= 256).
+// With P (T <= 16 only) the logits are formed from the partials plus the bias
+// and stored to L; otherwise they are read from L.
+hipError_t launch_route_select(float *L, const float *P, const float *bias, int32_t *idx, float *w,
+                               int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
+                               int32_t *blockhist, int T, int K, int E, hipStream_t s);
 hipError_t init_route_attributes();
 
 // ---- expert projections (experts.hip).  `items` lists the experts of one
@@ -51,11 +85,11 @@ struct ExpertLaunch {
     // are tokens (no gather), act / y go to act_s / ys, weight 1
     const uint8_t *shared_w;
     void *act_s;
-    float *ys;
+    void *ys;                    // [T, d] shared-expert output (bf16; f32 for f32 layers)
     const uint32_t *gen_dev;
     uint32_t *status;
     void *act;                   // [rows, I] bf16 (f32 for f32 layers)
-    float *y;                    // [rows, d]
+    void *y;                     // [rows, d] weighted expert outputs (bf16; f32 for f32 layers)
     const float *row_weight;     // per permuted row, or null (1.0)
     int d, I;
     // device-built work list: {n_items, n_tiles} read by the kernel (the
@@ -99,8 +133,9 @@ hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, c
                                 WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s);
 
 // ---- combine / publication and slot generation words (combine.hip)
-hipError_t launch_combine(const float *y, const float *ys, const int32_t *inv, float *out, const uint32_t *status,
-                          int T, int K, int d, hipStream_t s);
+// out[t] = ys[t] + sum_k y[inv[t, k]] in that order (y, ys bf16, or fp32 when f32)
+hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
+                          const uint32_t *status, int T, int K, int d, hipStream_t s);
 constexpr int GEN_BATCH = 64;
 struct GenBatch {
     uint32_t n;

@@ -56,7 +56,7 @@ uint64_t object_bytes_of(const msi_plan_desc &d)
 
 // Workspace layout for T tokens (offsets in bytes, each region 256-aligned).
 struct Workspace {
-    size_t logits, blockhist, act, act_s, y, ys, total;
+    size_t logits, parts, blockhist, act, act_s, y, ys, total;
 };
 
 Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
@@ -68,6 +68,8 @@ Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
     size_t off = 0;
     w.logits = off;
     off += align256(T * E * 4);
+    w.parts = off;              // router partial sums (T <= 16)
+    off += align256(T <= 16 ? ROUTER_SPLIT * T * E * 4 : 0);
     w.blockhist = off;
     off += align256(std::max<uint64_t>(nblk, 1) * E * 4);
     w.act = off;
@@ -75,9 +77,9 @@ Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
     w.act_s = off;
     off += align256(T * I * ab);
     w.y = off;
-    off += align256(T * K * D * 4);
+    off += align256(T * K * D * ab);    // y and ys: bf16 (fp32 for fp32 layers)
     w.ys = off;
-    off += align256(T * D * 4);
+    off += align256(T * D * ab);
     w.total = off;
     return w;
 }
@@ -137,10 +139,13 @@ struct msi_plan {
         return e;
     }
 
-    // Run `launch` bracketed by timing events on `s` when telemetry is on.
+    // Run `launch` with telemetry when it is on for this kind: the kernels it
+    // launches carry start / stop events recorded by the runtime at their own
+    // start and end.  A launch that started no kernel leaves no sample.
     template <typename F>
     hipError_t timed_launch(int kind, hipStream_t s, F &&launch)
     {
+        (void)s;
         if (!timing || !(timing_mask & (1u << kind)))
             return launch();
         if (timed.size() >= 8192)
@@ -148,9 +153,33 @@ struct msi_plan {
         hipEvent_t a = get_tevent(), b = get_tevent();
         if (!a || !b)
             return hipErrorOutOfMemory;
+        launch_timing() = LaunchTiming{a, b};
+        const hipError_t e = launch();
+        const bool used = launch_timing().start == nullptr;
+        launch_timing() = LaunchTiming{};
+        if (used)
+            timed.push_back(Timed{kind, a, b});
+        else {
+            tfree.push_back(a);
+            tfree.push_back(b);
+        }
+        return e;
+    }
+
+    // Copies are bracketed by events on their stream instead.
+    template <typename F>
+    hipError_t timed_copy(int kind, hipStream_t s, F &&copy)
+    {
+        if (!timing || !(timing_mask & (1u << kind)))
+            return copy();
+        if (timed.size() >= 8192)
+            resolve_timings();
+        hipEvent_t a = get_tevent(), b = get_tevent();
+        if (!a || !b)
+            return hipErrorOutOfMemory;
         hipError_t e = hipEventRecord(a, s);
         if (e == hipSuccess)
-            e = launch();
+            e = copy();
         if (e == hipSuccess)
             e = hipEventRecord(b, s);
         timed.push_back(Timed{kind, a, b});
@@ -454,26 +483,29 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
     float *L = reinterpret_cast<float *>(wsb + ws.logits);
+    float *P = nullptr;
     if (T > 0) {
         if (d.wdtype == MSI_W_F32)
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
                 return launch_router_logits_f32(static_cast<const float *>(a->x),
                                                 static_cast<const float *>(a->w_router), a->bias, L, T, D, E, s);
             }));
-        else if (T <= 16)
+        else if (T <= 16) {
+            P = reinterpret_cast<float *>(wsb + ws.parts);
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
                 return launch_router_stream(static_cast<const uint16_t *>(a->x),
-                                            static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s);
+                                            static_cast<const uint16_t *>(a->w_router), P, T, D, E, s);
             }));
-        else
+        } else
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
                 return launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
                                                  static_cast<const uint16_t *>(a->w_router), a->bias, L, T, D, E, s);
             }));
     }
     HIP_OK(p->timed_launch(MSI_K_TOPK, s, [&] {
-        return launch_route_select(L, a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm, a->r.inv,
-                                   a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s);
+        return launch_route_select(L, P, a->bias, a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm,
+                                   a->r.inv, a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K,
+                                   E, s);
     }));
     return MSI_OK;
 }
@@ -536,11 +568,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         X.gen_dev = p->gen_dev;
         X.status = p->status_dev;
         X.act = wsb + ws.act;
-        X.y = reinterpret_cast<float *>(wsb + ws.y);
+        X.y = wsb + ws.y;
         X.row_weight = a->r.row_weight;
         X.shared_w = static_cast<const uint8_t *>(a->shared_object);
         X.act_s = wsb + ws.act_s;
-        X.ys = reinterpret_cast<float *>(wsb + ws.ys);
+        X.ys = wsb + ws.ys;
         X.d = D;
         X.I = I;
         ExpertLaunch G = X, Dn = X;
@@ -555,8 +587,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
                                [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
-            return launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
-                                  has_sh ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv, a->out,
+            return launch_combine(wsb + ws.y, has_sh ? wsb + ws.ys : nullptr, false, a->r.inv, a->out,
                                   p->status_dev, T, K, D, cs);
         }));
         HIP_OK(hipMemcpyAsync(p->tail_host, p->status_dev, sizeof(uint32_t) * (E + 1), hipMemcpyDeviceToHost, cs));
@@ -681,7 +712,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             const SchedRound &round = sched.rounds[r];
             if (!round.fills.empty()) {
                 msi_status fst = MSI_OK;
-                const hipError_t fe_ = p->timed_launch(MSI_K_FILL, side, [&] {
+                const hipError_t fe_ = p->timed_copy(MSI_K_FILL, side, [&] {
                     fst = enqueue_fills(p, a->layer, round.fills, side);
                     return fst == MSI_OK ? hipSuccess : hipErrorUnknown;
                 });
@@ -724,11 +755,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             L.wbase = static_cast<const uint8_t *>(d.slot_pool);
             L.wstride = d.slot_stride;
             L.act = wsb + ws.act;
-            L.y = reinterpret_cast<float *>(wsb + ws.y);
+            L.y = wsb + ws.y;
             L.row_weight = a->r.row_weight;
             L.shared_w = static_cast<const uint8_t *>(a->shared_object);
             L.act_s = wsb + ws.act_s;
-            L.ys = reinterpret_cast<float *>(wsb + ws.ys);
+            L.ys = wsb + ws.ys;
             static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
                                              MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32,
                                              MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_DOWN_TILE,
@@ -769,8 +800,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     // ---- publication: out written only if every tile saw its generation
     if (rst == MSI_OK)
         if (p->timed_launch(MSI_K_COMBINE, cs, [&] {
-                return launch_combine(reinterpret_cast<const float *>(wsb + ws.y),
-                                      has_shared ? reinterpret_cast<const float *>(wsb + ws.ys) : nullptr, a->r.inv,
+                return launch_combine(wsb + ws.y, has_shared ? wsb + ws.ys : nullptr, f32w, a->r.inv,
                                       a->out, p->status_dev, T, K, D, cs);
             }) != hipSuccess)
             rst = fail(MSI_E_DEVICE, "combine launch failed");

@@ -68,6 +68,9 @@ PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
     slots_.assign(size_t(n_layers_) * pool_slots_, Slot{});
     window_busy_.assign(d.n_windows, 0);
     layer_version_.assign(n_layers_, 1);
+    res_index_.assign(size_t(n_layers_) * n_experts_, -1);
+    res_index_version_.assign(n_layers_, 0);
+    res_index_epoch_.assign(n_layers_, 0);
 }
 
 void PlanCore::published_map(uint32_t layer, int32_t *slot_of, uint32_t *gen_of) const
@@ -131,28 +134,42 @@ const FillRecord *PlanCore::fill(int64_t id) const
     return it == fills_.end() ? nullptr : &it->second;
 }
 
-int32_t PlanCore::resident_slot(uint32_t layer, uint32_t expert) const
+void PlanCore::rebuild_res_index(uint32_t layer) const
 {
-    if (zero_cache_)
-        return -1;
+    int32_t *ix = res_index_.data() + size_t(layer) * n_experts_;
+    std::fill(ix, ix + n_experts_, -1);
     for (uint32_t s = 0; s < pool_slots_; ++s) {
         const Slot &sl = slot(layer, s);
-        if (sl.expert != int32_t(expert))
+        if (sl.expert < 0 || ix[sl.expert] >= 0)
             continue;
         switch (sl.state) {
         case SlotState::DeviceReady:
         case SlotState::InUse:
         case SlotState::Recyclable:
-            return int32_t(s);
+            ix[sl.expert] = int32_t(s);
+            break;
         case SlotState::Loading:
             if (sl.epoch == epoch_)
-                return int32_t(s);   // usable once its ready event has completed
+                ix[sl.expert] = int32_t(s);   // usable once its ready event has completed
             break;
         default:
             break;
         }
     }
-    return -1;
+    res_index_version_[layer] = layer_version_[layer];
+    res_index_epoch_[layer] = epoch_;
+}
+
+// Every change of a slot's object, of Vacant / Loading / published, or of the
+// epoch moves the layer version or the epoch, so the table is current when
+// both match.
+int32_t PlanCore::resident_slot(uint32_t layer, uint32_t expert) const
+{
+    if (zero_cache_)
+        return -1;
+    if (res_index_version_[layer] != layer_version_[layer] || res_index_epoch_[layer] != epoch_)
+        rebuild_res_index(layer);
+    return res_index_[size_t(layer) * n_experts_ + expert];
 }
 
 int32_t PlanCore::choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude) const

@@ -159,6 +159,12 @@ private:
     std::vector<uint32_t> window_busy_;
     std::unordered_map<int64_t, FillRecord> fills_;   // unobserved fills
     std::vector<uint64_t> layer_version_;
+    // resident_slot lookup table per layer ([layer * E + expert] -> first
+    // qualifying slot), rebuilt when the layer's version or the epoch moved
+    mutable std::vector<int32_t> res_index_;
+    mutable std::vector<uint64_t> res_index_version_;   // 0: never built
+    mutable std::vector<uint32_t> res_index_epoch_;
+    void rebuild_res_index(uint32_t layer) const;
     int64_t next_fill_ = 0;
     msi_stats stats_{};
 };

@@ -14,6 +14,8 @@
 // and keys equal to it are taken in ascending expert id until K are chosen.
 // The selected experts come out in ascending id order from ballot prefix
 // counts, so no sort and no per-round cross-lane argmax is needed.
+#include <algorithm>
+
 #include "common.h"
 #include "gemm_tile.h"
 #include "kernels.h"
@@ -46,67 +48,53 @@ __global__ void __launch_bounds__(256) router_logits_f32_kernel(const float *__r
 }
 
 // ---------------------------------------------------------------- logits, bf16, T <= 16
-// Weight streaming: workgroup b owns experts 16b..16b+15; its four
-// wavefronts take quarters of d with the router rows as the 16x16x32 MFMA A
-// operand read straight from memory and the (<= 16) tokens as the B operand
-// from LDS; the four partial sums are added in wavefront order through LDS.
+// Weight streaming with the reduction split across workgroups: workgroup b
+// takes experts 16 (b % G) .. +15 and quarter b / G of the K steps of 32; its
+// four wavefronts take consecutive sixteenths of the K steps, so each lane
+// issues all of its loads at once (router rows as the 16x16x32 MFMA A operand,
+// token rows as the B operand, both straight from memory).  The wavefront
+// sums are added in wavefront order and the workgroup stores its partial
+// P[q][t][e]; the selection kernel adds the quarters in order and the bias.
 __global__ void __launch_bounds__(256) router_stream_kernel(const uint16_t *__restrict__ x,
-                                                            const uint16_t *__restrict__ wr,
-                                                            const float *__restrict__ bias, float *__restrict__ L,
+                                                            const uint16_t *__restrict__ wr, float *__restrict__ P,
                                                             int T, int d, int E)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];   // [16][d + 8]
-    __shared__ float red[3][64][4];
-    const int ldk = d + 8;
-    const int chunks = d / 8, total = T * chunks;
-    for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {   // loads batched 8 deep
-        uint4 v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total)
-                v[u] = *reinterpret_cast<const uint4 *>(x + int64_t(c / chunks) * d + (c % chunks) * 8);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total)
-                *reinterpret_cast<uint4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
-        }
-    }
-    __syncthreads();
+    __shared__ f32x4 red[3][64];
+    const int G = (E + 15) / 16;
+    const int g = int(blockIdx.x) % G, q = int(blockIdx.x) / G;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int e0 = blockIdx.x * 16;
-    const int row = e0 + (lane & 15);
+    const int nks = d / 32;
+    const int per = (nks + ROUTER_SPLIT * 4 - 1) / (ROUTER_SPLIT * 4);
+    const int s0 = min((q * 4 + wave) * per, nks), s1 = min(s0 + per, nks);
+    const int e0 = g * 16;
     const int j = lane & 15, kg = (lane >> 4) * 8;
-    const int kq = d / 4;
-    const bool rvalid = row < E, live = j < T;
-    const uint16_t *wp = wr + int64_t(rvalid ? row : 0) * d + wave * kq + kg;
-    const uint16_t *xr = xs + j * ldk + wave * kq + kg;
+    // rows past E and tokens past T read a valid row; their sums are never stored
+    const uint16_t *wp = wr + int64_t(min(e0 + j, E - 1)) * d + kg;
+    const uint16_t *xp = x + int64_t(min(j, T - 1)) * d + kg;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < kq; k0 += 32 * 8) {
-        u32x4 w[8];
+    for (int st = s0; st < s1; st += 4) {
+        u32x4 w[4], xv[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            w[u] = (rvalid && k0 + 32 * u < kq) ? load_stream16(wp + k0 + 32 * u) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            if (k0 + 32 * u >= kq)
-                break;
-            const uint4 xv = live ? *reinterpret_cast<const uint4 *>(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
-            acc = mfma16(as_bf16x8(w[u]), as_bf16x8(xv), acc);
+        for (int u = 0; u < 4; ++u) {
+            const int k = min(st + u, s1 - 1) * 32;       // clamped: no branch around the loads
+            w[u] = load_stream16(wp + k);
+            xv[u] = *reinterpret_cast<const u32x4 *>(xp + k);
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (st + u < s1)
+                acc = mfma16(as_bf16x8(w[u]), as_bf16x8(xv[u]), acc);
     }
     if (wave > 0)
-        for (int r = 0; r < 4; ++r)
-            red[wave - 1][lane][r] = acc[r];
+        red[wave - 1][lane] = acc;
     __syncthreads();
-    if (wave == 0 && live) {
+    if (wave == 0 && j < T) {
+        float *Pq = P + (int64_t(q) * T + j) * E;
+#pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float v = ((acc[r] + red[0][lane][r]) + red[1][lane][r]) + red[2][lane][r];
             const int e = e0 + 4 * (lane >> 4) + r;
             if (e < E)
-                L[int64_t(j) * E + e] = v + (bias ? bias[e] : 0.f);
+                Pq[e] = ((acc[r] + red[0][lane][r]) + red[1][lane][r]) + red[2][lane][r];
         }
     }
 }
@@ -122,84 +110,202 @@ __device__ __forceinline__ uint32_t order_key(float v)
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Selection of one token by one wavefront.  Lane l holds logits of experts
-// l + 64 j.  On return, sel_rank[j] is the output position (ascending id) of
-// expert l + 64 j, or -1, and w[j] its gate weight.
+// Radix select over PER keys per lane (absent entries hold key 0, below every
+// real key).  On return the K largest keys are those with (key & mask) >
+// prefix, plus the first `need` keys, in ascending id, with (key & mask) ==
+// prefix.  The scan stops as soon as every key matching the prefix is needed.
 template <int PER>
-__device__ __forceinline__ void wave_select(const float *__restrict__ Lrow, int E, int K, int lane, int *sel_rank,
-                                            float *w)
+__device__ __forceinline__ void radix_threshold(const uint32_t (&key)[PER], int K, uint32_t &prefix,
+                                                uint32_t &mask, int &need)
 {
-    float v[PER];
-    uint32_t key[PER];
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int e = lane + 64 * j;
-        v[j] = e < E ? Lrow[e] : -INFINITY;
-        key[j] = e < E ? order_key(v[j]) : 0u;    // 0 is below every real key
-    }
-    // radix select the K-th largest key
-    uint32_t prefix = 0u, mask = 0u;
-    int need = K;
-    for (int bit = 31; bit >= 0; --bit) {
+    prefix = 0u;
+    mask = 0u;
+    need = K;
+    int cur = PER * 64;             // keys matching the prefix so far
+    for (int bit = 31; bit >= 0 && cur != need; --bit) {
         const uint32_t b = 1u << bit, mk = mask | b, want = prefix | b;
         int cnt = 0;
 #pragma unroll
         for (int j = 0; j < PER; ++j)
             cnt += __popcll(__ballot((key[j] & mk) == want));
-        if (cnt >= need)
+        if (cnt >= need) {
             prefix = want;
-        else
+            cur = cnt;
+        } else {
             need -= cnt;
+            cur -= cnt;
+        }
         mask = mk;
     }
-    // keys above the threshold, then equal keys in ascending id, in id order
-    const uint64_t lt = lanemask_lt(lane);
-    int base = 0, eq_taken = 0;
-    float m = -INFINITY;
+}
+
+// Selection of one token by one wavefront.  Lane l holds the logits v[j] of
+// experts l + 64 j (j < PER).  emit(rank, expert, weight) is called once per
+// selected expert, rank = output position in ascending expert id.
+//
+// A threshold from the lane maxima comes first: every one of the K largest
+// logits is at least the K-th largest lane maximum, so only entries whose
+// masked key reaches that lane maximum's prefix are candidates.  When at most
+// 64 remain they are compacted (ascending id) into the wavefront's LDS row
+// and selected with one key per lane; otherwise all PER keys per lane are.
+template <int PER, typename Emit>
+__device__ __forceinline__ void wave_select(const float (&v)[PER], int E, int K, int lane, float *cand_v,
+                                            int32_t *cand_e, Emit emit)
+{
+    uint32_t key[PER];
+    uint32_t lm = 0u;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-        const bool gt = key[j] > prefix;
-        const bool eq = key[j] == prefix;
+        key[j] = lane + 64 * j < E ? order_key(v[j]) : 0u;
+        lm = max(lm, key[j]);
+    }
+    const uint64_t lt = lanemask_lt(lane);
+    uint32_t tp, tm;
+    int tn;
+    {
+        const uint32_t k1[1] = {lm};
+        radix_threshold<1>(k1, K, tp, tm, tn);
+    }
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        c += __popcll(__ballot(lane + 64 * j < E && (key[j] & tm) >= tp));
+    if (c <= 64) {
+        int base = 0;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const bool cd = lane + 64 * j < E && (key[j] & tm) >= tp;
+            const uint64_t bm = __ballot(cd);
+            if (cd) {
+                const int pos = base + __popcll(bm & lt);
+                cand_v[pos] = v[j];
+                cand_e[pos] = lane + 64 * j;
+            }
+            base += __popcll(bm);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        const float cv = lane < c ? cand_v[lane] : -INFINITY;
+        const int ce = lane < c ? cand_e[lane] : 0;
+        const uint32_t ck[1] = {lane < c ? order_key(cv) : 0u};
+        __builtin_amdgcn_wave_barrier();
+        uint32_t p, m;
+        int need;
+        radix_threshold<1>(ck, K, p, m, need);
+        const bool eq = (ck[0] & m) == p;
+        const bool sel = (ck[0] & m) > p || (eq && __popcll(__ballot(eq) & lt) < need);
+        const uint64_t selm = __ballot(sel);
+        const float mx = wave_max(sel ? cv : -INFINITY);
+        float w = sel ? expf(cv - mx) : 0.f;
+        const float sum = wave_sum(w);
+        w *= 1.0f / sum;
+        if (sel)
+            emit(__popcll(selm & lt), ce, w);
+        return;
+    }
+    uint32_t p, m;
+    int need;
+    radix_threshold<PER>(key, K, p, m, need);
+    int base = 0, eq_taken = 0, rank[PER];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const bool gt = (key[j] & m) > p;
+        const bool eq = (key[j] & m) == p;
         const uint64_t eqm = __ballot(eq);
         const bool sel = gt || (eq && eq_taken + __popcll(eqm & lt) < need);
         eq_taken += __popcll(eqm);
         const uint64_t selm = __ballot(sel);
-        sel_rank[j] = sel ? base + __popcll(selm & lt) : -1;
+        rank[j] = sel ? base + __popcll(selm & lt) : -1;
         base += __popcll(selm);
         if (sel)
-            m = fmaxf(m, v[j]);
+            mx = fmaxf(mx, v[j]);
     }
-    m = wave_max(m);
-    float s = 0.f;
+    mx = wave_max(mx);
+    float w[PER], sum = 0.f;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-        w[j] = sel_rank[j] >= 0 ? expf(v[j] - m) : 0.f;
-        s += w[j];
+        w[j] = rank[j] >= 0 ? expf(v[j] - mx) : 0.f;
+        sum += w[j];
     }
-    s = wave_sum(s);
-    const float inv = 1.0f / s;
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
 #pragma unroll
     for (int j = 0; j < PER; ++j)
-        w[j] *= inv;
+        if (rank[j] >= 0)
+            emit(rank[j], lane + 64 * j, w[j] * inv);
+}
+
+// Logits of token t for lane's experts lane + 64 j (-inf past E): read from
+// L, or formed from the ROUTER_SPLIT partials P (added in order, then the
+// bias) and stored to Lw.  Every load is issued, at a clamped index, before
+// any is used, so the row costs one memory round trip.
+template <int PER>
+__device__ __forceinline__ void load_logits(float (&v)[PER], const float *L, float *Lw, const float *__restrict__ P,
+                                            const float *__restrict__ bias, int t, int T, int E, int lane)
+{
+    int ec[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        ec[j] = min(lane + 64 * j, E - 1);
+    if (!P) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            v[j] = L[int64_t(t) * E + ec[j]];
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            if (lane + 64 * j >= E)
+                v[j] = -INFINITY;
+        return;
+    }
+    float pa[ROUTER_SPLIT][PER], bb[PER];
+#pragma unroll
+    for (int q = 0; q < ROUTER_SPLIT; ++q)
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            pa[q][j] = P[(int64_t(q) * T + t) * E + ec[j]];
+    if (bias) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            bb[j] = bias[ec[j]];
+    } else {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            bb[j] = 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        float a = pa[0][j];
+#pragma unroll
+        for (int q = 1; q < ROUTER_SPLIT; ++q)
+            a += pa[q][j];
+        v[j] = a + bb[j];
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        if (lane + 64 * j < E)
+            Lw[int64_t(t) * E + lane + 64 * j] = v[j];
+        else
+            v[j] = -INFINITY;
+    }
 }
 
 template <int PER>
 __global__ void __launch_bounds__(256) topk_kernel(const float *__restrict__ L, int32_t *__restrict__ idx,
                                                    float *__restrict__ wout, int T, int E, int K)
 {
-    const int lane = threadIdx.x & 63;
-    const int t = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    __shared__ float cand_v[4][64];
+    __shared__ int32_t cand_e[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int t = blockIdx.x * (blockDim.x >> 6) + wave;
     if (t >= T)
         return;
-    int rank[PER];
-    float w[PER];
-    wave_select<PER>(L + int64_t(t) * E, E, K, lane, rank, w);
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-        if (rank[j] >= 0) {
-            idx[int64_t(t) * K + rank[j]] = lane + 64 * j;
-            wout[int64_t(t) * K + rank[j]] = w[j];
-        }
+    float v[PER];
+    load_logits<PER>(v, L, nullptr, nullptr, nullptr, t, T, E, lane);
+    wave_select<PER>(v, E, K, lane, cand_v[wave], cand_e[wave], [&](int rank, int e, float w) {
+        idx[int64_t(t) * K + rank] = e;
+        wout[int64_t(t) * K + rank] = w;
+    });
 }
 
 // ---------------------------------------------------------------- permutation
@@ -311,68 +417,100 @@ __global__ void __launch_bounds__(256) perm_scatter_kernel(const int32_t *__rest
     }
 }
 
+// Inclusive scan of one value per thread of a 1024-thread workgroup:
+// wavefront scans, then the totals of the earlier wavefronts (integers, so
+// the grouping does not change the result).
+__device__ __forceinline__ int block_scan_incl_1024(int v, int32_t *wsum)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int u = __shfl_up(v, off, 64);
+        if (lane >= off)
+            v += u;
+    }
+    if (lane == 63)
+        wsum[wave] = v;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wave; ++w)
+        base += wsum[w];
+    return v + base;
+}
+
 // T <= PERM_BLOCK: top-K of every token (one wavefront per token), then the
-// histogram, scans and scatter, in one 1024-thread workgroup.  With
-// L == nullptr the selection is read from idx / w instead.
+// histogram, scans and scatter, in one 1024-thread workgroup, with a bitmask
+// of W = ceil(T / 32) words per expert.  The logits come from L, or, when P
+// is given, are formed here from the router's ROUTER_SPLIT partial sums
+// (added in order, then the bias) and stored to L.  With select == 0 the
+// selection is read from idx / w instead.
 template <int PER>
-__global__ void __launch_bounds__(1024) route_small_kernel(const float *__restrict__ L, int32_t *__restrict__ idx,
-                                                           float *__restrict__ w, int32_t *__restrict__ counts,
+__global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L, const float *__restrict__ P,
+                                                           const float *__restrict__ bias, int select,
+                                                           int32_t *__restrict__ idx, float *__restrict__ w,
+                                                           int32_t *__restrict__ counts,
                                                            int32_t *__restrict__ offsets, int32_t *__restrict__ perm,
                                                            int32_t *__restrict__ inv, float *__restrict__ row_weight,
                                                            int T, int K, int E)
 {
-    extern __shared__ uint32_t bits[];          // [E][PERM_BLOCK / 32]
-    __shared__ int32_t part[1024];
+    extern __shared__ uint32_t bits[];          // [E][W]
+    __shared__ int32_t excl[1024];              // first permuted row of each expert
+    __shared__ int32_t wsum[16];
     __shared__ int32_t sidx[PERM_BLOCK * 16];   // this workgroup's selection (T * K <= 4096)
     __shared__ float sw[PERM_BLOCK * 16];
+    __shared__ float cand_v[16][64];
+    __shared__ int32_t cand_e[16][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    clear_bits(bits, E);
+    const int W = (T + 31) >> 5;
+    for (int i = threadIdx.x; i < E * W; i += blockDim.x)
+        bits[i] = 0;
     __syncthreads();
-    if (L) {
+    if (select) {
         for (int t = wave; t < T; t += 16) {
-            int rank[PER];
-            float wv[PER];
-            wave_select<PER>(L + int64_t(t) * E, E, K, lane, rank, wv);
-#pragma unroll
-            for (int j = 0; j < PER; ++j)
-                if (rank[j] >= 0) {
-                    const int e = lane + 64 * j;
-                    idx[t * K + rank[j]] = e;
-                    w[t * K + rank[j]] = wv[j];
-                    sidx[t * K + rank[j]] = e;
-                    sw[t * K + rank[j]] = wv[j];
-                    atomicOr(&bits[e * (PERM_BLOCK / 32) + (t >> 5)], 1u << (t & 31));
-                }
+            float v[PER];
+            load_logits<PER>(v, L, L, P, bias, t, T, E, lane);
+            wave_select<PER>(v, E, K, lane, cand_v[wave], cand_e[wave], [&](int rank, int e, float wt) {
+                idx[t * K + rank] = e;
+                w[t * K + rank] = wt;
+                sidx[t * K + rank] = e;
+                sw[t * K + rank] = wt;
+                atomicOr(&bits[e * W + (t >> 5)], 1u << (t & 31));
+            });
         }
     } else {
         for (int a = threadIdx.x; a < T * K; a += blockDim.x) {
             const int t = a / K, e = idx[a];
             sidx[a] = e;
             sw[a] = w[a];
-            atomicOr(&bits[e * (PERM_BLOCK / 32) + (t >> 5)], 1u << (t & 31));
+            atomicOr(&bits[e * W + (t >> 5)], 1u << (t & 31));
         }
     }
     __syncthreads();
     const int e = threadIdx.x;
-    const int c = e < E ? row_popc(bits + e * (PERM_BLOCK / 32)) : 0;
-    part[e] = c;
-    __syncthreads();
-    block_scan_1024(part);
+    int c = 0;
+    if (e < E)
+        for (int q = 0; q < W; ++q)
+            c += __popc(bits[e * W + q]);
+    const int incl = block_scan_incl_1024(c, wsum);
+    excl[e] = incl - c;
     if (e < E) {
         counts[e] = c;
-        offsets[e] = part[e] - c;
+        offsets[e] = incl - c;
     }
     if (e == E - 1)
-        offsets[E] = part[e];
+        offsets[E] = incl;
     __syncthreads();
     for (int a = threadIdx.x; a < T * K; a += blockDim.x) {
         const int t = a / K;
         const int ee = sidx[a];
-        const int row = (part[ee] - row_popc(bits + ee * (PERM_BLOCK / 32))) +
-                        rank_below(bits + ee * (PERM_BLOCK / 32), t);
-        perm[row] = t;
-        inv[a] = row;
-        row_weight[row] = sw[a];
+        const uint32_t *row = bits + ee * W;
+        int r = excl[ee];
+        for (int q = 0; q < (t >> 5); ++q)
+            r += __popc(row[q]);
+        r += __popc(row[t >> 5] & ((1u << (t & 31)) - 1u));
+        perm[r] = t;
+        inv[a] = r;
+        row_weight[r] = sw[a];
     }
 }
 
@@ -385,7 +523,6 @@ hipError_t init_route_attributes()
         if (e == hipSuccess)
             e = allow_large_lds(f);
     };
-    set(reinterpret_cast<const void *>(&router_stream_kernel));
     set(reinterpret_cast<const void *>(&route_small_kernel<2>));
     set(reinterpret_cast<const void *>(&route_small_kernel<4>));
     set(reinterpret_cast<const void *>(&route_small_kernel<8>));
@@ -399,57 +536,62 @@ hipError_t launch_router_logits_f32(const float *x, const float *wr, const float
     const int64_t n = int64_t(T) * E;
     if (n == 0)
         return hipSuccess;
-    router_logits_f32_kernel<<<dim3(unsigned((n + 255) / 256)), dim3(256), 0, s>>>(x, wr, bias, L, T, d, E);
+    launch_k(router_logits_f32_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, x, wr, bias, L, T, d, E);
     return hipGetLastError();
 }
 
-hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T, int d,
-                                int E, hipStream_t s)
+hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, float *P, int T, int d, int E,
+                                hipStream_t s)
 {
-    const size_t lds = size_t(16) * (d + 8) * sizeof(uint16_t);
-    router_stream_kernel<<<unsigned((E + 15) / 16), 256, lds, s>>>(x, wr, bias, L, T, d, E);
+    if (T <= 0 || T > 16)
+        return hipErrorInvalidValue;
+    launch_k(router_stream_kernel, unsigned((E + 15) / 16 * ROUTER_SPLIT), 256, 0, s, x, wr, P, T, d, E);
     return hipGetLastError();
 }
 
 template <int PER>
-static void launch_route_small_t(const float *L, int32_t *idx, float *w, int32_t *counts, int32_t *offsets,
-                                 int32_t *perm, int32_t *inv, float *row_weight, int T, int K, int E, hipStream_t s)
+static void launch_route_small_t(float *L, const float *P, const float *bias, int32_t *idx, float *w,
+                                 int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
+                                 int T, int K, int E, hipStream_t s)
 {
-    const size_t lds = size_t(E) * (PERM_BLOCK / 32) * sizeof(uint32_t);
-    route_small_kernel<PER><<<1, 1024, lds, s>>>(L, idx, w, counts, offsets, perm, inv, row_weight, T, K, E);
+    const size_t lds = size_t(E) * std::max((T + 31) / 32, 1) * sizeof(uint32_t);
+    launch_k(route_small_kernel<PER>, 1, 1024, lds, s, L, P, bias, T > 0 ? 1 : 0, idx, w, counts, offsets, perm,
+             inv, row_weight, T, K, E);
 }
 
-hipError_t launch_route_select(const float *L, int32_t *idx, float *w, int32_t *counts, int32_t *offsets,
-                               int32_t *perm, int32_t *inv, float *row_weight, int32_t *blockhist, int T, int K,
-                               int E, hipStream_t s)
+hipError_t launch_route_select(float *L, const float *P, const float *bias, int32_t *idx, float *w,
+                               int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
+                               int32_t *blockhist, int T, int K, int E, hipStream_t s)
 {
     const int per = (E + 63) / 64;
     if (T <= PERM_BLOCK) {
         // T == 0 still writes zero counts and offsets
         if (per <= 2)
-            launch_route_small_t<2>(T ? L : nullptr, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<2>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
         else if (per <= 4)
-            launch_route_small_t<4>(T ? L : nullptr, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<4>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
         else if (per <= 8)
-            launch_route_small_t<8>(T ? L : nullptr, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<8>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
         else
-            launch_route_small_t<16>(T ? L : nullptr, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<16>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
         return hipGetLastError();
     }
+    if (P)
+        return hipErrorInvalidValue;      // partial logits are produced for T <= 16 only
     const dim3 grid(unsigned((T + 3) / 4)), block(256);
     if (per <= 2)
-        topk_kernel<2><<<grid, block, 0, s>>>(L, idx, w, T, E, K);
+        launch_k(topk_kernel<2>, grid, block, 0, s, L, idx, w, T, E, K);
     else if (per <= 4)
-        topk_kernel<4><<<grid, block, 0, s>>>(L, idx, w, T, E, K);
+        launch_k(topk_kernel<4>, grid, block, 0, s, L, idx, w, T, E, K);
     else if (per <= 8)
-        topk_kernel<8><<<grid, block, 0, s>>>(L, idx, w, T, E, K);
+        launch_k(topk_kernel<8>, grid, block, 0, s, L, idx, w, T, E, K);
     else
-        topk_kernel<16><<<grid, block, 0, s>>>(L, idx, w, T, E, K);
+        launch_k(topk_kernel<16>, grid, block, 0, s, L, idx, w, T, E, K);
     const size_t lds = size_t(E) * (PERM_BLOCK / 32) * sizeof(uint32_t);
     const int nblk = (T + PERM_BLOCK - 1) / PERM_BLOCK;
-    perm_hist_kernel<<<nblk, 256, lds, s>>>(idx, blockhist, T, K, E);
-    perm_scan_kernel<<<1, 1024, 0, s>>>(blockhist, nblk, E, counts, offsets);
-    perm_scatter_kernel<<<nblk, 256, lds, s>>>(idx, w, blockhist, offsets, perm, inv, row_weight, T, K, E);
+    launch_k(perm_hist_kernel, nblk, 256, lds, s, idx, blockhist, T, K, E);
+    launch_k(perm_scan_kernel, 1, 1024, 0, s, blockhist, nblk, E, counts, offsets);
+    launch_k(perm_scatter_kernel, nblk, 256, lds, s, idx, w, blockhist, offsets, perm, inv, row_weight, T, K, E);
     return hipGetLastError();
 }
 
