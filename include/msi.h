@@ -292,11 +292,17 @@ msi_status msi_slot_query(const msi_plan *plan, uint32_t layer, uint32_t slot, m
 msi_status msi_plan_stats(const msi_plan *plan, msi_stats *stats);
 
 /* Telemetry: enable = 0 off, 1 every kernel kind, otherwise a bit mask of
- * (1 << msi_kernel_kind).  Each selected launch of route/forward/fill on this
- * plan is bracketed by two HIP events on its own stream; msi_plan_timings
- * waits for the recorded events, accumulates the elapsed times per kernel
- * kind into *out and, if reset != 0, clears the accumulators. */
+ * (1 << msi_kernel_kind).  Each selected kernel launch of route/forward on
+ * this plan carries two HIP events that the runtime records at the start of
+ * its first kernel and the end of its last kernel; a fill (a copy) is
+ * bracketed by two events on the side stream.  msi_plan_timings waits for
+ * the recorded events, accumulates the elapsed times per kernel kind into
+ * *out and, if reset != 0, clears the accumulators.
+ * msi_plan_set_timing_period: time only every period-th launch of each kind
+ * (period >= 1, default 1), to keep the per-launch event cost off most
+ * launches; MSI_E_INVALID_ARG for period 0. */
 msi_status msi_plan_set_timing(msi_plan *plan, int enable);
+msi_status msi_plan_set_timing_period(msi_plan *plan, uint32_t period);
 msi_status msi_plan_timings(msi_plan *plan, msi_timings *out, int reset);
 
 /* Residual stream between stacked layers (attention omitted), row-major

@@ -91,7 +91,9 @@ class msi_timings(ctypes.Structure):
     _fields_ = [("launches", _u64 * len(KERNEL_KINDS)), ("ms", ctypes.c_double * len(KERNEL_KINDS))]
 
 
-EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy", "msi_plan_reset",
+EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_plan_set_timing_period",
+           "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy",
+           "msi_plan_reset",
            "msi_workspace_size", "msi_slot_fill", "msi_plan_poll", "msi_route", "msi_moe_forward",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
            "msi_debug_set_device_gen", "msi_stream_threshold"]
@@ -124,6 +126,7 @@ def _load():
     L.msi_plan_stats.argtypes = [_vp, P(msi_stats)]
     L.msi_debug_set_device_gen.argtypes = [_vp, _u32, _u32, _u32]
     L.msi_plan_set_timing.argtypes = [_vp, ctypes.c_int]
+    L.msi_plan_set_timing_period.argtypes = [_vp, _u32]
     L.msi_residual_init.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
     L.msi_residual_add.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
     L.msi_plan_timings.argtypes = [_vp, P(msi_timings), ctypes.c_int]
@@ -334,6 +337,10 @@ class Plan:
         s = msi_stats()
         _check(lib.msi_plan_stats(self.h, ctypes.byref(s)))
         return {n: getattr(s, n) for n, _ in msi_stats._fields_ if n != "reserved"}
+
+    def set_timing_period(self, period: int):
+        """Time only every period-th launch of each timed kind."""
+        _check(lib.msi_plan_set_timing_period(self.h, period))
 
     def set_timing(self, enable=True, kinds=None):
         """Telemetry on/off; ``kinds`` (names of KERNEL_KINDS) restricts it."""

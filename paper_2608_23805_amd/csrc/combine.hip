@@ -14,9 +14,13 @@ namespace msi {
 // fp32 layers: y and ys in fp32, four columns per thread.
 __global__ void __launch_bounds__(256) combine_f32_kernel(const float *__restrict__ y, const float *__restrict__ ys,
                                                           const int32_t *__restrict__ inv, float *__restrict__ out,
-                                                          const uint32_t *__restrict__ status, int T, int K, int d)
+                                                          const uint32_t *__restrict__ status, uint32_t *host_status, int T,
+                                                          int K, int d)
 {
-    if (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+    const uint32_t st = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (host_status && blockIdx.x == 0 && threadIdx.x == 0)
+        *host_status = st;         // pinned host word: read by the host after the stream completes
+    if (st != 0u)
         return;
     const int d4 = d / 4;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -48,9 +52,13 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // fixed order (shared expert, then the K routed rows in selection order).
 __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict__ y, const uint16_t *__restrict__ ys,
                                                       const int32_t *__restrict__ inv, float *__restrict__ out,
-                                                      const uint32_t *__restrict__ status, int T, int K, int d)
+                                                      const uint32_t *__restrict__ status, uint32_t *host_status, int T,
+                                                          int K, int d)
 {
-    if (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+    const uint32_t st = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (host_status && blockIdx.x == 0 && threadIdx.x == 0)
+        *host_status = st;         // pinned host word: read by the host after the stream completes
+    if (st != 0u)
         return;
     const int d8 = d / 8;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -90,20 +98,20 @@ __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict
 }
 
 hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
-                          const uint32_t *status, int T, int K, int d, hipStream_t s)
+                          const uint32_t *status, uint32_t *host_status, int T, int K, int d, hipStream_t s)
 {
     if (f32) {
         const int64_t n = int64_t(T) * (d / 4);
         if (n == 0)
             return hipSuccess;
         launch_k(combine_f32_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const float *>(y),
-                 static_cast<const float *>(ys), inv, out, status, T, K, d);
+                 static_cast<const float *>(ys), inv, out, status, host_status, T, K, d);
     } else {
         const int64_t n = int64_t(T) * (d / 8);
         if (n == 0)
             return hipSuccess;
         launch_k(combine_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const uint16_t *>(y),
-                 static_cast<const uint16_t *>(ys), inv, out, status, T, K, d);
+                 static_cast<const uint16_t *>(ys), inv, out, status, host_status, T, K, d);
     }
     return hipGetLastError();
 }

@@ -4,6 +4,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector
+// memory loads of the wavefront are outstanding; expcnt and lgkmcnt are left
+// at their maxima, i.e. not waited for.
+#define VMCNT_WAIT(n) ((((n) & 0xF) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
+
 namespace msi {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;

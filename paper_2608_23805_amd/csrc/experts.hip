@@ -134,57 +134,137 @@ int tiles_down_stream(int nrows, int d, int I)
     return d / (stream::WAVES * stream::ROWS);
 }
 
-// Stage the (<= 16) B-operand rows of one expert into LDS [16][K + 8].
-// Loads are issued in batches of 8 per thread before their LDS stores, so a
-// 64 KiB staging costs two memory round trips, not sixteen.
-__device__ __forceinline__ void stage_rows(uint16_t *xs, const uint16_t *__restrict__ src, const int32_t *perm,
-                                           int row0, int n, int K)
+// Stream-path prologue, ordered so that the dependent memory round trips
+// before the first MFMA are few: the item is found by division (every stream
+// item of a launch has the same tile count), the slot generation word is read
+// alongside and checked only before the store (a stale slot is read but
+// nothing is written), the token rows of the B operand are fetched before the
+// first weight batch is issued, and their LDS stores wait only for them.
+struct StreamTile {
+    WorkItem it;
+    int local;          // tile index within the item
+    bool valid;
+};
+
+__device__ __forceinline__ StreamTile stream_tile(const ExpertLaunch &L, int per_item)
 {
-    const int ldk = K + 8;
-    const int chunks = K / 8;
-    const int total = n * chunks;
-    for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {
-        u32x4 v[8];     // ext-vector array: stays in registers
+    StreamTile st{};
+    // with a device-built work list the grid is an upper bound: workgroups
+    // past the real tile count exit, and the XCD spread uses the real count
+    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
+    const int n_items = L.dev_counts ? L.dev_counts[0] : L.n_items;
+    if (int(blockIdx.x) >= ntiles)
+        return st;
+    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    const int i = t / per_item;
+    if (i >= n_items)
+        return st;
+    st.it = L.items[i];
+    st.local = t - i * per_item;
+    st.valid = st.it.nrows > 0;       // nrows 0: unpublished expert, no work
+    return st;
+}
+
+// Generation word of the tile's slot (read early, compared late).
+__device__ __forceinline__ uint32_t slot_gen_now(const WorkItem &it, const uint32_t *gen_dev)
+{
+    return it.slot < 0 ? it.gen : __hip_atomic_load(gen_dev + it.slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool slot_gen_ok(const WorkItem &it, uint32_t g, uint32_t *status)
+{
+    asm volatile("" : "+v"(g));     // the compare stays here, after the work: the load's wait is not hoisted
+    if (g == it.gen)
+        return true;
+    if (threadIdx.x == 0)
+        atomicOr(status, STATUS_STALE);
+    return false;
+}
+
+// B-operand rows of one expert (n <= 16) staged into LDS [16][K + 8]:
+// wavefront w handles rows w, w + 4, w + 8, w + 12, so each row's source
+// index is wavefront-uniform; lane l takes 16-byte chunks l, l + 64, ...
+// One pass covers 64 * CPL chunks of a row; rows longer than that take
+// further passes.
+template <int CPL>
+struct StageRows {
+    u32x4 v[4][CPL];
+
+    __device__ __forceinline__ void load(const uint16_t *__restrict__ src, const int32_t *perm, int row0, int n,
+                                         int K, int pass)
+    {
+        // the wavefront index is uniform: the row indices below are scalar
+        const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+        const int lane = threadIdx.x & 63, cpr = K / 8;
+        int64_t srow[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total) {
-                const int j = c / chunks, q = c % chunks;
-                const int64_t r = perm ? int64_t(perm[row0 + j]) : int64_t(row0 + j);
-                v[u] = *reinterpret_cast<const u32x4 *>(src + r * K + q * 8);
+        for (int q = 0; q < 4; ++q) {             // all source rows first (clamped, no branch)
+            const int r = min(wave + 4 * q, n - 1);
+            srow[q] = perm ? int64_t(perm[row0 + r]) : int64_t(row0 + r);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (wave + 4 * q < n) {
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int ch = lane + 64 * (pass * CPL + c);
+                    if (ch < cpr)
+                        v[q][c] = *reinterpret_cast<const u32x4 *>(src + srow[q] * K + ch * 8);
+                }
             }
         }
+    }
+
+    __device__ __forceinline__ void store(uint16_t *xs, int n, int K, int pass) const
+    {
+        const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+        const int lane = threadIdx.x & 63, cpr = K / 8;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total)
-                *reinterpret_cast<u32x4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
+        for (int q = 0; q < 4; ++q) {
+            const int r = wave + 4 * q;
+            if (r < n) {
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int ch = lane + 64 * (pass * CPL + c);
+                    if (ch < cpr)
+                        *reinterpret_cast<u32x4 *>(xs + r * (K + 8) + ch * 8) = v[q][c];
+                }
+            }
         }
     }
-}
+
+    // passes after the first (rows longer than 64 * CPL chunks)
+    __device__ __forceinline__ void rest(const uint16_t *__restrict__ src, const int32_t *perm, int row0, int n,
+                                         int K, uint16_t *xs)
+    {
+        for (int pass = 1; pass * 64 * CPL < K / 8; ++pass) {
+            load(src, perm, row0, n, K, pass);
+            store(xs, n, K, pass);
+        }
+    }
+};
 
 template <int U>
 __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
-    // with a device-built work list the grid is an upper bound: workgroups
-    // past the real tile count exit, and the XCD spread uses the real count
-    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
-    if (int(blockIdx.x) >= ntiles)
-        return;
-    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
-    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
-    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
-        return;
-    const int n = it.nrows;
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];   // [16][d + 8]
     const int d = L.d, I = L.I, ldk = d + 8;
+    const StreamTile st = stream_tile(L, I / (stream::WAVES * stream::ROWS));
+    if (!st.valid)
+        return;
+    const WorkItem &it = st.it;
+    const int n = it.nrows;
     const bool sh = it.slot < 0;
-    stage_rows(xs, reinterpret_cast<const uint16_t *>(L.x), sh ? nullptr : L.perm, it.row0, n, d);
-    __syncthreads();
+    const uint32_t gnow = slot_gen_now(it, L.gen_dev);
+    // the gathered token rows of x (the shared expert reads the tokens in order)
+    const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
+    const int32_t *xperm = sh ? nullptr : L.perm;
+    StageRows<4> sr;                              // one pass for d <= 2048
+    sr.load(xsrc, xperm, it.row0, n, d, 0);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int i0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
+    const int i0 = (st.local * stream::WAVES + wave) * stream::ROWS;
     const int j = lane & 15, kg = (lane >> 4) * 8;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + kg;
@@ -192,22 +272,45 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
     const uint16_t *xr = xs + j * ldk + kg;
     const bool live = j < n;
 
+    // Weight batches are double-buffered in registers: batch b + 1 is in
+    // flight while batch b is multiplied; batch 0 is issued before the token
+    // rows are written to LDS.
+    u32x4 wg[2][U], wu[2][U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        wg[0][u] = load_stream16(gp + 32 * u);
+        wu[0][u] = load_stream16(up + 32 * u);
+    }
+    sr.store(xs, n, d, 0);
+    sr.rest(xsrc, xperm, it.row0, n, d, xs);
+    __syncthreads();
+
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < d; k0 += 32 * U) {
-        u32x4 wg[U], wu[U];
+    const int nb = d / (32 * U);
+    for (int b = 0; b < nb; b += 2) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            wg[u] = load_stream16(gp + k0 + 32 * u);
-            wu[u] = load_stream16(up + k0 + 32 * u);
-        }
+        for (int h = 0; h < 2; ++h) {
+            if (b + h >= nb)
+                break;
+            const int k0 = (b + h) * 32 * U;
+            if (b + h + 1 < nb) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint4 xv = live ? *reinterpret_cast<const uint4 *>(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
-            const bf16x8 b = as_bf16x8(xv);
-            ag = mfma16(as_bf16x8(wg[u]), b, ag);
-            au = mfma16(as_bf16x8(wu[u]), b, au);
+                for (int u = 0; u < U; ++u) {
+                    wg[h ^ 1][u] = load_stream16(gp + k0 + 32 * U + 32 * u);
+                    wu[h ^ 1][u] = load_stream16(up + k0 + 32 * U + 32 * u);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint4 xv = live ? *reinterpret_cast<const uint4 *>(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
+                const bf16x8 bx = as_bf16x8(xv);
+                ag = mfma16(as_bf16x8(wg[h][u]), bx, ag);
+                au = mfma16(as_bf16x8(wu[h][u]), bx, au);
+            }
         }
     }
+    if (!slot_gen_ok(it, gnow, L.status))
+        return;
     // lane holds rows i0 + 4*(lane/16) + r of token j
     if (live) {
         uint2 v;
@@ -222,43 +325,53 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
 template <int U>
 __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t as[];
-    // with a device-built work list the grid is an upper bound: workgroups
-    // past the real tile count exit, and the XCD spread uses the real count
-    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
-    if (int(blockIdx.x) >= ntiles)
-        return;
-    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
-    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
-    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
-        return;
-    const int n = it.nrows;
+    extern __shared__ __attribute__((aligned(16))) uint16_t as[];   // [16][I + 8]
     const int d = L.d, I = L.I, ldk = I + 8;
+    const StreamTile st = stream_tile(L, d / (stream::WAVES * stream::ROWS));
+    if (!st.valid)
+        return;
+    const WorkItem &it = st.it;
+    const int n = it.nrows;
     const bool sh = it.slot < 0;
-    stage_rows(as, reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act), nullptr, it.row0, n, I);
-    __syncthreads();
+    const uint32_t gnow = slot_gen_now(it, L.gen_dev);
+    // the expert's act rows are contiguous
+    const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
+    StageRows<1> sr;                              // one pass for I <= 512
+    sr.load(asrc, nullptr, it.row0, n, I, 0);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int c0 = ((t - it.tile0) * stream::WAVES + wave) * stream::ROWS;
+    const int c0 = (st.local * stream::WAVES + wave) * stream::ROWS;
     const int j = lane & 15, kg = (lane >> 4) * 8;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *wp = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0 + j) * I + kg;
     const uint16_t *ar = as + j * ldk + kg;
     const bool live = j < n;
 
+    // the first weight batch is issued before the act rows are written to LDS
+    u32x4 w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        w[u] = load_stream16(wp + 32 * u);
+    sr.store(as, n, I, 0);
+    sr.rest(asrc, nullptr, it.row0, n, I, as);
+    __syncthreads();
+
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < I; k0 += 32 * U) {
-        u32x4 w[U];
+        if (k0 > 0) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            w[u] = load_stream16(wp + k0 + 32 * u);
+            for (int u = 0; u < U; ++u)
+                w[u] = load_stream16(wp + k0 + 32 * u);
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint4 av = live ? *reinterpret_cast<const uint4 *>(ar + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
             acc = mfma16(as_bf16x8(w[u]), as_bf16x8(av), acc);
         }
     }
+    if (!slot_gen_ok(it, gnow, L.status))
+        return;
     if (live) {
         const int64_t row = it.row0 + j;
         const float w = sh ? 1.0f : L.row_weight[row];
@@ -298,7 +411,8 @@ __global__ void __launch_bounds__(1024) fast_worklist_kernel(const int32_t *__re
                                                              const int32_t *__restrict__ slot_of,
                                                              const uint32_t *__restrict__ gen_of, int E, int T,
                                                              int has_shared, int tpg, int tpd, WorkItem *gu,
-                                                             WorkItem *dn, int32_t *info, uint32_t *tail)
+                                                             WorkItem *dn, int32_t *info, uint32_t *status,
+                                                             uint32_t *host_counts)
 {
     __shared__ int32_t part[1024];
     const int e = threadIdx.x;
@@ -331,18 +445,19 @@ __global__ void __launch_bounds__(1024) fast_worklist_kernel(const int32_t *__re
         info[1] = n * tpg;
         info[2] = n;
         info[3] = n * tpd;
-        __hip_atomic_store(tail, any_miss ? STATUS_MISS : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(status, any_miss ? STATUS_MISS : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     if (e < E)
-        tail[1 + e] = uint32_t(c);
+        host_counts[e] = uint32_t(c);     // pinned host words: the demanded set, read after the stream completes
 }
 
 hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
                                 const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
-                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s)
+                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *status, uint32_t *host_counts,
+                                hipStream_t s)
 {
     launch_k(fast_worklist_kernel, 1, 1024, 0, s, counts, offsets, slot_of, gen_of, E, T, has_shared, tpg, tpd,
-             gu, dn, info, tail);
+             gu, dn, info, status, host_counts);
     return hipGetLastError();
 }
 

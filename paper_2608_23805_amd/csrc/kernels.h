@@ -126,16 +126,20 @@ hipError_t init_q4_attributes();
 // Device-built stream-path work list of one forward whose demanded experts
 // are all published (one workgroup): shared expert first, then demanded
 // experts in ascending id; a demanded expert without a published slot sets
-// STATUS_MISS and gets an item that writes nothing.  info = {n_gu, tiles_gu,
-// n_dn, tiles_dn}; tail = [status, counts[E]] for the host.
+// STATUS_MISS in *status and gets an item that writes nothing.  info =
+// {n_gu, tiles_gu, n_dn, tiles_dn}; host_counts[E] (pinned host words,
+// device-visible address) receives the per-expert token counts.
 hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
                                 const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
-                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *tail, hipStream_t s);
+                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *status, uint32_t *host_counts,
+                                hipStream_t s);
 
 // ---- combine / publication and slot generation words (combine.hip)
-// out[t] = ys[t] + sum_k y[inv[t, k]] in that order (y, ys bf16, or fp32 when f32)
+// out[t] = ys[t] + sum_k y[inv[t, k]] in that order (y, ys bf16, or fp32 when f32),
+// unless *status is nonzero; *status is also copied to host_status (a pinned
+// host word, device-visible address), if given
 hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
-                          const uint32_t *status, int T, int K, int d, hipStream_t s);
+                          const uint32_t *status, uint32_t *host_status, int T, int K, int d, hipStream_t s);
 constexpr int GEN_BATCH = 64;
 struct GenBatch {
     uint32_t n;

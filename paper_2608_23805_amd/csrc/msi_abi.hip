@@ -110,7 +110,9 @@ struct msi_plan {
     uint32_t *res_gen_dev = nullptr;    // [n_layers][E]
     int32_t *res_host = nullptr;        // pinned staging [2 * E]
     int32_t *info_dev = nullptr;        // {n_gu, tiles_gu, n_dn, tiles_dn}
-    uint32_t *tail_host = nullptr;      // pinned [1 + E]
+    uint32_t *tail_host = nullptr;      // pinned [1 + E]: status, then per-expert counts (written by kernels)
+    uint32_t *tail_hdev = nullptr;      // device-visible address of tail_host
+    uint32_t *status_hdev = nullptr;    // device-visible address of status_host
     std::vector<uint64_t> res_version;  // per layer: layer version uploaded
     std::vector<uint8_t> direct_ok;     // per layer: last forward needed no fill
     // timing telemetry
@@ -120,6 +122,8 @@ struct msi_plan {
     };
     bool timing = false;
     uint32_t timing_mask = 0;           // kernel kinds bracketed by events
+    uint32_t timing_period = 1;         // time every period-th launch of a kind
+    uint64_t timing_seen[MSI_NKERN] = {};
     std::vector<Timed> timed;
     std::vector<hipEvent_t> tfree;
     uint64_t t_launches[MSI_NKERN] = {};
@@ -146,7 +150,7 @@ struct msi_plan {
     hipError_t timed_launch(int kind, hipStream_t s, F &&launch)
     {
         (void)s;
-        if (!timing || !(timing_mask & (1u << kind)))
+        if (!timing || !(timing_mask & (1u << kind)) || (timing_seen[kind]++ % timing_period) != 0)
             return launch();
         if (timed.size() >= 8192)
             resolve_timings();
@@ -170,7 +174,7 @@ struct msi_plan {
     template <typename F>
     hipError_t timed_copy(int kind, hipStream_t s, F &&copy)
     {
-        if (!timing || !(timing_mask & (1u << kind)))
+        if (!timing || !(timing_mask & (1u << kind)) || (timing_seen[kind]++ % timing_period) != 0)
             return copy();
         if (timed.size() >= 8192)
             resolve_timings();
@@ -349,7 +353,9 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         hipHostMalloc(&p->counts_host, sizeof(int32_t) * desc->n_experts, hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc(&p->status_host, 256, hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc(&p->res_host, sizeof(int32_t) * 2 * E, hipHostMallocDefault) != hipSuccess ||
-        hipHostMalloc(&p->tail_host, sizeof(uint32_t) * (E + 1), hipHostMallocDefault) != hipSuccess)
+        hipHostMalloc(&p->tail_host, sizeof(uint32_t) * (E + 1), hipHostMallocDefault) != hipSuccess ||
+        hipHostGetDevicePointer(reinterpret_cast<void **>(&p->tail_hdev), p->tail_host, 0) != hipSuccess ||
+        hipHostGetDevicePointer(reinterpret_cast<void **>(&p->status_hdev), p->status_host, 0) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "pinned host allocation failed");
     if (hipMemset(p->gen_dev, 0, nslots * sizeof(uint32_t)) != hipSuccess ||
         hipMemset(p->status_dev, 0, sizeof(uint32_t) * (E + 64)) != hipSuccess ||
@@ -555,10 +561,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         const int has_sh = a->shared_object ? 1 : 0;
         const int max_items = std::min(E, T * K) + has_sh;
         WorkItem *gu = p->table_dev, *dn = p->table_dev + (E + 1);
+        p->tail_host[0] = 0u;     // overwritten by the combine of this forward
         HIP_OK(p->timed_launch(MSI_K_WORKLIST, cs, [&] {
             return launch_fast_worklist(a->r.counts, a->r.offsets, p->res_slot_dev + size_t(L0) * E,
                                         p->res_gen_dev + size_t(L0) * E, E, T, has_sh, tpg, tpd, gu, dn,
-                                        p->info_dev, p->status_dev, cs);
+                                        p->info_dev, p->status_dev, p->tail_hdev + 1, cs);
         }));
         ExpertLaunch X{};
         X.x = a->x;
@@ -588,9 +595,10 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
                                [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
             return launch_combine(wsb + ws.y, has_sh ? wsb + ws.ys : nullptr, false, a->r.inv, a->out,
-                                  p->status_dev, T, K, D, cs);
+                                  p->status_dev, p->tail_hdev, T, K, D, cs);
         }));
-        HIP_OK(hipMemcpyAsync(p->tail_host, p->status_dev, sizeof(uint32_t) * (E + 1), hipMemcpyDeviceToHost, cs));
+        // the work list kernel wrote the counts and the combine the status
+        // straight into tail_host: no copy, one synchronisation
         HIP_OK(hipStreamSynchronize(cs));
         const uint32_t st = p->tail_host[0];
         if (!(st & STATUS_MISS)) {
@@ -797,16 +805,15 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         }
     }
 
-    // ---- publication: out written only if every tile saw its generation
+    // ---- publication: out written only if every tile saw its generation; the
+    // combine copies the status word to status_host (no launch when T == 0)
+    *p->status_host = 0u;
     if (rst == MSI_OK)
         if (p->timed_launch(MSI_K_COMBINE, cs, [&] {
                 return launch_combine(wsb + ws.y, has_shared ? wsb + ws.ys : nullptr, f32w, a->r.inv,
-                                      a->out, p->status_dev, T, K, D, cs);
+                                      a->out, p->status_dev, p->status_hdev, T, K, D, cs);
             }) != hipSuccess)
             rst = fail(MSI_E_DEVICE, "combine launch failed");
-    if (rst == MSI_OK && hipMemcpyAsync(p->status_host, p->status_dev, sizeof(uint32_t), hipMemcpyDeviceToHost,
-                                        cs) != hipSuccess)
-        rst = fail(MSI_E_DEVICE, "status read failed");
     const hipError_t se = hipStreamSynchronize(cs);
     (void)hipStreamSynchronize(side);
     if (se != hipSuccess && rst == MSI_OK)
@@ -891,6 +898,16 @@ msi_status msi_plan_set_timing(msi_plan *p, int enable)
         return fail(MSI_E_INVALID_ARG, "null plan");
     p->timing = enable != 0;
     p->timing_mask = enable == 1 ? ~0u : uint32_t(enable);
+    return MSI_OK;
+}
+
+msi_status msi_plan_set_timing_period(msi_plan *p, uint32_t period)
+{
+    if (!p || period == 0)
+        return fail(MSI_E_INVALID_ARG, "null plan or zero period");
+    p->timing_period = period;
+    for (uint64_t &c : p->timing_seen)
+        c = 0;
     return MSI_OK;
 }
 
