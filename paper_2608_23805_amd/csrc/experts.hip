@@ -124,7 +124,7 @@ int tiles_gateup_stream(int nrows, int d, int I)
 {
     (void)nrows;
     (void)d;
-    return I / (stream::WAVES * stream::ROWS);
+    return I / stream::ROWS;
 }
 
 int tiles_down_stream(int nrows, int d, int I)
@@ -244,12 +244,18 @@ struct StageRows {
     }
 };
 
+// Gate/up, stream path: a workgroup owns 16 rows of Wg and of Wu; its four
+// wavefronts take the four quarters of d (U K steps of 32 per weight batch)
+// and their fp32 partial sums are added in wavefront order before SiLU(g) * u.
+// Sixteen-row workgroups keep the grid many times larger than the number of
+// resident workgroups, so the last partial round of the launch is short.
 template <int U>
 __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];   // [16][d + 8]
+    __shared__ f32x4 red[3][2][64];
     const int d = L.d, I = L.I, ldk = d + 8;
-    const StreamTile st = stream_tile(L, I / (stream::WAVES * stream::ROWS));
+    const StreamTile st = stream_tile(L, I / stream::ROWS);
     if (!st.valid)
         return;
     const WorkItem &it = st.it;
@@ -264,12 +270,13 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int i0 = (st.local * stream::WAVES + wave) * stream::ROWS;
+    const int i0 = st.local * stream::ROWS;
+    const int kq = d / stream::WAVES;             // this wavefront's quarter of d
     const int j = lane & 15, kg = (lane >> 4) * 8;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
-    const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + kg;
+    const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + wave * kq + kg;
     const uint16_t *up = gp + int64_t(I) * d;
-    const uint16_t *xr = xs + j * ldk + kg;
+    const uint16_t *xr = xs + j * ldk + wave * kq + kg;
     const bool live = j < n;
 
     // Weight batches are double-buffered in registers: batch b + 1 is in
@@ -286,7 +293,7 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
     __syncthreads();
 
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
-    const int nb = d / (32 * U);
+    const int nb = kq / (32 * U);
     for (int b = 0; b < nb; b += 2) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -308,6 +315,19 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
                 au = mfma16(as_bf16x8(wu[h][u]), bx, au);
             }
         }
+    }
+    // quarters of d added in wavefront order
+    if (wave > 0) {
+        red[wave - 1][0][lane] = ag;
+        red[wave - 1][1][lane] = au;
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        ag[r] = ((ag[r] + red[0][0][lane][r]) + red[1][0][lane][r]) + red[2][0][lane][r];
+        au[r] = ((au[r] + red[0][1][lane][r]) + red[1][1][lane][r]) + red[2][1][lane][r];
     }
     if (!slot_gen_ok(it, gnow, L.status))
         return;
@@ -385,10 +405,13 @@ hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s)
     if (L.n_tiles == 0)
         return hipSuccess;
     const size_t lds = size_t(stream::MAXN) * (L.d + 8) * sizeof(uint16_t);
-    if (L.d % 256 == 0)
+    // U K steps of 32 per batch must divide the quarter d / 4 (d % 256 == 0)
+    if (L.d % 1024 == 0)
         launch_k(stream_gateup_kernel<8>, L.n_tiles, 256, lds, s, L);
+    else if (L.d % 512 == 0)
+        launch_k(stream_gateup_kernel<4>, L.n_tiles, 256, lds, s, L);
     else
-        launch_k(stream_gateup_kernel<1>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_kernel<2>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -562,7 +585,8 @@ hipError_t init_kernel_attributes()
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Down>));
     set(reinterpret_cast<const void *>(&stream_gateup_kernel<8>));
-    set(reinterpret_cast<const void *>(&stream_gateup_kernel<1>));
+    set(reinterpret_cast<const void *>(&stream_gateup_kernel<4>));
+    set(reinterpret_cast<const void *>(&stream_gateup_kernel<2>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<16>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
     if (e == hipSuccess)
