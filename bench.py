@@ -108,7 +108,7 @@ def bench_decode(args, cs, side):
     # a further untimed pass with every launch carrying events: per-kernel durations
     plan.set_timing(args.telemetry == "on")
     plan.set_timing_period(1)
-    _run(plan, xs, dev, r, ws, out, 0, 32, cs, side)
+    _run(plan, xs, dev, r, ws, out, 32, 0, cs, side)      # _run clears the telemetry before its steps
     t_all = plan.timings()
     # algorithmic bytes of each step's gate/up launch (one round): the
     # demanded experts' Wg and Wu once, their tokens' x rows once, act written
@@ -136,7 +136,8 @@ def bench_decode(args, cs, side):
                roofline={"bound": "hbm", "kernel": "stream_gateup_kernel", "achieved": round(achieved, 1),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                          "traffic": recorded_traffic(), "bytes_per_launch": int(bytes_gu),
-                         "avg_launch_us": round(avg_gu * 1e3, 2), "launches_timed": n_gu},
+                         "avg_launch_us": round(avg_gu * 1e3, 2), "launches_timed": n_gu,
+                         "bytes_per_batch_mean": int(sum(bytes_b) / len(bytes_b))},
                down={"achieved_GBs": round(bytes_dn / (avg_dn * 1e-3) / 1e9, 1) if avg_dn > 0 else None,
                      "avg_launch_us": round(avg_dn * 1e3, 2), "bytes_per_launch": int(bytes_dn)},
                stats={k: st[k] for k in ("fills", "hits", "misses", "rounds")})
