@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MSI_ABI_VERSION 1u
+#define MSI_ABI_VERSION 2u
 
 typedef int32_t msi_status;
 
@@ -129,6 +129,7 @@ typedef struct {
     float *weights;              /* [T, K] gate weights (restricted softmax), fp32    */
     int32_t *counts;             /* [E] tokens per expert                             */
     int32_t *offsets;            /* [E + 1] exclusive prefix of counts                */
+    int32_t *demand;             /* [E + 1] demanded experts: their number, then their ids ascending */
     int32_t *perm;               /* [T * K] token of each permuted row; rows ordered by (expert, token) */
     int32_t *inv;                /* [T, K] permuted row of each (token, k)            */
     float *row_weight;           /* [T * K] gate weight of each permuted row          */
@@ -207,8 +208,7 @@ typedef enum {
     MSI_K_SHARED = 8,          /* shared expert, gate/up and down                 */
     MSI_K_COMBINE = 9,
     MSI_K_FILL = 10,           /* one batch of slot fills on the side stream      */
-    MSI_K_WORKLIST = 11,       /* device-built work list of a forward             */
-    MSI_NKERN = 12
+    MSI_NKERN = 11
 } msi_kernel_kind;
 
 typedef struct {
@@ -264,8 +264,11 @@ msi_status msi_plan_poll(msi_plan *plan);
 /* Router and permutation on `stream` (no host synchronisation): logits
  * (bf16 MFMA or fp32 with fp32 accumulation) plus bias, top-K by (logit desc,
  * expert id asc), softmax restricted to the selected set in fp32, then the
- * stable token-by-expert permutation.  Fully deterministic.  Errors:
- * MSI_E_INVALID_ARG, MSI_E_NOMEM (workspace), MSI_E_DEVICE. */
+ * stable token-by-expert permutation and the list of demanded experts.  Fully
+ * deterministic.  For 1 <= T <= 16 bf16 tokens all of it is one launch whose
+ * workgroups count their arrival in a plan-owned word: msi_route calls on one
+ * plan must not overlap in time (e.g. on two streams without ordering).
+ * Errors: MSI_E_INVALID_ARG, MSI_E_NOMEM (workspace), MSI_E_DEVICE. */
 msi_status msi_route(msi_plan *plan, const msi_route_args *args, void *stream);
 
 /* One MoE layer against the slot pool (Section 4 scheduling).  Reads the
@@ -276,6 +279,11 @@ msi_status msi_route(msi_plan *plan, const msi_route_args *args, void *stream);
  * in-kernel generation checks, runs the shared expert, and publishes
  * out[t] = shared(x_t) + sum over the token's experts in ascending id of
  * w * expert(x_t), in fp32.  Blocks until the status word is known.
+ * When the layer's previous forward needed no fill and T is within the stream
+ * path, the work list is instead built on the device from r.demand and the
+ * published residency table (no host round trip before the expert kernels),
+ * and the call returns once the combine has published the status: output rows
+ * may still be in flight, ordered before later work on `compute_stream`.
  * out is bit-identical for every slot capacity.  Errors: MSI_E_STALE (a
  * kernel saw an unexpected slot generation; out is untouched), MSI_E_BUSY (no
  * slot could be freed), MSI_E_INVALID_ARG, MSI_E_NOMEM, MSI_E_DEVICE. */

@@ -16,7 +16,7 @@ from typing import List, Optional, Sequence, Tuple
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmsi.so")
 
-MSI_ABI_VERSION = 1
+MSI_ABI_VERSION = 2
 MSI_OK = 0
 MSI_E_INVALID_ARG = -1
 MSI_E_SHORT = -2
@@ -57,8 +57,8 @@ class msi_ticket(ctypes.Structure):
 
 
 class msi_routing(ctypes.Structure):
-    _fields_ = [("idx", _vp), ("weights", _vp), ("counts", _vp), ("offsets", _vp), ("perm", _vp),
-                ("inv", _vp), ("row_weight", _vp)]
+    _fields_ = [("idx", _vp), ("weights", _vp), ("counts", _vp), ("offsets", _vp), ("demand", _vp),
+                ("perm", _vp), ("inv", _vp), ("row_weight", _vp)]
 
 
 class msi_route_args(ctypes.Structure):
@@ -84,7 +84,7 @@ class msi_stats(ctypes.Structure):
 
 
 KERNEL_KINDS = ["router_logits", "topk", "permute", "gateup_tile", "gateup_stream", "down_tile",
-                "down_stream", "expert_f32", "shared", "combine", "fill", "worklist"]
+                "down_stream", "expert_f32", "shared", "combine", "fill"]
 
 
 class msi_timings(ctypes.Structure):
@@ -196,6 +196,7 @@ class Routing:
     weights: object
     counts: object
     offsets: object
+    demand: object
     perm: object
     inv: object
     row_weight: object
@@ -207,7 +208,7 @@ class Routing:
         f32 = dict(dtype=torch.float32, device=device)
         return Routing(idx=torch.empty((T, K), **i32), weights=torch.empty((T, K), **f32),
                        counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
-                       perm=torch.empty(T * K, **i32), inv=torch.empty((T, K), **i32),
+                       demand=torch.empty(E + 1, **i32), perm=torch.empty(T * K, **i32), inv=torch.empty((T, K), **i32),
                        row_weight=torch.empty(T * K, **f32))
 
     def __setattr__(self, name, value):
@@ -219,7 +220,7 @@ class Routing:
         if getattr(self, "_c", None) is None:
             object.__setattr__(self, "_c", msi_routing(
                 _ptr(self.idx), _ptr(self.weights), _ptr(self.counts), _ptr(self.offsets),
-                _ptr(self.perm), _ptr(self.inv), _ptr(self.row_weight)))
+                _ptr(self.demand), _ptr(self.perm), _ptr(self.inv), _ptr(self.row_weight)))
         return self._c
 
 

@@ -6,21 +6,60 @@
 // nothing, Section 5.7).  out[t] = shared(x_t) + sum over the token's
 // experts in ascending id of the weighted contributions, summed in fp32 in
 // that fixed order so the result does not depend on slot capacity.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace msi {
 
+// Status handling shared by both combines.  Every workgroup reads the status
+// word.  With an arrival counter (small grids: one counter update per
+// workgroup), thread 0 of each workgroup counts itself in after its read and
+// the last to arrive (the counter wraps back to zero) clears the word, so the
+// next forward starts from a clean word without a launch of its own.
+// Workgroup 0 also publishes to pinned host words: the demanded experts
+// (count, then ids) when `demand` is given, then status | STATUS_DONE with a
+// system-scope release, so a host that sees the done bit also sees the list.
+__device__ __forceinline__ uint32_t combine_status(const CombinePublish &P)
+{
+    uint32_t st;
+    if (P.arrive) {
+        __shared__ uint32_t st_s;
+        if (threadIdx.x == 0) {
+            const uint32_t v = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            st_s = v;
+            __builtin_amdgcn_s_waitcnt(0);      // the word is read before this workgroup counts itself in
+            if (atomicInc(P.arrive, gridDim.x - 1u) == gridDim.x - 1u)
+                __hip_atomic_store(P.status, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();
+        st = st_s;
+    } else {
+        st = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (blockIdx.x == 0 && P.host) {
+        if (P.demand) {
+            const int n = P.demand[0];
+            for (int i = threadIdx.x; i <= n; i += blockDim.x)
+                __hip_atomic_store(P.host + 1 + i, uint32_t(P.demand[i]), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_SYSTEM);
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");   // system scope: the list before the done bit
+            __hip_atomic_store(P.host, st | STATUS_DONE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+    }
+    return st;
+}
+
 // fp32 layers: y and ys in fp32, four columns per thread.
 __global__ void __launch_bounds__(256) combine_f32_kernel(const float *__restrict__ y, const float *__restrict__ ys,
                                                           const int32_t *__restrict__ inv, float *__restrict__ out,
-                                                          const uint32_t *__restrict__ status, uint32_t *host_status, int T,
-                                                          int K, int d)
+                                                          CombinePublish P, int T, int K, int d)
 {
-    const uint32_t st = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (host_status && blockIdx.x == 0 && threadIdx.x == 0)
-        *host_status = st;         // pinned host word: read by the host after the stream completes
-    if (st != 0u)
+    if (combine_status(P) != 0u)
         return;
     const int d4 = d / 4;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -52,13 +91,9 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // fixed order (shared expert, then the K routed rows in selection order).
 __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict__ y, const uint16_t *__restrict__ ys,
                                                       const int32_t *__restrict__ inv, float *__restrict__ out,
-                                                      const uint32_t *__restrict__ status, uint32_t *host_status, int T,
-                                                          int K, int d)
+                                                      CombinePublish P, int T, int K, int d)
 {
-    const uint32_t st = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (host_status && blockIdx.x == 0 && threadIdx.x == 0)
-        *host_status = st;         // pinned host word: read by the host after the stream completes
-    if (st != 0u)
+    if (combine_status(P) != 0u)
         return;
     const int d8 = d / 8;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -98,20 +133,19 @@ __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict
 }
 
 hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
-                          const uint32_t *status, uint32_t *host_status, int T, int K, int d, hipStream_t s)
+                          const CombinePublish &P, int T, int K, int d, hipStream_t s)
 {
+    if (!P.status)
+        return hipErrorInvalidValue;
+    // at least one workgroup even for T == 0: the status is still published and cleared
     if (f32) {
-        const int64_t n = int64_t(T) * (d / 4);
-        if (n == 0)
-            return hipSuccess;
+        const int64_t n = std::max<int64_t>(int64_t(T) * (d / 4), 1);
         launch_k(combine_f32_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const float *>(y),
-                 static_cast<const float *>(ys), inv, out, status, host_status, T, K, d);
+                 static_cast<const float *>(ys), inv, out, P, T, K, d);
     } else {
-        const int64_t n = int64_t(T) * (d / 8);
-        if (n == 0)
-            return hipSuccess;
+        const int64_t n = std::max<int64_t>(int64_t(T) * (d / 8), 1);
         launch_k(combine_kernel, unsigned((n + 255) / 256), 256, 0, s, static_cast<const uint16_t *>(y),
-                 static_cast<const uint16_t *>(ys), inv, out, status, host_status, T, K, d);
+                 static_cast<const uint16_t *>(ys), inv, out, P, T, K, d);
     }
     return hipGetLastError();
 }

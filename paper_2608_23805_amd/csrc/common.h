@@ -32,6 +32,7 @@ constexpr int PERM_BLOCK = 256;
 // status word bits written by kernels that detect a problem
 constexpr uint32_t STATUS_STALE = 1u;   // a tile saw a slot generation it did not expect
 constexpr uint32_t STATUS_MISS = 2u;    // a demanded expert had no published slot (device work list)
+constexpr uint32_t STATUS_DONE = 1u << 31;   // host copy only: the combine has published the status
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
@@ -93,6 +94,64 @@ __device__ __forceinline__ int find_item(const WorkItem *items, int n_items, int
             hi = mid - 1;
     }
     return lo;
+}
+
+// Device-built work list of a decode forward: item i of a launch is the
+// shared expert (i == 0, when there is one) or the (i - has_shared)-th
+// demanded expert in ascending id, with its slot and generation from the
+// layer's published residency table.  `demand` holds the number of demanded
+// experts, then their ids ascending, as the routing wrote them.
+struct DirectList {
+    const int32_t *demand;       // [1 + E], or null: the launch has a host-built list
+    const int32_t *slot_of;      // [E] published global slot of each expert of the layer, -1 if none
+    const uint32_t *gen_of;      // [E] its published generation
+    const int32_t *counts;       // [E] rows per expert
+    const int32_t *offsets;      // [E + 1] first permuted row per expert
+    int has_shared;
+    int T;                       // rows of the shared expert
+    int E;                       // experts of the layer (demand holds 1 + E words)
+};
+
+// Tile of workgroup b in a direct launch: the tiles of one item stay on one
+// XCD (the hardware hands workgroup b to XCD b % 8) and items go round-robin
+// over the XCDs, so the spread is even for any number of items.  The grid is
+// a multiple of 8 * per_item.
+__device__ __forceinline__ void direct_tile(int b, int per_item, int &item, int &local)
+{
+    const int q = b >> 3;
+    item = (b & 7) + 8 * (q / per_item);
+    local = q % per_item;
+}
+
+// Item i (tiles i * per_item ..) of a direct launch.  False past the last
+// item.  A demanded expert without a published slot raises STATUS_MISS and
+// comes back with nrows 0 (no work): the forward publishes nothing and is
+// rescheduled by the host.  Every load is issued at a clamped, valid index
+// before any branch (the empty asm statements keep the compiler from sinking
+// them below one), so the lookup costs two dependent round trips.
+__device__ __forceinline__ bool direct_item(const DirectList &D, int i, int per_item, uint32_t *status, WorkItem &it)
+{
+    const int j = i - D.has_shared;
+    // (i is uniform: the values are kept in scalar registers)
+    int n = __builtin_amdgcn_readfirstlane(D.demand[0]);
+    int e = __builtin_amdgcn_readfirstlane(D.demand[1 + min(max(j, 0), D.E - 1)]);
+    asm volatile("" : "+s"(n), "+s"(e));
+    e = min(max(e, 0), D.E - 1);              // entries past n are stale: keep the reads in bounds
+    int32_t s = __builtin_amdgcn_readfirstlane(D.slot_of[e]);
+    int32_t r0 = __builtin_amdgcn_readfirstlane(D.offsets[e]);
+    int32_t c = __builtin_amdgcn_readfirstlane(D.counts[e]);
+    uint32_t g = __builtin_amdgcn_readfirstlane(D.gen_of[e]);
+    asm volatile("" : "+s"(s), "+s"(r0), "+s"(c), "+s"(g));
+    if (j >= n)
+        return false;
+    if (j < 0) {
+        it = WorkItem{-1, -1, 0u, 0, D.T, 0};
+        return true;
+    }
+    it = WorkItem{e, s, g, r0, s < 0 ? 0 : c, i * per_item};
+    if (s < 0 && threadIdx.x == 0)
+        atomicOr(status, STATUS_MISS);
+    return true;
 }
 
 // Generation check done by every tile before it reads a slot: true if the

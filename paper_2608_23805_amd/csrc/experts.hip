@@ -138,8 +138,8 @@ int tiles_down_stream(int nrows, int d, int I)
 // before the first MFMA are few: the item is found by division (every stream
 // item of a launch has the same tile count), the slot generation word is read
 // alongside and checked only before the store (a stale slot is read but
-// nothing is written), the token rows of the B operand are fetched before the
-// first weight batch is issued, and their LDS stores wait only for them.
+// nothing is written), and the first weight batch is issued before the
+// kernel waits for anything else.
 struct StreamTile {
     WorkItem it;
     int local;          // tile index within the item
@@ -149,19 +149,21 @@ struct StreamTile {
 __device__ __forceinline__ StreamTile stream_tile(const ExpertLaunch &L, int per_item)
 {
     StreamTile st{};
-    // with a device-built work list the grid is an upper bound: workgroups
-    // past the real tile count exit, and the XCD spread uses the real count
-    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
-    const int n_items = L.dev_counts ? L.dev_counts[0] : L.n_items;
-    if (int(blockIdx.x) >= ntiles)
+    if (L.direct.demand) {
+        int i;
+        direct_tile(int(blockIdx.x), per_item, i, st.local);
+        if (!direct_item(L.direct, i, per_item, L.status, st.it))
+            return st;
+        st.valid = st.it.nrows > 0;       // nrows 0: unpublished expert, no work
         return st;
-    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
+    }
+    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
     const int i = t / per_item;
-    if (i >= n_items)
+    if (i >= L.n_items)
         return st;
     st.it = L.items[i];
     st.local = t - i * per_item;
-    st.valid = st.it.nrows > 0;       // nrows 0: unpublished expert, no work
+    st.valid = st.it.nrows > 0;
     return st;
 }
 
@@ -247,14 +249,19 @@ struct StageRows {
 // Gate/up, stream path: a workgroup owns 16 rows of Wg and of Wu; its four
 // wavefronts take the four quarters of d (U K steps of 32 per weight batch)
 // and their fp32 partial sums are added in wavefront order before SiLU(g) * u.
-// Sixteen-row workgroups keep the grid many times larger than the number of
-// resident workgroups, so the last partial round of the launch is short.
+// Both MFMA operands come straight from memory: the weights (A operand) are
+// streamed once, and the lanes of token j (B operand) read row j of the item
+// from x, which stays in the caches (every item reads rows of the same few
+// tokens); lanes past the item's rows hold zeros.  With no LDS staging
+// buffer the occupancy is set by registers alone, and no barrier separates
+// the first weight batch from the first MFMA.  Sixteen-row workgroups keep
+// the grid many times larger than the number of resident workgroups, so the
+// last partial round of the launch is short.
 template <int U>
-__global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
+__global__ void __launch_bounds__(256, 3) stream_gateup_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];   // [16][d + 8]
     __shared__ f32x4 red[3][2][64];
-    const int d = L.d, I = L.I, ldk = d + 8;
+    const int d = L.d, I = L.I;
     const StreamTile st = stream_tile(L, I / stream::ROWS);
     if (!st.valid)
         return;
@@ -262,11 +269,6 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
     const int n = it.nrows;
     const bool sh = it.slot < 0;
     const uint32_t gnow = slot_gen_now(it, L.gen_dev);
-    // the gathered token rows of x (the shared expert reads the tokens in order)
-    const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
-    const int32_t *xperm = sh ? nullptr : L.perm;
-    StageRows<4> sr;                              // one pass for d <= 2048
-    sr.load(xsrc, xperm, it.row0, n, d, 0);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -276,21 +278,35 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + wave * kq + kg;
     const uint16_t *up = gp + int64_t(I) * d;
-    const uint16_t *xr = xs + j * ldk + wave * kq + kg;
     const bool live = j < n;
 
-    // Weight batches are double-buffered in registers: batch b + 1 is in
-    // flight while batch b is multiplied; batch 0 is issued before the token
-    // rows are written to LDS.
-    u32x4 wg[2][U], wu[2][U];
+    // This lane's token (the shared expert's rows are the tokens in order),
+    // read before the weights are issued: memory reads complete in order, so
+    // waiting for it later leaves the weight batch in flight.  Lanes past
+    // the item's rows read its last row and multiply zeros: every read is
+    // unconditional, so the compiler's waits stay exact.
+    const int jr = it.row0 + min(j, n - 1);
+    const int64_t xrow = sh ? int64_t(jr) : int64_t(L.perm[jr]);
+    // Weight and token batches are double-buffered in registers: batch b + 1
+    // is in flight while batch b is multiplied.  (The empty asm statements
+    // keep the issue order: token index, weights, then the token rows.)
+    u32x4 wg[2][U], wu[2][U], xb[2][U];
+    asm volatile("" ::: "memory");
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         wg[0][u] = load_stream16(gp + 32 * u);
         wu[0][u] = load_stream16(up + 32 * u);
     }
-    sr.store(xs, n, d, 0);
-    sr.rest(xsrc, xperm, it.row0, n, d, xs);
-    __syncthreads();
+    asm volatile("" ::: "memory");
+    const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + wave * kq + kg;
+    auto load_x = [&](u32x4(&dst)[U], int k0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(xp + k0 + 32 * u);
+            dst[u] = live ? v : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    load_x(xb[0], 0);
 
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
     const int nb = kq / (32 * U);
@@ -306,11 +322,11 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
                     wg[h ^ 1][u] = load_stream16(gp + k0 + 32 * U + 32 * u);
                     wu[h ^ 1][u] = load_stream16(up + k0 + 32 * U + 32 * u);
                 }
+                load_x(xb[h ^ 1], k0 + 32 * U);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const uint4 xv = live ? *reinterpret_cast<const uint4 *>(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
-                const bf16x8 bx = as_bf16x8(xv);
+                const bf16x8 bx = as_bf16x8(xb[h][u]);
                 ag = mfma16(as_bf16x8(wg[h][u]), bx, ag);
                 au = mfma16(as_bf16x8(wu[h][u]), bx, au);
             }
@@ -342,6 +358,9 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kernel(ExpertLaunch L)
     }
 }
 
+// Down, stream path: a workgroup owns 64 output columns (16 per wavefront)
+// over all of I; the expert's act rows (the B operand, shared by the four
+// wavefronts) are staged once in LDS.
 template <int U>
 __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
 {
@@ -404,14 +423,11 @@ hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    const size_t lds = size_t(stream::MAXN) * (L.d + 8) * sizeof(uint16_t);
     // U K steps of 32 per batch must divide the quarter d / 4 (d % 256 == 0)
-    if (L.d % 1024 == 0)
-        launch_k(stream_gateup_kernel<8>, L.n_tiles, 256, lds, s, L);
-    else if (L.d % 512 == 0)
-        launch_k(stream_gateup_kernel<4>, L.n_tiles, 256, lds, s, L);
+    if (L.d % 512 == 0)
+        launch_k(stream_gateup_kernel<4>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_gateup_kernel<2>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_kernel<2>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -424,63 +440,6 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
         launch_k(stream_down_kernel<16>, L.n_tiles, 256, lds, s, L);
     else
         launch_k(stream_down_kernel<4>, L.n_tiles, 256, lds, s, L);
-    return hipGetLastError();
-}
-
-// ============================================================== device work list
-
-__global__ void __launch_bounds__(1024) fast_worklist_kernel(const int32_t *__restrict__ counts,
-                                                             const int32_t *__restrict__ offsets,
-                                                             const int32_t *__restrict__ slot_of,
-                                                             const uint32_t *__restrict__ gen_of, int E, int T,
-                                                             int has_shared, int tpg, int tpd, WorkItem *gu,
-                                                             WorkItem *dn, int32_t *info, uint32_t *status,
-                                                             uint32_t *host_counts)
-{
-    __shared__ int32_t part[1024];
-    const int e = threadIdx.x;
-    const int c = e < E ? counts[e] : 0;
-    part[e] = c > 0 ? 1 : 0;
-    __syncthreads();
-    block_scan_1024(part);
-    const int base = has_shared ? 1 : 0;
-    bool miss = false;
-    if (c > 0) {
-        const int pos = base + part[e] - 1;
-        int32_t s = slot_of[e];
-        uint32_t g = gen_of[e];
-        int n = c;
-        if (s < 0) {            // not published: this forward will not publish; the item writes nothing
-            miss = true;
-            n = 0;
-        }
-        gu[pos] = WorkItem{e, s, g, offsets[e], n, pos * tpg};
-        dn[pos] = WorkItem{e, s, g, offsets[e], n, pos * tpd};
-    }
-    if (e == 0 && has_shared) {
-        gu[0] = WorkItem{-1, -1, 0u, 0, T, 0};
-        dn[0] = WorkItem{-1, -1, 0u, 0, T, 0};
-    }
-    const int any_miss = __syncthreads_or(miss ? 1 : 0);
-    if (e == 0) {
-        const int n = base + part[1023];
-        info[0] = n;
-        info[1] = n * tpg;
-        info[2] = n;
-        info[3] = n * tpd;
-        __hip_atomic_store(status, any_miss ? STATUS_MISS : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (e < E)
-        host_counts[e] = uint32_t(c);     // pinned host words: the demanded set, read after the stream completes
-}
-
-hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
-                                const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
-                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *status, uint32_t *host_counts,
-                                hipStream_t s)
-{
-    launch_k(fast_worklist_kernel, 1, 1024, 0, s, counts, offsets, slot_of, gen_of, E, T, has_shared, tpg, tpd,
-             gu, dn, info, status, host_counts);
     return hipGetLastError();
 }
 
@@ -584,9 +543,6 @@ hipError_t init_kernel_attributes()
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Down>));
-    set(reinterpret_cast<const void *>(&stream_gateup_kernel<8>));
-    set(reinterpret_cast<const void *>(&stream_gateup_kernel<4>));
-    set(reinterpret_cast<const void *>(&stream_gateup_kernel<2>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<16>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
     if (e == hipSuccess)

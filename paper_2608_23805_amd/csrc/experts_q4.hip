@@ -116,17 +116,28 @@ __device__ __forceinline__ void q4_rows_dot(const uint8_t *__restrict__ nib, con
     }
 }
 
+// Tile t of a stream launch and its item: from the device-built list (the
+// grid is then an upper bound) or the host list.
+__device__ __forceinline__ bool q4_tile(const ExpertLaunch &L, int per_item, int &t, WorkItem &it)
+{
+    if (L.direct.demand) {
+        int i, local;
+        direct_tile(int(blockIdx.x), per_item, i, local);
+        t = i * per_item + local;
+        return direct_item(L.direct, i, per_item, L.status, it);
+    }
+    t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
+    it = L.items[find_item(L.items, L.n_items, t)];
+    return true;
+}
+
 __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
-    // with a device-built work list the grid is an upper bound: workgroups
-    // past the real tile count exit, and the XCD spread uses the real count
-    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
-    if (int(blockIdx.x) >= ntiles)
-        return;
-    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
-    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
-    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
+    int t;
+    WorkItem it;
+    if (!q4_tile(L, L.I / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
+        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8;
     const bool sh = it.slot < 0;
@@ -153,14 +164,10 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
 __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t as[];
-    // with a device-built work list the grid is an upper bound: workgroups
-    // past the real tile count exit, and the XCD spread uses the real count
-    const int ntiles = L.dev_counts ? L.dev_counts[1] : int(gridDim.x);
-    if (int(blockIdx.x) >= ntiles)
-        return;
-    const int t = xcd_swizzle(int(blockIdx.x), ntiles);
-    const WorkItem it = L.items[find_item(L.items, L.dev_counts ? L.dev_counts[0] : L.n_items, t)];
-    if (it.nrows == 0 || !slot_current(it, L.gen_dev, L.status))    // nrows 0: unpublished expert, no work
+    int t;
+    WorkItem it;
+    if (!q4_tile(L, L.d / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
+        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
     const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8;
     const bool sh = it.slot < 0;

@@ -58,18 +58,28 @@ inline hipError_t allow_large_lds(const void *f)
     return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                int(160 * 1024 - a.sharedSizeBytes));
 }
-// streaming router for 1 <= T <= 16 tokens (bf16): partial logits
-// P[ROUTER_SPLIT][T][E] without the bias
-constexpr int ROUTER_SPLIT = 4;
-hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, float *P, int T, int d, int E,
-                                hipStream_t s);
-// top-K + restricted softmax + permutation (one fused workgroup when T <= 256).
-// With P (T <= 16 only) the logits are formed from the partials plus the bias
-// and stored to L; otherwise they are read from L.
-hipError_t launch_route_select(float *L, const float *P, const float *bias, int32_t *idx, float *w,
-                               int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
-                               int32_t *blockhist, int T, int K, int E, hipStream_t s);
+// Outputs of one routing (device arrays, see msi_routing).
+struct RouteOut {
+    int32_t *idx;
+    float *w;
+    int32_t *counts;
+    int32_t *offsets;
+    int32_t *demand;
+    int32_t *perm;
+    int32_t *inv;
+    float *row_weight;
+};
+// top-K + restricted softmax + permutation of logits L (bias included): one
+// fused workgroup when T <= 256, else top-K, histogram, scan and scatter
+hipError_t launch_route_select(const float *L, const RouteOut &o, int32_t *blockhist, int T, int K, int E,
+                               hipStream_t s);
 hipError_t init_route_attributes();
+// decode routing for 1 <= T <= 16 tokens (bf16) in one launch: logits plus
+// bias to L, then, in the last workgroup to finish, top-K, softmax and
+// permutation.  `arrive` is a zero device word that the launch leaves zero;
+// launches that share it must not overlap.
+hipError_t launch_route_decode(const uint16_t *x, const uint16_t *wr, const float *bias, float *L,
+                               uint32_t *arrive, const RouteOut &o, int T, int d, int K, int E, hipStream_t s);
 
 // ---- expert projections (experts.hip).  `items` lists the experts of one
 // launch (device memory), `n_tiles` the launch's total tile count.
@@ -92,9 +102,11 @@ struct ExpertLaunch {
     void *y;                     // [rows, d] weighted expert outputs (bf16; f32 for f32 layers)
     const float *row_weight;     // per permuted row, or null (1.0)
     int d, I;
-    // device-built work list: {n_items, n_tiles} read by the kernel (the
-    // grid is an upper bound; workgroups past n_tiles exit), or null
-    const int32_t *dev_counts;
+    // device-built work list (stream kernels only): items resolved by each
+    // workgroup from the routing's demanded experts and the residency table;
+    // the grid (n_tiles) is then an upper bound and workgroups past the last
+    // item exit.  direct.demand null: `items` is the list.
+    DirectList direct;
 };
 
 // tiles per item of each launch kind
@@ -123,23 +135,20 @@ hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t init_q4_attributes();
 
-// Device-built stream-path work list of one forward whose demanded experts
-// are all published (one workgroup): shared expert first, then demanded
-// experts in ascending id; a demanded expert without a published slot sets
-// STATUS_MISS in *status and gets an item that writes nothing.  info =
-// {n_gu, tiles_gu, n_dn, tiles_dn}; host_counts[E] (pinned host words,
-// device-visible address) receives the per-expert token counts.
-hipError_t launch_fast_worklist(const int32_t *counts, const int32_t *offsets, const int32_t *slot_of,
-                                const uint32_t *gen_of, int E, int T, int has_shared, int tpg, int tpd,
-                                WorkItem *gu, WorkItem *dn, int32_t *info, uint32_t *status, uint32_t *host_counts,
-                                hipStream_t s);
-
 // ---- combine / publication and slot generation words (combine.hip)
-// out[t] = ys[t] + sum_k y[inv[t, k]] in that order (y, ys bf16, or fp32 when f32),
-// unless *status is nonzero; *status is also copied to host_status (a pinned
-// host word, device-visible address), if given
+// Status word of a forward and where the combine publishes it.
+struct CombinePublish {
+    uint32_t *status;            // device status word
+    uint32_t *arrive;            // zero device word, left zero: the last workgroup to read the status
+                                 // clears it; or null (large grids): the word is left as it is
+    uint32_t *host;              // pinned host words (device-visible address), or null:
+                                 // [0] status | STATUS_DONE, then, with demand, [1] count, [2..] ids
+    const int32_t *demand;       // routing's demanded experts, or null
+};
+// out[t] = ys[t] + sum_k y[inv[t, k]] in that order (y, ys bf16, or fp32 when
+// f32), unless the status word is nonzero
 hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
-                          const uint32_t *status, uint32_t *host_status, int T, int K, int d, hipStream_t s);
+                          const CombinePublish &P, int T, int K, int d, hipStream_t s);
 constexpr int GEN_BATCH = 64;
 struct GenBatch {
     uint32_t n;

@@ -56,7 +56,7 @@ uint64_t object_bytes_of(const msi_plan_desc &d)
 
 // Workspace layout for T tokens (offsets in bytes, each region 256-aligned).
 struct Workspace {
-    size_t logits, parts, blockhist, act, act_s, y, ys, total;
+    size_t logits, blockhist, act, act_s, y, ys, total;
 };
 
 Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
@@ -68,8 +68,6 @@ Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
     size_t off = 0;
     w.logits = off;
     off += align256(T * E * 4);
-    w.parts = off;              // router partial sums (T <= 16)
-    off += align256(T <= 16 ? ROUTER_SPLIT * T * E * 4 : 0);
     w.blockhist = off;
     off += align256(std::max<uint64_t>(nblk, 1) * E * 4);
     w.act = off;
@@ -109,8 +107,9 @@ struct msi_plan {
     int32_t *res_slot_dev = nullptr;    // [n_layers][E] published global slot or -1
     uint32_t *res_gen_dev = nullptr;    // [n_layers][E]
     int32_t *res_host = nullptr;        // pinned staging [2 * E]
-    int32_t *info_dev = nullptr;        // {n_gu, tiles_gu, n_dn, tiles_dn}
-    uint32_t *tail_host = nullptr;      // pinned [1 + E]: status, then per-expert counts (written by kernels)
+    uint32_t *arrive_dev = nullptr;     // arrival counters (zero between launches): [ARRIVE_ROUTE], [ARRIVE_COMBINE]
+    bool status_clean = true;           // status_dev is zero (the last forward's combine cleared it)
+    uint32_t *tail_host = nullptr;      // pinned [2 + E]: status | DONE, demanded count, ids (written by the combine)
     uint32_t *tail_hdev = nullptr;      // device-visible address of tail_host
     uint32_t *status_hdev = nullptr;    // device-visible address of status_host
     std::vector<uint64_t> res_version;  // per layer: layer version uploaded
@@ -281,7 +280,34 @@ msi_status enqueue_fills(msi_plan *p, uint32_t layer, const std::vector<FillReco
 
 bool routing_ok(const msi_routing &r)
 {
-    return r.idx && r.weights && r.counts && r.offsets && r.perm && r.inv && r.row_weight;
+    return r.idx && r.weights && r.counts && r.offsets && r.demand && r.perm && r.inv && r.row_weight;
+}
+
+RouteOut route_out(const msi_routing &r)
+{
+    return RouteOut{r.idx, r.weights, r.counts, r.offsets, r.demand, r.perm, r.inv, r.row_weight};
+}
+
+constexpr int ARRIVE_ROUTE = 0, ARRIVE_COMBINE = 32;   // words of arrive_dev, 128 bytes apart
+
+// Wait for the combine of a direct forward to publish STATUS_DONE in the
+// pinned word w.  The host spins on the word (no interrupt wake-up); every
+// 256 polls it asks the stream, so a stream that failed, or finished without
+// publishing, ends the wait with an error.
+hipError_t wait_published(const uint32_t *w, hipStream_t s)
+{
+    for (uint32_t i = 1;; ++i) {
+        if (__atomic_load_n(w, __ATOMIC_ACQUIRE) & STATUS_DONE)
+            return hipSuccess;
+        if ((i & 255u) == 0) {
+            const hipError_t e = hipStreamQuery(s);
+            if (e == hipSuccess)
+                return (__atomic_load_n(w, __ATOMIC_ACQUIRE) & STATUS_DONE) ? hipSuccess : hipErrorUnknown;
+            if (e != hipErrorNotReady)
+                return e;
+        }
+        __builtin_ia32_pause();
+    }
 }
 
 }  // namespace
@@ -346,19 +372,21 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         hipMalloc(&p->status_dev, sizeof(uint32_t) * (E + 64)) != hipSuccess ||
         hipMalloc(&p->res_slot_dev, sizeof(int32_t) * E * NL) != hipSuccess ||
         hipMalloc(&p->res_gen_dev, sizeof(uint32_t) * E * NL) != hipSuccess ||
-        hipMalloc(&p->info_dev, 64) != hipSuccess ||
+        hipMalloc(&p->arrive_dev, 256) != hipSuccess ||
         hipMalloc(&p->table_dev, p->table_cap * sizeof(WorkItem)) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "device allocation failed");
     if (hipHostMalloc(&p->table_host, p->table_cap * sizeof(WorkItem), hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc(&p->counts_host, sizeof(int32_t) * desc->n_experts, hipHostMallocDefault) != hipSuccess ||
-        hipHostMalloc(&p->status_host, 256, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->status_host, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
         hipHostMalloc(&p->res_host, sizeof(int32_t) * 2 * E, hipHostMallocDefault) != hipSuccess ||
-        hipHostMalloc(&p->tail_host, sizeof(uint32_t) * (E + 1), hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&p->tail_host, sizeof(uint32_t) * (E + 2), hipHostMallocMapped | hipHostMallocCoherent) !=
+            hipSuccess ||
         hipHostGetDevicePointer(reinterpret_cast<void **>(&p->tail_hdev), p->tail_host, 0) != hipSuccess ||
         hipHostGetDevicePointer(reinterpret_cast<void **>(&p->status_hdev), p->status_host, 0) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "pinned host allocation failed");
     if (hipMemset(p->gen_dev, 0, nslots * sizeof(uint32_t)) != hipSuccess ||
         hipMemset(p->status_dev, 0, sizeof(uint32_t) * (E + 64)) != hipSuccess ||
+        hipMemset(p->arrive_dev, 0, 256) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess)
         return cleanup(MSI_E_DEVICE, "device initialisation failed");
     *out = p;
@@ -393,8 +421,8 @@ msi_status msi_plan_destroy(msi_plan *p)
         (void)hipFree(p->res_slot_dev);
     if (p->res_gen_dev)
         (void)hipFree(p->res_gen_dev);
-    if (p->info_dev)
-        (void)hipFree(p->info_dev);
+    if (p->arrive_dev)
+        (void)hipFree(p->arrive_dev);
     if (p->res_host)
         (void)hipHostFree(p->res_host);
     if (p->tail_host)
@@ -489,7 +517,7 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
     float *L = reinterpret_cast<float *>(wsb + ws.logits);
-    float *P = nullptr;
+    const RouteOut o = route_out(a->r);
     if (T > 0) {
         if (d.wdtype == MSI_W_F32)
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
@@ -497,11 +525,13 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
                                                 static_cast<const float *>(a->w_router), a->bias, L, T, D, E, s);
             }));
         else if (T <= 16) {
-            P = reinterpret_cast<float *>(wsb + ws.parts);
+            // logits, selection and permutation in one launch
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
-                return launch_router_stream(static_cast<const uint16_t *>(a->x),
-                                            static_cast<const uint16_t *>(a->w_router), P, T, D, E, s);
+                return launch_route_decode(static_cast<const uint16_t *>(a->x),
+                                           static_cast<const uint16_t *>(a->w_router), a->bias, L,
+                                           p->arrive_dev + ARRIVE_ROUTE, o, T, D, K, E, s);
             }));
+            return MSI_OK;
         } else
             HIP_OK(p->timed_launch(MSI_K_ROUTER_LOGITS, s, [&] {
                 return launch_router_logits_bf16(static_cast<const uint16_t *>(a->x),
@@ -509,9 +539,7 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
             }));
     }
     HIP_OK(p->timed_launch(MSI_K_TOPK, s, [&] {
-        return launch_route_select(L, P, a->bias, a->r.idx, a->r.weights, a->r.counts, a->r.offsets, a->r.perm,
-                                   a->r.inv, a->r.row_weight, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K,
-                                   E, s);
+        return launch_route_select(L, o, reinterpret_cast<int32_t *>(wsb + ws.blockhist), T, K, E, s);
     }));
     return MSI_OK;
 }
@@ -559,14 +587,11 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         const int tpg = q4w ? tiles_gateup_q4_stream(1, D, I) : tiles_gateup_stream(1, D, I);
         const int tpd = q4w ? tiles_down_q4_stream(1, D, I) : tiles_down_stream(1, D, I);
         const int has_sh = a->shared_object ? 1 : 0;
-        const int max_items = std::min(E, T * K) + has_sh;
-        WorkItem *gu = p->table_dev, *dn = p->table_dev + (E + 1);
-        p->tail_host[0] = 0u;     // overwritten by the combine of this forward
-        HIP_OK(p->timed_launch(MSI_K_WORKLIST, cs, [&] {
-            return launch_fast_worklist(a->r.counts, a->r.offsets, p->res_slot_dev + size_t(L0) * E,
-                                        p->res_gen_dev + size_t(L0) * E, E, T, has_sh, tpg, tpd, gu, dn,
-                                        p->info_dev, p->status_dev, p->tail_hdev + 1, cs);
-        }));
+        const int max_items = (std::min(E, T * K) + has_sh + 7) / 8 * 8;   // whole rounds of 8 items (XCDs)
+        if (!p->status_clean)
+            HIP_OK(launch_clear_word(p->status_dev, cs));
+        p->status_clean = false;
+        __atomic_store_n(&p->tail_host[0], 0u, __ATOMIC_RELAXED);   // the combine of this forward sets STATUS_DONE
         ExpertLaunch X{};
         X.x = a->x;
         X.perm = a->r.perm;
@@ -582,30 +607,29 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         X.ys = wsb + ws.ys;
         X.d = D;
         X.I = I;
+        X.direct = DirectList{a->r.demand, p->res_slot_dev + size_t(L0) * E, p->res_gen_dev + size_t(L0) * E,
+                              a->r.counts, a->r.offsets, has_sh, T, E};
         ExpertLaunch G = X, Dn = X;
-        G.items = gu;
         G.n_tiles = max_items * tpg;
-        G.dev_counts = p->info_dev;
-        Dn.items = dn;
         Dn.n_tiles = max_items * tpd;
-        Dn.dev_counts = p->info_dev + 2;
         HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs,
                                [&] { return q4w ? launch_gateup_q4_stream(G, cs) : launch_gateup_stream(G, cs); }));
         HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
                                [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
+        const CombinePublish pub{p->status_dev, p->arrive_dev + ARRIVE_COMBINE, p->tail_hdev, a->r.demand};
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
-            return launch_combine(wsb + ws.y, has_sh ? wsb + ws.ys : nullptr, false, a->r.inv, a->out,
-                                  p->status_dev, p->tail_hdev, T, K, D, cs);
+            return launch_combine(wsb + ws.y, has_sh ? wsb + ws.ys : nullptr, false, a->r.inv, a->out, pub, T, K,
+                                  D, cs);
         }));
-        // the work list kernel wrote the counts and the combine the status
-        // straight into tail_host: no copy, one synchronisation
-        HIP_OK(hipStreamSynchronize(cs));
-        const uint32_t st = p->tail_host[0];
+        p->status_clean = true;
+        // the combine publishes the status and the demanded experts straight
+        // into tail_host once the expert kernels are done; the output rows it
+        // is still writing are ordered before later work on the stream
+        HIP_OK(wait_published(&p->tail_host[0], cs));
+        const uint32_t st = __atomic_load_n(&p->tail_host[0], __ATOMIC_ACQUIRE);
         if (!(st & STATUS_MISS)) {
-            std::vector<int32_t> dem;
-            for (int e = 0; e < E; ++e)
-                if (p->tail_host[1 + e])
-                    dem.push_back(e);
+            const uint32_t n = std::min<uint32_t>(p->tail_host[1], uint32_t(E));
+            std::vector<int32_t> dem(p->tail_host + 2, p->tail_host + 2 + n);
             if (st & STATUS_STALE) {
                 core.stats().stale_detected++;
                 core.stats().forwards++;
@@ -704,7 +728,9 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         HIP_OK(hipMemcpyAsync(p->table_dev, p->table_host, table.size() * sizeof(WorkItem), hipMemcpyHostToDevice,
                               cs));
     }
-    HIP_OK(launch_clear_word(p->status_dev, cs));
+    if (!p->status_clean)
+        HIP_OK(launch_clear_word(p->status_dev, cs));
+    p->status_clean = false;            // set again below once the word is read back as zero
 
     // ---- rounds: fills on the side stream, kernels on the compute stream
     std::vector<hipEvent_t> round_events;
@@ -806,18 +832,24 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     }
 
     // ---- publication: out written only if every tile saw its generation; the
-    // combine copies the status word to status_host (no launch when T == 0)
+    // combine publishes the status word to status_host (also when T == 0)
     *p->status_host = 0u;
-    if (rst == MSI_OK)
+    if (rst == MSI_OK) {
+        // no arrival counter: one counter update per workgroup of a large grid costs more than the clear
+        const CombinePublish pub{p->status_dev, nullptr, p->status_hdev, nullptr};
         if (p->timed_launch(MSI_K_COMBINE, cs, [&] {
                 return launch_combine(wsb + ws.y, has_shared ? wsb + ws.ys : nullptr, f32w, a->r.inv,
-                                      a->out, p->status_dev, p->status_hdev, T, K, D, cs);
+                                      a->out, pub, T, K, D, cs);
             }) != hipSuccess)
             rst = fail(MSI_E_DEVICE, "combine launch failed");
+    }
     const hipError_t se = hipStreamSynchronize(cs);
     (void)hipStreamSynchronize(side);
     if (se != hipSuccess && rst == MSI_OK)
         rst = fail(MSI_E_DEVICE, std::string("compute stream: ") + hipGetErrorString(se));
+    // the device word still holds what the combine read: clean if that was zero
+    const uint32_t hst = __atomic_load_n(p->status_host, __ATOMIC_ACQUIRE);
+    p->status_clean = rst == MSI_OK && hst == STATUS_DONE;
 
     // ---- layer exit: observe this forward's fills, release consumers
     for (const SchedRound &round : sched.rounds)
@@ -844,7 +876,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     }
     if (rst != MSI_OK)
         return rst;
-    if (*p->status_host & STATUS_STALE) {
+    if (hst & STATUS_STALE) {
         core.stats().stale_detected++;
         core.invalidate_read_slots(a->layer, sched);
         p->direct_ok[a->layer] = 0;

@@ -47,58 +47,6 @@ __global__ void __launch_bounds__(256) router_logits_f32_kernel(const float *__r
     L[i] = acc + (bias ? bias[e] : 0.f);
 }
 
-// ---------------------------------------------------------------- logits, bf16, T <= 16
-// Weight streaming with the reduction split across workgroups: workgroup b
-// takes experts 16 (b % G) .. +15 and quarter b / G of the K steps of 32; its
-// four wavefronts take consecutive sixteenths of the K steps, so each lane
-// issues all of its loads at once (router rows as the 16x16x32 MFMA A operand,
-// token rows as the B operand, both straight from memory).  The wavefront
-// sums are added in wavefront order and the workgroup stores its partial
-// P[q][t][e]; the selection kernel adds the quarters in order and the bias.
-__global__ void __launch_bounds__(256) router_stream_kernel(const uint16_t *__restrict__ x,
-                                                            const uint16_t *__restrict__ wr, float *__restrict__ P,
-                                                            int T, int d, int E)
-{
-    __shared__ f32x4 red[3][64];
-    const int G = (E + 15) / 16;
-    const int g = int(blockIdx.x) % G, q = int(blockIdx.x) / G;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nks = d / 32;
-    const int per = (nks + ROUTER_SPLIT * 4 - 1) / (ROUTER_SPLIT * 4);
-    const int s0 = min((q * 4 + wave) * per, nks), s1 = min(s0 + per, nks);
-    const int e0 = g * 16;
-    const int j = lane & 15, kg = (lane >> 4) * 8;
-    // rows past E and tokens past T read a valid row; their sums are never stored
-    const uint16_t *wp = wr + int64_t(min(e0 + j, E - 1)) * d + kg;
-    const uint16_t *xp = x + int64_t(min(j, T - 1)) * d + kg;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int st = s0; st < s1; st += 4) {
-        u32x4 w[4], xv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int k = min(st + u, s1 - 1) * 32;       // clamped: no branch around the loads
-            w[u] = load_stream16(wp + k);
-            xv[u] = *reinterpret_cast<const u32x4 *>(xp + k);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (st + u < s1)
-                acc = mfma16(as_bf16x8(w[u]), as_bf16x8(xv[u]), acc);
-    }
-    if (wave > 0)
-        red[wave - 1][lane] = acc;
-    __syncthreads();
-    if (wave == 0 && j < T) {
-        float *Pq = P + (int64_t(q) * T + j) * E;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int e = e0 + 4 * (lane >> 4) + r;
-            if (e < E)
-                Pq[e] = ((acc[r] + red[0][lane][r]) + red[1][lane][r]) + red[2][lane][r];
-        }
-    }
-}
-
 // ---------------------------------------------------------------- top-K
 
 // Order-preserving key: a > b as floats <=> key(a) > key(b); -0.0 folds onto +0.0.
@@ -236,58 +184,19 @@ __device__ __forceinline__ void wave_select(const float (&v)[PER], int E, int K,
             emit(rank[j], lane + 64 * j, w[j] * inv);
 }
 
-// Logits of token t for lane's experts lane + 64 j (-inf past E): read from
-// L, or formed from the ROUTER_SPLIT partials P (added in order, then the
-// bias) and stored to Lw.  Every load is issued, at a clamped index, before
-// any is used, so the row costs one memory round trip.
+// Logits of token t for lane's experts lane + 64 j (-inf past E).  Every load
+// is issued, at a clamped index, before any is used, so the row costs one
+// memory round trip.
 template <int PER>
-__device__ __forceinline__ void load_logits(float (&v)[PER], const float *L, float *Lw, const float *__restrict__ P,
-                                            const float *__restrict__ bias, int t, int T, int E, int lane)
+__device__ __forceinline__ void load_logits(float (&v)[PER], const float *L, int t, int E, int lane)
 {
-    int ec[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j)
-        ec[j] = min(lane + 64 * j, E - 1);
-    if (!P) {
+        v[j] = L[int64_t(t) * E + min(lane + 64 * j, E - 1)];
 #pragma unroll
-        for (int j = 0; j < PER; ++j)
-            v[j] = L[int64_t(t) * E + ec[j]];
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-            if (lane + 64 * j >= E)
-                v[j] = -INFINITY;
-        return;
-    }
-    float pa[ROUTER_SPLIT][PER], bb[PER];
-#pragma unroll
-    for (int q = 0; q < ROUTER_SPLIT; ++q)
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-            pa[q][j] = P[(int64_t(q) * T + t) * E + ec[j]];
-    if (bias) {
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-            bb[j] = bias[ec[j]];
-    } else {
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-            bb[j] = 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        float a = pa[0][j];
-#pragma unroll
-        for (int q = 1; q < ROUTER_SPLIT; ++q)
-            a += pa[q][j];
-        v[j] = a + bb[j];
-    }
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        if (lane + 64 * j < E)
-            Lw[int64_t(t) * E + lane + 64 * j] = v[j];
-        else
+    for (int j = 0; j < PER; ++j)
+        if (lane + 64 * j >= E)
             v[j] = -INFINITY;
-    }
 }
 
 template <int PER>
@@ -301,7 +210,7 @@ __global__ void __launch_bounds__(256) topk_kernel(const float *__restrict__ L, 
     if (t >= T)
         return;
     float v[PER];
-    load_logits<PER>(v, L, nullptr, nullptr, nullptr, t, T, E, lane);
+    load_logits<PER>(v, L, t, E, lane);
     wave_select<PER>(v, E, K, lane, cand_v[wave], cand_e[wave], [&](int rank, int e, float w) {
         idx[int64_t(t) * K + rank] = e;
         wout[int64_t(t) * K + rank] = w;
@@ -365,7 +274,8 @@ __global__ void __launch_bounds__(256) perm_hist_kernel(const int32_t *__restric
 // (loads issued 16 at a time), then an exclusive scan over experts.
 __global__ void __launch_bounds__(1024) perm_scan_kernel(int32_t *__restrict__ blockhist, int nblk, int E,
                                                          int32_t *__restrict__ counts,
-                                                         int32_t *__restrict__ offsets)
+                                                         int32_t *__restrict__ offsets,
+                                                         int32_t *__restrict__ demand)
 {
     __shared__ int32_t part[1024];
     const int e = threadIdx.x;
@@ -392,6 +302,14 @@ __global__ void __launch_bounds__(1024) perm_scan_kernel(int32_t *__restrict__ b
         offsets[e] = part[e] - run;
     if (e == E - 1)
         offsets[E] = part[e];
+    __syncthreads();
+    part[e] = e < E && run > 0 ? 1 : 0;
+    __syncthreads();
+    block_scan_1024(part);
+    if (e < E && run > 0)
+        demand[part[e]] = e;                    // demanded experts, ascending, after the count
+    if (e == E - 1)
+        demand[0] = part[e];
 }
 
 __global__ void __launch_bounds__(256) perm_scatter_kernel(const int32_t *__restrict__ idx,
@@ -438,26 +356,19 @@ __device__ __forceinline__ int block_scan_incl_1024(int v, int32_t *wsum)
     return v + base;
 }
 
-// T <= PERM_BLOCK: top-K of every token (one wavefront per token), then the
-// histogram, scans and scatter, in one 1024-thread workgroup, with a bitmask
-// of W = ceil(T / 32) words per expert.  The logits come from L, or, when P
-// is given, are formed here from the router's ROUTER_SPLIT partial sums
-// (added in order, then the bias) and stored to L.  With select == 0 the
-// selection is read from idx / w instead.
-template <int PER>
-__global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L, const float *__restrict__ P,
-                                                           const float *__restrict__ bias, int select,
-                                                           int32_t *__restrict__ idx, float *__restrict__ w,
-                                                           int32_t *__restrict__ counts,
-                                                           int32_t *__restrict__ offsets, int32_t *__restrict__ perm,
-                                                           int32_t *__restrict__ inv, float *__restrict__ row_weight,
-                                                           int T, int K, int E)
+// T <= TMAX (<= PERM_BLOCK): top-K of every token (one wavefront per token),
+// then the histogram, scans and scatter, by one 1024-thread workgroup, with a
+// bitmask of W = ceil(T / 32) words per expert (`bits`, E * W words of LDS).
+// The logits are read from L (bias included).  With select == 0 the
+// selection is read from o.idx / o.w instead.
+template <int PER, int TMAX>
+__device__ __forceinline__ void route_small_body(uint32_t *bits, const float *L, int select, const RouteOut &o,
+                                                 int T, int K, int E)
 {
-    extern __shared__ uint32_t bits[];          // [E][W]
     __shared__ int32_t excl[1024];              // first permuted row of each expert
     __shared__ int32_t wsum[16];
-    __shared__ int32_t sidx[PERM_BLOCK * 16];   // this workgroup's selection (T * K <= 4096)
-    __shared__ float sw[PERM_BLOCK * 16];
+    __shared__ int32_t sidx[TMAX * 16];         // this workgroup's selection (K <= 16)
+    __shared__ float sw[TMAX * 16];
     __shared__ float cand_v[16][64];
     __shared__ int32_t cand_e[16][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -468,10 +379,10 @@ __global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L
     if (select) {
         for (int t = wave; t < T; t += 16) {
             float v[PER];
-            load_logits<PER>(v, L, L, P, bias, t, T, E, lane);
+            load_logits<PER>(v, L, t, E, lane);
             wave_select<PER>(v, E, K, lane, cand_v[wave], cand_e[wave], [&](int rank, int e, float wt) {
-                idx[t * K + rank] = e;
-                w[t * K + rank] = wt;
+                o.idx[t * K + rank] = e;
+                o.w[t * K + rank] = wt;
                 sidx[t * K + rank] = e;
                 sw[t * K + rank] = wt;
                 atomicOr(&bits[e * W + (t >> 5)], 1u << (t & 31));
@@ -479,9 +390,9 @@ __global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L
         }
     } else {
         for (int a = threadIdx.x; a < T * K; a += blockDim.x) {
-            const int t = a / K, e = idx[a];
+            const int t = a / K, e = o.idx[a];
             sidx[a] = e;
-            sw[a] = w[a];
+            sw[a] = o.w[a];
             atomicOr(&bits[e * W + (t >> 5)], 1u << (t & 31));
         }
     }
@@ -491,14 +402,20 @@ __global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L
     if (e < E)
         for (int q = 0; q < W; ++q)
             c += __popc(bits[e * W + q]);
-    const int incl = block_scan_incl_1024(c, wsum);
+    // one scan of (demanded << 16) + count: T * K <= 4096 keeps the halves apart
+    const int packed = block_scan_incl_1024(c | (c > 0 ? 0x10000 : 0), wsum);
+    const int incl = packed & 0xFFFF, nz = packed >> 16;
     excl[e] = incl - c;
     if (e < E) {
-        counts[e] = c;
-        offsets[e] = incl - c;
+        o.counts[e] = c;
+        o.offsets[e] = incl - c;
+        if (c > 0)
+            o.demand[nz] = e;                   // demanded experts, ascending, after the count
     }
-    if (e == E - 1)
-        offsets[E] = incl;
+    if (e == E - 1) {
+        o.offsets[E] = incl;
+        o.demand[0] = nz;
+    }
     __syncthreads();
     for (int a = threadIdx.x; a < T * K; a += blockDim.x) {
         const int t = a / K;
@@ -508,10 +425,104 @@ __global__ void __launch_bounds__(1024) route_small_kernel(float *__restrict__ L
         for (int q = 0; q < (t >> 5); ++q)
             r += __popc(row[q]);
         r += __popc(row[t >> 5] & ((1u << (t & 31)) - 1u));
-        perm[r] = t;
-        inv[a] = r;
-        row_weight[r] = sw[a];
+        o.perm[r] = t;
+        o.inv[a] = r;
+        o.row_weight[r] = sw[a];
     }
+}
+
+template <int PER>
+__global__ void __launch_bounds__(1024) route_small_kernel(const float *__restrict__ L, int select, RouteOut o,
+                                                           int T, int K, int E)
+{
+    extern __shared__ uint32_t bits[];          // [E][W]
+    route_small_body<PER, PERM_BLOCK>(bits, L, select, o, T, K, E);
+}
+
+// ---------------------------------------------------------------- decode routing, bf16, T <= 16
+// Logits, selection and permutation in one launch.  Workgroup g (16
+// wavefronts) streams router rows 16 g .. 16 g + 15: its wavefronts take
+// consecutive sixteenths of the K steps of 32, so each lane issues all of its
+// loads at once (router rows as the 16x16x32 MFMA A operand, token rows as
+// the B operand, both straight from memory).  The wavefront sums are added in
+// a fixed order (four groups of four wavefronts, each group in wavefront
+// order, then the groups in order, then the bias).  After storing its logits
+// each workgroup releases them and counts itself in; the last to arrive (the
+// counter wraps back to zero on its arrival) acquires every workgroup's
+// logits and runs the selection and permutation of route_small_kernel.  No
+// workgroup waits for another, so the launch completes in any schedule.
+template <int PER>
+__global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__restrict__ x,
+                                                            const uint16_t *__restrict__ wr,
+                                                            const float *__restrict__ bias, float *L,
+                                                            uint32_t *__restrict__ arrive, RouteOut o, int T, int d,
+                                                            int K, int E)
+{
+    extern __shared__ uint32_t bits[];          // [E][1]
+    __shared__ f32x4 red[16][64];
+    __shared__ uint32_t last;
+    constexpr int GROUPS = 4, WPG = 16 / GROUPS;   // summation groups, wavefronts per group
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nks = d / 32;
+    const int per = (nks + 15) / 16;
+    const int s0 = min(wave * per, nks), s1 = min(s0 + per, nks);
+    const int e0 = int(blockIdx.x) * 16;
+    const int j = lane & 15, kg = (lane >> 4) * 8;
+    // rows past E and tokens past T read a valid row; their sums are never stored
+    const uint16_t *wp = wr + int64_t(min(e0 + j, E - 1)) * d + kg;
+    const uint16_t *xp = x + int64_t(min(j, T - 1)) * d + kg;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int st = s0; st < s1; st += 4) {
+        u32x4 wv[4], xv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int k = min(st + u, s1 - 1) * 32;       // clamped: no branch around the loads
+            wv[u] = load_stream16(wp + k);
+            xv[u] = *reinterpret_cast<const u32x4 *>(xp + k);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (st + u < s1)
+                acc = mfma16(as_bf16x8(wv[u]), as_bf16x8(xv[u]), acc);
+    }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+        float bv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            bv[r] = bias ? bias[min(e0 + 4 * (lane >> 4) + r, E - 1)] : 0.f;
+        if (j < T) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int e = e0 + 4 * (lane >> 4) + r;
+                float a = 0.f;
+#pragma unroll
+                for (int q = 0; q < GROUPS; ++q) {
+                    float pq = red[q * WPG][lane][r];
+#pragma unroll
+                    for (int u = 1; u < WPG; ++u)
+                        pq += red[q * WPG + u][lane][r];
+                    a = q == 0 ? pq : a + pq;
+                }
+                if (e < E)
+                    L[int64_t(j) * E + e] = a + bv[r];
+            }
+        }
+        // release: only this wavefront stored logits
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const bool is_last = atomicInc(arrive, gridDim.x - 1u) == gridDim.x - 1u;
+        if (is_last)
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every workgroup's logits
+        last = is_last ? 1u : 0u;
+    }
+    __syncthreads();                            // orders this workgroup's reads after the acquire
+    if (!last)
+        return;
+    route_small_body<PER, 16>(bits, L, 1, o, T, K, E);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -540,58 +551,69 @@ hipError_t launch_router_logits_f32(const float *x, const float *wr, const float
     return hipGetLastError();
 }
 
-hipError_t launch_router_stream(const uint16_t *x, const uint16_t *wr, float *P, int T, int d, int E,
-                                hipStream_t s)
+template <int PER>
+static void launch_route_decode_t(const uint16_t *x, const uint16_t *wr, const float *bias, float *L,
+                                  uint32_t *arrive, const RouteOut &o, int T, int d, int K, int E, hipStream_t s)
 {
-    if (T <= 0 || T > 16)
+    launch_k(route_decode_kernel<PER>, unsigned((E + 15) / 16), 1024, size_t(E) * sizeof(uint32_t), s, x, wr, bias,
+             L, arrive, o, T, d, K, E);
+}
+
+hipError_t launch_route_decode(const uint16_t *x, const uint16_t *wr, const float *bias, float *L,
+                               uint32_t *arrive, const RouteOut &o, int T, int d, int K, int E, hipStream_t s)
+{
+    if (T <= 0 || T > 16 || E <= 0 || E > 1024 || K <= 0 || K > 16 || d % 32 != 0 || !arrive)
         return hipErrorInvalidValue;
-    launch_k(router_stream_kernel, unsigned((E + 15) / 16 * ROUTER_SPLIT), 256, 0, s, x, wr, P, T, d, E);
+    const int per = (E + 63) / 64;
+    if (per <= 2)
+        launch_route_decode_t<2>(x, wr, bias, L, arrive, o, T, d, K, E, s);
+    else if (per <= 4)
+        launch_route_decode_t<4>(x, wr, bias, L, arrive, o, T, d, K, E, s);
+    else if (per <= 8)
+        launch_route_decode_t<8>(x, wr, bias, L, arrive, o, T, d, K, E, s);
+    else
+        launch_route_decode_t<16>(x, wr, bias, L, arrive, o, T, d, K, E, s);
     return hipGetLastError();
 }
 
 template <int PER>
-static void launch_route_small_t(float *L, const float *P, const float *bias, int32_t *idx, float *w,
-                                 int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
-                                 int T, int K, int E, hipStream_t s)
+static void launch_route_small_t(const float *L, const RouteOut &o, int T, int K, int E, hipStream_t s)
 {
     const size_t lds = size_t(E) * std::max((T + 31) / 32, 1) * sizeof(uint32_t);
-    launch_k(route_small_kernel<PER>, 1, 1024, lds, s, L, P, bias, T > 0 ? 1 : 0, idx, w, counts, offsets, perm,
-             inv, row_weight, T, K, E);
+    launch_k(route_small_kernel<PER>, 1, 1024, lds, s, L, T > 0 ? 1 : 0, o, T, K, E);
 }
 
-hipError_t launch_route_select(float *L, const float *P, const float *bias, int32_t *idx, float *w,
-                               int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *inv, float *row_weight,
-                               int32_t *blockhist, int T, int K, int E, hipStream_t s)
+hipError_t launch_route_select(const float *L, const RouteOut &o, int32_t *blockhist, int T, int K, int E,
+                               hipStream_t s)
 {
     const int per = (E + 63) / 64;
     if (T <= PERM_BLOCK) {
-        // T == 0 still writes zero counts and offsets
+        // T == 0 still writes zero counts, offsets and demand
         if (per <= 2)
-            launch_route_small_t<2>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<2>(L, o, T, K, E, s);
         else if (per <= 4)
-            launch_route_small_t<4>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<4>(L, o, T, K, E, s);
         else if (per <= 8)
-            launch_route_small_t<8>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<8>(L, o, T, K, E, s);
         else
-            launch_route_small_t<16>(L, P, bias, idx, w, counts, offsets, perm, inv, row_weight, T, K, E, s);
+            launch_route_small_t<16>(L, o, T, K, E, s);
         return hipGetLastError();
     }
-    if (P)
-        return hipErrorInvalidValue;      // partial logits are produced for T <= 16 only
     const dim3 grid(unsigned((T + 3) / 4)), block(256);
     if (per <= 2)
-        launch_k(topk_kernel<2>, grid, block, 0, s, L, idx, w, T, E, K);
+        launch_k(topk_kernel<2>, grid, block, 0, s, L, o.idx, o.w, T, E, K);
     else if (per <= 4)
-        launch_k(topk_kernel<4>, grid, block, 0, s, L, idx, w, T, E, K);
+        launch_k(topk_kernel<4>, grid, block, 0, s, L, o.idx, o.w, T, E, K);
     else if (per <= 8)
-        launch_k(topk_kernel<8>, grid, block, 0, s, L, idx, w, T, E, K);
+        launch_k(topk_kernel<8>, grid, block, 0, s, L, o.idx, o.w, T, E, K);
     else
-        launch_k(topk_kernel<16>, grid, block, 0, s, L, idx, w, T, E, K);
+        launch_k(topk_kernel<16>, grid, block, 0, s, L, o.idx, o.w, T, E, K);
     const size_t lds = size_t(E) * (PERM_BLOCK / 32) * sizeof(uint32_t);
     const int nblk = (T + PERM_BLOCK - 1) / PERM_BLOCK;
-    launch_k(perm_hist_kernel, nblk, 256, lds, s, idx, blockhist, T, K, E);
-    launch_k(perm_scan_kernel, 1, 1024, 0, s, blockhist, nblk, E, counts, offsets);
-    launch_k(perm_scatter_kernel, nblk, 256, lds, s, idx, w, blockhist, offsets, perm, inv, row_weight, T, K, E);
+    launch_k(perm_hist_kernel, nblk, 256, lds, s, o.idx, blockhist, T, K, E);
+    launch_k(perm_scan_kernel, 1, 1024, 0, s, blockhist, nblk, E, o.counts, o.offsets, o.demand);
+    launch_k(perm_scatter_kernel, nblk, 256, lds, s, o.idx, o.w, blockhist, o.offsets, o.perm, o.inv, o.row_weight,
+             T, K, E);
     return hipGetLastError();
 }
 

@@ -79,6 +79,7 @@ def run_layer(plan, dl: DeviceLayer, T: Optional[int] = None, compute=None, side
     L = ws[: T * s.E * 4].view(torch.float32).view(T, s.E)
     return {"status": st, "out": out, "idx": r.idx.cpu().numpy(), "w": r.weights.cpu().numpy(),
             "counts": r.counts.cpu().numpy(), "offsets": r.offsets.cpu().numpy(),
+            "demand": r.demand.cpu().numpy(),
             "perm": r.perm.cpu().numpy(), "inv": r.inv.cpu().numpy(),
             "row_weight": r.row_weight.cpu().numpy(), "logits": L.cpu().numpy(), "routing": r}
 

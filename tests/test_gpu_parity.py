@@ -30,6 +30,9 @@ def _check_permutation(o, res, E):
     assert np.array_equal(res["idx"], np.sort(res["idx"], axis=1)), "idx not ascending"
     assert np.array_equal(res["counts"], counts)
     assert np.array_equal(res["offsets"], offsets)
+    demanded = np.nonzero(counts)[0]             # the demanded experts, ascending
+    assert res["demand"][0] == len(demanded)
+    assert np.array_equal(res["demand"][1:1 + len(demanded)], demanded)
     assert np.array_equal(res["perm"], perm)
     assert np.array_equal(res["inv"], inv)
     T, K = res["idx"].shape
