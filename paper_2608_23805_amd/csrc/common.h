@@ -169,6 +169,69 @@ __device__ __forceinline__ bool slot_current(const WorkItem &it, const uint32_t 
     return false;
 }
 
+// B-operand rows of one expert (n <= 16) staged into LDS [16][K + 8]:
+// wavefront w handles rows w, w + 4, w + 8, w + 12, so each row's source
+// index is wavefront-uniform; lane l takes 16-byte chunks l, l + 64, ...
+// One pass covers 64 * CPL chunks of a row; rows longer than that take
+// further passes.
+template <int CPL>
+struct StageRows {
+    u32x4 v[4][CPL];
+
+    __device__ __forceinline__ void load(const uint16_t *__restrict__ src, const int32_t *perm, int row0, int n,
+                                         int K, int pass)
+    {
+        // the wavefront index is uniform: the row indices below are scalar
+        const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+        const int lane = threadIdx.x & 63, cpr = K / 8;
+        int64_t srow[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {             // all source rows first (clamped, no branch)
+            const int r = min(wave + 4 * q, n - 1);
+            srow[q] = perm ? int64_t(perm[row0 + r]) : int64_t(row0 + r);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (wave + 4 * q < n) {
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int ch = lane + 64 * (pass * CPL + c);
+                    if (ch < cpr)
+                        v[q][c] = *reinterpret_cast<const u32x4 *>(src + srow[q] * K + ch * 8);
+                }
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(uint16_t *xs, int n, int K, int pass) const
+    {
+        const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+        const int lane = threadIdx.x & 63, cpr = K / 8;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int r = wave + 4 * q;
+            if (r < n) {
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int ch = lane + 64 * (pass * CPL + c);
+                    if (ch < cpr)
+                        *reinterpret_cast<u32x4 *>(xs + r * (K + 8) + ch * 8) = v[q][c];
+                }
+            }
+        }
+    }
+
+    // passes after the first (rows longer than 64 * CPL chunks)
+    __device__ __forceinline__ void rest(const uint16_t *__restrict__ src, const int32_t *perm, int row0, int n,
+                                         int K, uint16_t *xs)
+    {
+        for (int pass = 1; pass * 64 * CPL < K / 8; ++pass) {
+            load(src, perm, row0, n, K, pass);
+            store(xs, n, K, pass);
+        }
+    }
+};
+
 // ---- wavefront reductions (64 lanes)
 __device__ __forceinline__ float wave_max(float v)
 {

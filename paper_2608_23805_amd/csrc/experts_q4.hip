@@ -48,7 +48,7 @@ int tiles_gateup_q4_stream(int nrows, int d, int I)
 {
     (void)nrows;
     (void)d;
-    return I / (q4s::WAVES * q4s::ROWS);
+    return I / q4s::ROWS;
 }
 
 int tiles_down_q4_stream(int nrows, int d, int I)
@@ -56,64 +56,6 @@ int tiles_down_q4_stream(int nrows, int d, int I)
     (void)nrows;
     (void)I;
     return d / (q4s::WAVES * q4s::ROWS);
-}
-
-// Stage the (<= 16) B-operand rows (bf16) into LDS [16][K + 8], loads batched.
-__device__ __forceinline__ void q4_stage_rows(uint16_t *xs, const uint16_t *__restrict__ src, const int32_t *perm,
-                                              int row0, int n, int K)
-{
-    const int ldk = K + 8, chunks = K / 8, total = n * chunks;
-    for (int c0 = threadIdx.x; c0 < total; c0 += 8 * blockDim.x) {
-        u32x4 v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total) {
-                const int64_t r = perm ? int64_t(perm[row0 + c / chunks]) : int64_t(row0 + c / chunks);
-                v[u] = *reinterpret_cast<const u32x4 *>(src + r * K + (c % chunks) * 8);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int c = c0 + u * int(blockDim.x);
-            if (c < total)
-                *reinterpret_cast<u32x4 *>(xs + (c / chunks) * ldk + (c % chunks) * 8) = v[u];
-        }
-    }
-}
-
-// One wavefront: 16 rows of a q4 matrix [rows, K] against the staged tokens.
-// Lane (row r = lane % 16, k group g = lane / 16) loads the 4 bytes holding
-// elements 32b + 8g .. 32b + 8g + 7 of its row for block b; the output lane
-// (rows 4g..4g+3, token lane % 16) applies those rows' block scales.
-template <int U>
-__device__ __forceinline__ void q4_rows_dot(const uint8_t *__restrict__ nib, const uint16_t *__restrict__ scl,
-                                            int row0, int K, const uint16_t *xrow, int lane, f32x4 &acc)
-{
-    const int r = lane & 15, g = lane >> 4;
-    const int nblk = K / 32;
-    const uint32_t *qp = reinterpret_cast<const uint32_t *>(nib + int64_t(row0 + r) * (K / 2)) + g;
-    const uint16_t *sp = scl + int64_t(row0 + 4 * g) * nblk;
-    for (int b0 = 0; b0 < nblk; b0 += U) {
-        uint32_t q[U];
-        float s[4][U];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            q[u] = __builtin_nontemporal_load(qp + 4 * (b0 + u));
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                s[rr][u] = half_to_float(sp[rr * nblk + b0 + u]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4 *>(xrow + 32 * (b0 + u)));
-            const f32x4 part = mfma16(unpack_q4(q[u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                acc[rr] = fmaf(s[rr][u], part[rr], acc[rr]);
-        }
-    }
 }
 
 // Tile t of a stream launch and its item: from the device-built list (the
@@ -131,27 +73,124 @@ __device__ __forceinline__ bool q4_tile(const ExpertLaunch &L, int per_item, int
     return true;
 }
 
+// CH consecutive fp16 block scales of one row, in one vector load (the row's
+// scales start 16-byte aligned and CH divides the blocks of a quarter of d).
+template <int CH>
+__device__ __forceinline__ void load_scales(uint32_t (&w)[CH / 2], const uint16_t *p)
+{
+    if constexpr (CH == 16) {
+        const u32x4 a = reinterpret_cast<const u32x4 *>(p)[0], b = reinterpret_cast<const u32x4 *>(p)[1];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            w[i] = a[i];
+            w[4 + i] = b[i];
+        }
+    } else if constexpr (CH == 8) {
+        const u32x4 a = *reinterpret_cast<const u32x4 *>(p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w[i] = a[i];
+    } else if constexpr (CH == 4) {
+        const uint2 a = *reinterpret_cast<const uint2 *>(p);
+        w[0] = a.x;
+        w[1] = a.y;
+    } else {
+        w[0] = *reinterpret_cast<const uint32_t *>(p);
+    }
+}
+
+__device__ __forceinline__ float scale_at(const uint32_t *w, int b)
+{
+    return half_to_float(uint16_t(w[b >> 1] >> (16 * (b & 1))));
+}
+
+// Gate/up, 4-bit stream path: a workgroup owns 16 rows of Wg and of Wu; its
+// four wavefronts take the four quarters of d and add their fp32 partial sums
+// in wavefront order before SiLU(g) * u, so an item is I / 16 workgroups.
+// Within a quarter, blocks go in chunks of CH: every nibble word and block
+// scale of a chunk, for both matrices, is issued before its first MFMA.
+// Lane (row r = lane % 16, group g = lane / 16) holds elements 8g .. 8g + 7 of
+// each block of row r; the output lane (rows 4g .. 4g + 3, token lane % 16)
+// applies those rows' block scales to each block's exact partial sum.
+template <int CH>
 __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    __shared__ f32x4 red[3][2][64];
     int t;
     WorkItem it;
-    if (!q4_tile(L, L.I / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
+    if (!q4_tile(L, L.I / q4s::ROWS, t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8;
+    const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8, nblk = d / 32, nq = nblk / q4s::WAVES;
     const bool sh = it.slot < 0;
-    q4_stage_rows(xs, reinterpret_cast<const uint16_t *>(L.x), sh ? nullptr : L.perm, it.row0, n, d);
-    __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int i0 = ((t - it.tile0) * q4s::WAVES + wave) * q4s::ROWS;
-    const int j = lane & 15, g = lane >> 4;
+    const int i0 = (t - it.tile0) * q4s::ROWS;
+    const int r = lane & 15, g = lane >> 4;
+    const int bq = wave * nq;                          // this wavefront's first block
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mb = q4_matrix_bytes(I, d);
-    const uint16_t *xrow = xs + j * ldk + 8 * g;      // rows past n hold stale data: their outputs are not stored
+    const uint32_t *qp[2];
+    const uint16_t *sp[2];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+        const uint8_t *mat = base + m * mb;
+        qp[m] = reinterpret_cast<const uint32_t *>(mat + int64_t(i0 + r) * (d / 2)) + 4 * bq + g;
+        sp[m] = reinterpret_cast<const uint16_t *>(mat + int64_t(I) * (d / 2)) + int64_t(i0 + 4 * g) * nblk + bq;
+    }
+    uint32_t q[2][CH], sc[2][4][CH / 2];
+    auto issue = [&](int c0) {
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+#pragma unroll
+            for (int u = 0; u < CH; ++u)
+                q[m][u] = __builtin_nontemporal_load(qp[m] + 4 * (c0 + u));
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                load_scales<CH>(sc[m][rr], sp[m] + rr * nblk + c0);
+        }
+    };
+    issue(0);                                          // the first chunk goes out before the token rows
+    {
+        const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
+        const int32_t *xperm = sh ? nullptr : L.perm;
+        StageRows<4> sr;                               // one pass for d <= 2048
+        sr.load(xsrc, xperm, it.row0, n, d, 0);
+        sr.store(xs, n, d, 0);
+        sr.rest(xsrc, xperm, it.row0, n, d, xs);
+    }
+    __syncthreads();
+    const uint16_t *xrow = xs + r * ldk + 8 * g + 32 * bq;   // rows past n hold stale data: not stored
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
-    q4_rows_dot<8>(base, reinterpret_cast<const uint16_t *>(base + I * (d / 2)), i0, d, xrow, lane, ag);
-    q4_rows_dot<8>(base + mb, reinterpret_cast<const uint16_t *>(base + mb + I * (d / 2)), i0, d, xrow, lane, au);
+    for (int c0 = 0; c0 < nq; c0 += CH) {
+        if (c0 > 0)
+            issue(c0);
+#pragma unroll
+        for (int u = 0; u < CH; ++u) {
+            const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4 *>(xrow + 32 * (c0 + u)));
+            const f32x4 pg = mfma16(unpack_q4(q[0][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 pu = mfma16(unpack_q4(q[1][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                ag[rr] = fmaf(scale_at(sc[0][rr], u), pg[rr], ag[rr]);
+                au[rr] = fmaf(scale_at(sc[1][rr], u), pu[rr], au[rr]);
+            }
+        }
+    }
+    // quarters of d added in wavefront order
+    if (wave > 0) {
+        red[wave - 1][0][lane] = ag;
+        red[wave - 1][1][lane] = au;
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+        ag[rr] = ((ag[rr] + red[0][0][lane][rr]) + red[1][0][lane][rr]) + red[2][0][lane][rr];
+        au[rr] = ((au[rr] + red[0][1][lane][rr]) + red[1][1][lane][rr]) + red[2][1][lane][rr];
+    }
+    const int j = lane & 15;
     if (j < n) {
         uint2 v;
         v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
@@ -161,6 +200,10 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
     }
 }
 
+// Down, 4-bit stream path: a workgroup owns 64 output columns (16 per
+// wavefront) over all of I, in chunks of CH blocks; the first chunk's nibble
+// words and block scales are issued before the act rows are staged.
+template <int CH>
 __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t as[];
@@ -169,17 +212,48 @@ __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
     if (!q4_tile(L, L.d / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8;
+    const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8, nblk = I / 32;
     const bool sh = it.slot < 0;
-    q4_stage_rows(as, reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act), nullptr, it.row0, n, I);
-    __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c0 = ((t - it.tile0) * q4s::WAVES + wave) * q4s::ROWS;
-    const int j = lane & 15, g = lane >> 4;
+    const int r = lane & 15, g = lane >> 4;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint8_t *wd = base + 2 * q4_matrix_bytes(I, d);
+    const uint32_t *qp = reinterpret_cast<const uint32_t *>(wd + int64_t(c0 + r) * (I / 2)) + g;
+    const uint16_t *sp = reinterpret_cast<const uint16_t *>(wd + int64_t(d) * (I / 2)) + int64_t(c0 + 4 * g) * nblk;
+    uint32_t q[CH], sc[4][CH / 2];
+    auto issue = [&](int b0) {
+#pragma unroll
+        for (int u = 0; u < CH; ++u)
+            q[u] = __builtin_nontemporal_load(qp + 4 * (b0 + u));
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+            load_scales<CH>(sc[rr], sp + rr * nblk + b0);
+    };
+    issue(0);
+    {
+        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
+        StageRows<1> sr;                               // one pass for I <= 512
+        sr.load(asrc, nullptr, it.row0, n, I, 0);
+        sr.store(as, n, I, 0);
+        sr.rest(asrc, nullptr, it.row0, n, I, as);
+    }
+    __syncthreads();
+    const uint16_t *arow = as + r * ldk + 8 * g;       // rows past n hold stale data: not stored
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    q4_rows_dot<4>(wd, reinterpret_cast<const uint16_t *>(wd + d * (I / 2)), c0, I, as + j * ldk + 8 * g, lane, acc);
+    for (int b0 = 0; b0 < nblk; b0 += CH) {
+        if (b0 > 0)
+            issue(b0);
+#pragma unroll
+        for (int u = 0; u < CH; ++u) {
+            const bf16x8 ab = as_bf16x8(*reinterpret_cast<const u32x4 *>(arow + 32 * (b0 + u)));
+            const f32x4 part = mfma16(unpack_q4(q[u]), ab, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                acc[rr] = fmaf(scale_at(sc[rr], u), part[rr], acc[rr]);
+        }
+    }
+    const int j = lane & 15;
     if (j < n) {
         const int64_t row = it.row0 + j;
         const float w = sh ? 1.0f : L.row_weight[row];
@@ -192,7 +266,17 @@ hipError_t launch_gateup_q4_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    launch_k(stream_gateup_q4_kernel, L.n_tiles, 256, size_t(16) * (L.d + 8) * 2, s, L);
+    // chunk: the largest of 16, 8, 4, 2 blocks dividing a quarter of d (d % 256 == 0)
+    const int nq = L.d / 128;
+    const size_t lds = size_t(16) * (L.d + 8) * 2;
+    if (nq % 16 == 0)
+        launch_k(stream_gateup_q4_kernel<16>, L.n_tiles, 256, lds, s, L);
+    else if (nq % 8 == 0)
+        launch_k(stream_gateup_q4_kernel<8>, L.n_tiles, 256, lds, s, L);
+    else if (nq % 4 == 0)
+        launch_k(stream_gateup_q4_kernel<4>, L.n_tiles, 256, lds, s, L);
+    else
+        launch_k(stream_gateup_q4_kernel<2>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -200,7 +284,15 @@ hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    launch_k(stream_down_q4_kernel, L.n_tiles, 256, size_t(16) * (L.I + 8) * 2, s, L);
+    // chunk: the largest of 16, 8, 4 blocks dividing I / 32 (I % 128 == 0)
+    const int nblk = L.I / 32;
+    const size_t lds = size_t(16) * (L.I + 8) * 2;
+    if (nblk % 16 == 0)
+        launch_k(stream_down_q4_kernel<16>, L.n_tiles, 256, lds, s, L);
+    else if (nblk % 8 == 0)
+        launch_k(stream_down_q4_kernel<8>, L.n_tiles, 256, lds, s, L);
+    else
+        launch_k(stream_down_q4_kernel<4>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -406,9 +498,19 @@ hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s)
 
 hipError_t init_q4_attributes()
 {
-    hipError_t e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel));
+    hipError_t e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<16>));
     if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel));
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<8>));
+    if (e == hipSuccess)
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<4>));
+    if (e == hipSuccess)
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<2>));
+    if (e == hipSuccess)
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<16>));
+    if (e == hipSuccess)
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<8>));
+    if (e == hipSuccess)
+        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<4>));
     if (e == hipSuccess)
         e = allow_large_lds(reinterpret_cast<const void *>(&tile_q4_kernel<true>));
     if (e == hipSuccess)
