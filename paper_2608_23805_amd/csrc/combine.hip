@@ -13,28 +13,28 @@
 
 namespace msi {
 
-// Status handling shared by both combines.  Every workgroup reads the status
-// word.  With an arrival counter (small grids: one counter update per
-// workgroup), thread 0 of each workgroup counts itself in after its read and
-// the last to arrive (the counter wraps back to zero) clears the word, so the
-// next forward starts from a clean word without a launch of its own.
+// Status handling shared by both combines.  With an arrival counter (small
+// grids: one counter update per workgroup), thread 0 of each workgroup alone
+// reads the status word and shares it through LDS, then counts the workgroup
+// in; the ticket is checked at the end of the kernel, and the last workgroup
+// to arrive (the counter wraps back to zero) clears the word, after every
+// workgroup has read it, so the next forward starts from a clean word without
+// a launch of its own.  Without a counter every thread reads the word.
 // Workgroup 0 also publishes to pinned host words: the demanded experts
 // (count, then ids) when `demand` is given, then status | STATUS_DONE with a
 // system-scope release, so a host that sees the done bit also sees the list.
-__device__ __forceinline__ uint32_t combine_status(const CombinePublish &P)
+__device__ __forceinline__ uint32_t combine_status(const CombinePublish &P, uint32_t &ticket)
 {
     uint32_t st;
+    ticket = 0u;
     if (P.arrive) {
         __shared__ uint32_t st_s;
-        if (threadIdx.x == 0) {
-            const uint32_t v = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            st_s = v;
-            __builtin_amdgcn_s_waitcnt(0);      // the word is read before this workgroup counts itself in
-            if (atomicInc(P.arrive, gridDim.x - 1u) == gridDim.x - 1u)
-                __hip_atomic_store(P.status, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+        if (threadIdx.x == 0)
+            st_s = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
         st = st_s;
+        if (threadIdx.x == 0)
+            ticket = atomicInc(P.arrive, gridDim.x - 1u);   // issued after this workgroup's read
     } else {
         st = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -54,12 +54,21 @@ __device__ __forceinline__ uint32_t combine_status(const CombinePublish &P)
     return st;
 }
 
+__device__ __forceinline__ void combine_finish(const CombinePublish &P, uint32_t ticket)
+{
+    if (P.arrive && threadIdx.x == 0 && ticket == gridDim.x - 1u)
+        __hip_atomic_store(P.status, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // fp32 layers: y and ys in fp32, four columns per thread.
 __global__ void __launch_bounds__(256) combine_f32_kernel(const float *__restrict__ y, const float *__restrict__ ys,
                                                           const int32_t *__restrict__ inv, float *__restrict__ out,
                                                           CombinePublish P, int T, int K, int d)
 {
-    if (combine_status(P) != 0u)
+    uint32_t ticket;
+    const uint32_t st = combine_status(P, ticket);
+    combine_finish(P, ticket);
+    if (st != 0u)
         return;
     const int d4 = d / 4;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -89,47 +98,56 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 
 // bf16 y and ys, eight columns per thread; the sum is in fp32 in the same
 // fixed order (shared expert, then the K routed rows in selection order).
+// The row indices and the shared row are read together with the status word,
+// so the kernel costs two dependent memory round trips before its store.
 __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict__ y, const uint16_t *__restrict__ ys,
                                                       const int32_t *__restrict__ inv, float *__restrict__ out,
                                                       CombinePublish P, int T, int K, int d)
 {
-    if (combine_status(P) != 0u)
-        return;
     const int d8 = d / 8;
+    const int64_t n = int64_t(T) * d8;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= int64_t(T) * d8)
-        return;
-    const int t = int(i / d8), c = int(i % d8) * 8;
-    float a[8];
-    if (ys) {
-        const u32x4 s = *reinterpret_cast<const u32x4 *>(ys + int64_t(t) * d + c);
+    const bool live = i < n;
+    const int64_t ic = live ? i : 0;
+    const int t = int(ic / d8), c = int(ic % d8) * 8;
+    int32_t row[16];
+    u32x4 s = {0u, 0u, 0u, 0u};
+    if (n > 0) {                                       // T == 0: nothing to read
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K)
+                row[k] = inv[int64_t(t) * K + k];
+        if (ys)
+            s = *reinterpret_cast<const u32x4 *>(ys + int64_t(t) * d + c);
+    }
+    uint32_t ticket;
+    const uint32_t st = combine_status(P, ticket);
+    if (st == 0u && live) {
+        float a[8];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             a[2 * q] = bf16_lo(s[q]);
             a[2 * q + 1] = bf16_hi(s[q]);
         }
-    } else {
+        u32x4 v[16];
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-            a[q] = 0.f;
-    }
-    u32x4 v[16];
+        for (int k = 0; k < 16; ++k)
+            if (k < K)
+                v[k] = *reinterpret_cast<const u32x4 *>(y + int64_t(row[k]) * d + c);
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-        if (k < K)
-            v[k] = *reinterpret_cast<const u32x4 *>(y + int64_t(inv[int64_t(t) * K + k]) * d + c);
+        for (int k = 0; k < 16; ++k)
+            if (k < K) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-        if (k < K) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                a[2 * q] += bf16_lo(v[k][q]);
-                a[2 * q + 1] += bf16_hi(v[k][q]);
+                for (int q = 0; q < 4; ++q) {
+                    a[2 * q] += bf16_lo(v[k][q]);
+                    a[2 * q + 1] += bf16_hi(v[k][q]);
+                }
             }
-        }
-    float4 *o = reinterpret_cast<float4 *>(out + int64_t(t) * d + c);
-    o[0] = make_float4(a[0], a[1], a[2], a[3]);
-    o[1] = make_float4(a[4], a[5], a[6], a[7]);
+        float4 *o = reinterpret_cast<float4 *>(out + int64_t(t) * d + c);
+        o[0] = make_float4(a[0], a[1], a[2], a[3]);
+        o[1] = make_float4(a[4], a[5], a[6], a[7]);
+    }
+    combine_finish(P, ticket);
 }
 
 hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t *inv, float *out,
