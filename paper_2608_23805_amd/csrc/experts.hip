@@ -183,21 +183,57 @@ __device__ __forceinline__ bool slot_gen_ok(const WorkItem &it, uint32_t g, uint
     return false;
 }
 
+// Weight slabs.  A wavefront's 16 weight rows reach registers in whole
+// 128-byte lines: one 16-byte load per lane covers 8 rows x 128 bytes (lane l:
+// row l / 8, chunk l % 8), two loads cover a slab of 16 rows x 64 columns.
+// (Loading in the MFMA fragment layout instead, 16 rows x 64 bytes per load,
+// reads every line in two halves and streams about 15% slower.)  The slab is
+// then rearranged into fragments through the wavefront's own 2 KiB of LDS,
+// chunks XOR-swizzled by row so that both the writes and the fragment reads
+// are free of bank conflicts.
+namespace slab {
+constexpr int BYTES = 16 * 128;
+
+// element offset, from the slab's first row and column, of lane's load h (rows 8h .. 8h + 7)
+__device__ __forceinline__ int src(int lane, int h, int ld) { return (8 * h + (lane >> 3)) * ld + (lane & 7) * 8; }
+
+// LDS byte offset of the 16 bytes that load h brought to lane
+__device__ __forceinline__ int dst(int lane, int h)
+{
+    const int r = 8 * h + (lane >> 3);
+    return r * 128 + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
+}
+
+// LDS byte offset of lane's MFMA fragment (row lane % 16, elements 8 (lane / 16) ..) of K step ks (0, 1)
+__device__ __forceinline__ int frag(int lane, int ks)
+{
+    const int r = lane & 15;
+    return r * 128 + (((4 * ks + (lane >> 4)) ^ ((r >> 1) & 7)) << 4);
+}
+}  // namespace slab
+
+__device__ __forceinline__ void lds_wait()
+{
+    __builtin_amdgcn_s_waitcnt(0xC07F);          // lgkmcnt(0): this wavefront's LDS accesses done
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Gate/up, stream path: a workgroup owns 16 rows of Wg and of Wu; its four
-// wavefronts take the four quarters of d (U K steps of 32 per weight batch)
-// and their fp32 partial sums are added in wavefront order before SiLU(g) * u.
-// Both MFMA operands come straight from memory: the weights (A operand) are
-// streamed once, and the lanes of token j (B operand) read row j of the item
-// from x, which stays in the caches (every item reads rows of the same few
-// tokens); lanes past the item's rows hold zeros.  With no LDS staging
-// buffer the occupancy is set by registers alone, and no barrier separates
-// the first weight batch from the first MFMA.  Sixteen-row workgroups keep
-// the grid many times larger than the number of resident workgroups, so the
-// last partial round of the launch is short.
-template <int U>
+// wavefronts take the four quarters of d (U K steps of 32, U / 2 slabs per
+// matrix, per weight batch) and their fp32 partial sums are added in
+// wavefront order before SiLU(g) * u.  The weights (A operand) are streamed
+// once, in whole lines (weight slabs above); the lanes of token j (B operand)
+// read row j of the item straight from x, which stays in the caches (every
+// item reads rows of the same few tokens).  Sixteen-row workgroups keep the
+// grid many times larger than the number of resident workgroups, so the last
+// partial round of the launch is short.
+template <int U, int NB>
 __global__ void __launch_bounds__(256, 3) stream_gateup_kernel(ExpertLaunch L)
 {
+    constexpr int SL = U / 2;                     // slabs per matrix per batch
     __shared__ f32x4 red[3][2][64];
+    __shared__ __attribute__((aligned(16))) uint8_t tr[stream::WAVES][2 * SL * slab::BYTES];
     const int d = L.d, I = L.I;
     const StreamTile st = stream_tile(L, I / stream::ROWS);
     if (!st.valid)
@@ -213,60 +249,77 @@ __global__ void __launch_bounds__(256, 3) stream_gateup_kernel(ExpertLaunch L)
     const int kq = d / stream::WAVES;             // this wavefront's quarter of d
     const int j = lane & 15, kg = (lane >> 4) * 8;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
-    const uint16_t *gp = reinterpret_cast<const uint16_t *>(base) + int64_t(i0 + j) * d + wave * kq + kg;
-    const uint16_t *up = gp + int64_t(I) * d;
+    const uint16_t *w0 = reinterpret_cast<const uint16_t *>(base) + int64_t(i0) * d + wave * kq;
+    const uint16_t *gp0 = w0 + slab::src(lane, 0, d), *gp1 = w0 + slab::src(lane, 1, d);
+    const int64_t um = int64_t(I) * d;            // Wu follows Wg
     const bool live = j < n;
+    uint8_t *t = tr[wave];
 
     // This lane's token (the shared expert's rows are the tokens in order),
     // read before the weights are issued: memory reads complete in order, so
     // waiting for it later leaves the weight batch in flight.  Lanes past
-    // the item's rows read its last row and multiply zeros: every read is
+    // the item's rows read its last row: an MFMA output column depends only
+    // on its own B column, and those columns are never stored.  Every read is
     // unconditional, so the compiler's waits stay exact.
     const int jr = it.row0 + min(j, n - 1);
     const int64_t xrow = sh ? int64_t(jr) : int64_t(L.perm[jr]);
-    // Weight and token batches are double-buffered in registers: batch b + 1
-    // is in flight while batch b is multiplied.  (The empty asm statements
-    // keep the issue order: token index, weights, then the token rows.)
-    u32x4 wg[2][U], wu[2][U], xb[2][U];
-    asm volatile("" ::: "memory");
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        wg[0][u] = load_stream16(gp + 32 * u);
-        wu[0][u] = load_stream16(up + 32 * u);
-    }
-    asm volatile("" ::: "memory");
+    // The quarter goes in chunks of NB batches, each fully unrolled: weight
+    // and token batches are double-buffered in registers (batch b + 1 is in
+    // flight while batch b is rearranged and multiplied), and with no
+    // register live across chunks the compiler's memory waits stay exact.
+    // (The empty asm statements keep the issue order: token index, weights,
+    // token rows.)
     const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + wave * kq + kg;
+    auto load_w = [&](u32x4(&dst)[2][SL][2], int k0) {
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                dst[m][s][0] = load_stream16(gp0 + m * um + k0 + 64 * s);
+                dst[m][s][1] = load_stream16(gp1 + m * um + k0 + 64 * s);
+            }
+    };
     auto load_x = [&](u32x4(&dst)[U], int k0) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const u32x4 v = *reinterpret_cast<const u32x4 *>(xp + k0 + 32 * u);
-            dst[u] = live ? v : u32x4{0u, 0u, 0u, 0u};
-        }
+        for (int u = 0; u < U; ++u)
+            dst[u] = *reinterpret_cast<const u32x4 *>(xp + k0 + 32 * u);
     };
-    load_x(xb[0], 0);
-
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
-    const int nb = kq / (32 * U);
-    for (int b = 0; b < nb; b += 2) {
+    const int nchunk = kq / (32 * U * NB);
+    for (int c = 0; c < nchunk; ++c) {
+        const int kc = c * 32 * U * NB;
+        u32x4 w[2][2][SL][2], xb[2][U];               // [buffer][matrix][slab][load]
+        asm volatile("" ::: "memory");
+        load_w(w[0], kc);
+        asm volatile("" ::: "memory");
+        load_x(xb[0], kc);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (b + h >= nb)
-                break;
-            const int k0 = (b + h) * 32 * U;
-            if (b + h + 1 < nb) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    wg[h ^ 1][u] = load_stream16(gp + k0 + 32 * U + 32 * u);
-                    wu[h ^ 1][u] = load_stream16(up + k0 + 32 * U + 32 * u);
-                }
-                load_x(xb[h ^ 1], k0 + 32 * U);
+        for (int b = 0; b < NB; ++b) {
+            if (b + 1 < NB) {
+                load_w(w[(b + 1) & 1], kc + (b + 1) * 32 * U);
+                load_x(xb[(b + 1) & 1], kc + (b + 1) * 32 * U);
             }
+            // rearrange batch b into fragments
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int s = 0; s < SL; ++s)
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+                        *reinterpret_cast<u32x4 *>(t + (m * SL + s) * slab::BYTES + slab::dst(lane, q)) =
+                            w[b & 1][m][s][q];
+            lds_wait();
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const bf16x8 bx = as_bf16x8(xb[h][u]);
-                ag = mfma16(as_bf16x8(wg[h][u]), bx, ag);
-                au = mfma16(as_bf16x8(wu[h][u]), bx, au);
+                const bf16x8 bx = as_bf16x8(xb[b & 1][u]);
+                const u32x4 fg =
+                    *reinterpret_cast<const u32x4 *>(t + (u >> 1) * slab::BYTES + slab::frag(lane, u & 1));
+                const u32x4 fu =
+                    *reinterpret_cast<const u32x4 *>(t + (SL + (u >> 1)) * slab::BYTES + slab::frag(lane, u & 1));
+                ag = mfma16(as_bf16x8(fg), bx, ag);
+                au = mfma16(as_bf16x8(fu), bx, au);
             }
+            lds_wait();                               // the next batch overwrites this wavefront's slabs
         }
     }
     // quarters of d added in wavefront order
@@ -296,12 +349,17 @@ __global__ void __launch_bounds__(256, 3) stream_gateup_kernel(ExpertLaunch L)
 }
 
 // Down, stream path: a workgroup owns 64 output columns (16 per wavefront)
-// over all of I; the expert's act rows (the B operand, shared by the four
-// wavefronts) are staged once in LDS.
-template <int U>
-__global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
+// over all of I, in chunks of NB batches of 4 K steps (2 slabs of Wd rows,
+// loaded in whole lines and rearranged through the wavefront's LDS as in the
+// gate/up kernel), each chunk fully unrolled.  The expert's act rows (the B
+// operand, shared by the four wavefronts) are staged once in LDS; the first
+// two weight batches are issued before them.
+template <int NB>
+__global__ void __launch_bounds__(256, 4) stream_down_kernel(ExpertLaunch L)
 {
+    constexpr int U = 4, SL = U / 2;
     extern __shared__ __attribute__((aligned(16))) uint16_t as[];   // [16][I + 8]
+    __shared__ __attribute__((aligned(16))) uint8_t tr[stream::WAVES][SL * slab::BYTES];
     const int d = L.d, I = L.I, ldk = I + 8;
     const StreamTile st = stream_tile(L, d / (stream::WAVES * stream::ROWS));
     if (!st.valid)
@@ -310,49 +368,75 @@ __global__ void __launch_bounds__(256, 2) stream_down_kernel(ExpertLaunch L)
     const int n = it.nrows;
     const bool sh = it.slot < 0;
     const uint32_t gnow = slot_gen_now(it, L.gen_dev);
-    // the expert's act rows are contiguous
-    const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
-    StageRows<1> sr;                              // one pass for I <= 512
-    sr.load(asrc, nullptr, it.row0, n, I, 0);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int c0 = (st.local * stream::WAVES + wave) * stream::ROWS;
     const int j = lane & 15, kg = (lane >> 4) * 8;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
-    const uint16_t *wp = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0 + j) * I + kg;
-    const uint16_t *ar = as + j * ldk + kg;
+    const uint16_t *w0 = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0) * I;
+    const uint16_t *gp0 = w0 + slab::src(lane, 0, I), *gp1 = w0 + slab::src(lane, 1, I);
     const bool live = j < n;
-
-    // the first weight batch is issued before the act rows are written to LDS
-    u32x4 w[U];
+    uint8_t *t = tr[wave];
+    auto load_w = [&](u32x4(&dst)[SL][2], int k0) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-        w[u] = load_stream16(wp + 32 * u);
-    sr.store(as, n, I, 0);
-    sr.rest(asrc, nullptr, it.row0, n, I, as);
+        for (int s = 0; s < SL; ++s) {
+            dst[s][0] = load_stream16(gp0 + k0 + 64 * s);
+            dst[s][1] = load_stream16(gp1 + k0 + 64 * s);
+        }
+    };
+    u32x4 w[2][SL][2];
+    asm volatile("" ::: "memory");
+    load_w(w[0], 0);
+    if (NB > 1)
+        load_w(w[1], 32 * U);
+    asm volatile("" ::: "memory");
+    // the expert's act rows are contiguous
+    {
+        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
+        StageRows<1> sr;                              // one pass for I <= 512
+        sr.load(asrc, nullptr, it.row0, n, I, 0);
+        sr.store(as, n, I, 0);
+        sr.rest(asrc, nullptr, it.row0, n, I, as);
+    }
     __syncthreads();
+    const uint16_t *ar = as + j * ldk + kg;          // rows past n hold stale data: their outputs are not stored
 
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < I; k0 += 32 * U) {
-        if (k0 > 0) {
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                w[u] = load_stream16(wp + k0 + 32 * u);
+    const int nchunk = I / (32 * U * NB);
+    for (int c = 0; c < nchunk; ++c) {
+        const int kc = c * 32 * U * NB;
+        if (c > 0) {
+            load_w(w[0], kc);
+            if (NB > 1)
+                load_w(w[1], kc + 32 * U);
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint4 av = live ? *reinterpret_cast<const uint4 *>(ar + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
-            acc = mfma16(as_bf16x8(w[u]), as_bf16x8(av), acc);
+        for (int b = 0; b < NB; ++b) {
+            if (b >= 1 && b + 1 < NB)                 // batches 0 and 1 went out with the chunk
+                load_w(w[(b + 1) & 1], kc + (b + 1) * 32 * U);
+#pragma unroll
+            for (int s = 0; s < SL; ++s)
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    *reinterpret_cast<u32x4 *>(t + s * slab::BYTES + slab::dst(lane, q)) = w[b & 1][s][q];
+            lds_wait();
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const u32x4 fw = *reinterpret_cast<const u32x4 *>(t + (u >> 1) * slab::BYTES + slab::frag(lane, u & 1));
+                const uint4 av = *reinterpret_cast<const uint4 *>(ar + kc + b * 32 * U + 32 * u);
+                acc = mfma16(as_bf16x8(fw), as_bf16x8(av), acc);
+            }
+            lds_wait();                               // the next batch overwrites this wavefront's slabs
         }
     }
     if (!slot_gen_ok(it, gnow, L.status))
         return;
     if (live) {
         const int64_t row = it.row0 + j;
-        const float w = sh ? 1.0f : L.row_weight[row];
+        const float wt = sh ? 1.0f : L.row_weight[row];
         *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * (lane >> 4)) =
-            make_uint2(pack_bf16x2(acc[0] * w, acc[1] * w), pack_bf16x2(acc[2] * w, acc[3] * w));
+            make_uint2(pack_bf16x2(acc[0] * wt, acc[1] * wt), pack_bf16x2(acc[2] * wt, acc[3] * wt));
     }
 }
 
@@ -360,11 +444,16 @@ hipError_t launch_gateup_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    // U K steps of 32 per batch must divide the quarter d / 4 (d % 256 == 0)
-    if (L.d % 512 == 0)
-        launch_k(stream_gateup_kernel<4>, L.n_tiles, 256, 0, s, L);
+    // chunks of NB batches of U K steps of 32 must divide the quarter d / 4 (d % 256 == 0)
+    const int kq = L.d / 4;
+    if (kq % 512 == 0)
+        launch_k(stream_gateup_kernel<4, 4>, L.n_tiles, 256, 0, s, L);
+    else if (kq % 256 == 0)
+        launch_k(stream_gateup_kernel<4, 2>, L.n_tiles, 256, 0, s, L);
+    else if (kq % 128 == 0)
+        launch_k(stream_gateup_kernel<4, 1>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_gateup_kernel<2>, L.n_tiles, 256, 0, s, L);
+        launch_k(stream_gateup_kernel<2, 1>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -372,11 +461,14 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
+    // chunks of NB batches of 128 columns must divide I (I % 128 == 0)
     const size_t lds = size_t(stream::MAXN) * (L.I + 8) * sizeof(uint16_t);
     if (L.I % 512 == 0)
-        launch_k(stream_down_kernel<16>, L.n_tiles, 256, lds, s, L);
-    else
         launch_k(stream_down_kernel<4>, L.n_tiles, 256, lds, s, L);
+    else if (L.I % 256 == 0)
+        launch_k(stream_down_kernel<2>, L.n_tiles, 256, lds, s, L);
+    else
+        launch_k(stream_down_kernel<1>, L.n_tiles, 256, lds, s, L);
     return hipGetLastError();
 }
 
@@ -480,8 +572,9 @@ hipError_t init_kernel_attributes()
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Down>));
-    set(reinterpret_cast<const void *>(&stream_down_kernel<16>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
+    set(reinterpret_cast<const void *>(&stream_down_kernel<2>));
+    set(reinterpret_cast<const void *>(&stream_down_kernel<1>));
     if (e == hipSuccess)
         e = init_route_attributes();
     if (e == hipSuccess)
