@@ -181,7 +181,9 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                ms_per_step=round(ms, 3),
                T=s.T, layer_tflops=round(layer_flops / (ms * 1e-3) / 1e12, 1),
                layer_mfma_frac=round(layer_flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-               roofline={"bound": "mfma", "kernel": "tile_gemm_kernel<GateUp>", "achieved": round(achieved, 1),
+               roofline={"bound": "mfma",
+                         "kernel": "q4_tile_kernel<GateUp>" if s.wdtype == "q4b32" else "ring_gemm_kernel<GateUp>",
+                         "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
                          "flops_per_launch": flops_gu, "avg_launch_us": round(avg_gu * 1e3, 1),

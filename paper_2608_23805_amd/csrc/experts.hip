@@ -1,7 +1,8 @@
 // experts.hip -- per-expert gate/up (SiLU-gated) and down projections for
 // gfx950, three variants chosen per expert from its routed-token count only:
 //
-//  * tile path (bf16, > STREAM tokens): LDS-staged MFMA tiles of gemm_tile.h.
+//  * tile path (bf16, > STREAM tokens): 256 x 256 MFMA tiles fed by a ring of
+//    LDS stages that buffer loads fill directly (gemm_ring.h).
 //  * stream path (bf16, <= 16 tokens): weight streaming.  The weights are the
 //    MFMA A operand read straight from HBM in the 16x16x32 fragment layout
 //    (each wavefront owns 16 weight rows; each weight byte is read once), the
@@ -13,6 +14,7 @@
 // y[row, d] = row_weight * (act Wd^T), rows in permuted order, both rounded
 // to bf16 once (fp32 throughout for fp32 layers).
 #include "common.h"
+#include "gemm_ring.h"
 #include "gemm_tile.h"
 #include "kernels.h"
 
@@ -20,59 +22,23 @@ namespace msi {
 
 // ============================================================== tile path
 
-static TileArgs tile_args(const ExpertLaunch &L, bool gateup)
-{
-    TileArgs p{};
-    if (gateup) {
-        p.a = reinterpret_cast<const uint16_t *>(L.x);
-        p.lda = L.d;
-        p.perm = L.perm;
-        p.K = L.d;
-        p.n_tiles_n = L.I / 128;
-        p.out = L.act;
-        p.ldo = L.I;
-    } else {
-        p.a = reinterpret_cast<const uint16_t *>(L.act);
-        p.lda = L.I;
-        p.perm = nullptr;
-        p.K = L.I;
-        p.n_tiles_n = L.d / tile::BN;
-        p.out = L.y;
-        p.ldo = L.d;
-        p.row_weight = L.row_weight;
-    }
-    p.wbase = L.wbase;
-    p.wstride = L.wstride;
-    p.shared_w = L.shared_w;
-    p.a_s = reinterpret_cast<const uint16_t *>(L.act_s);
-    p.out_s = gateup ? L.act_s : L.ys;
-    p.n_valid = 1 << 30;
-    p.d = L.d;
-    p.I = L.I;
-    p.items = L.items;
-    p.n_items = L.n_items;
-    p.gen_dev = L.gen_dev;
-    p.status = L.status;
-    return p;
-}
-
 int tiles_gateup_tile(int nrows, int d, int I)
 {
     (void)d;
-    return ((nrows + tile::BM - 1) / tile::BM) * (I / 128);
+    return ring_tiles_gateup(nrows, I);
 }
 
 int tiles_down_tile(int nrows, int d, int I)
 {
     (void)I;
-    return ((nrows + tile::BM - 1) / tile::BM) * (d / tile::BN);
+    return ring_tiles_down(nrows, d);
 }
 
 hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    launch_k(tile_gemm_kernel<TileMode::GateUp>, L.n_tiles, tile::THREADS, tile::LDS_BYTES, s, tile_args(L, true));
+    launch_k(ring_gemm_kernel<RingMode::GateUp>, L.n_tiles, ring::THREADS, 0, s, L);
     return hipGetLastError();
 }
 
@@ -80,7 +46,7 @@ hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    launch_k(tile_gemm_kernel<TileMode::Down>, L.n_tiles, tile::THREADS, tile::LDS_BYTES, s, tile_args(L, false));
+    launch_k(ring_gemm_kernel<RingMode::Down>, L.n_tiles, ring::THREADS, 0, s, L);
     return hipGetLastError();
 }
 
@@ -570,8 +536,6 @@ hipError_t init_kernel_attributes()
             e = allow_large_lds(f);
     };
     set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
-    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::GateUp>));
-    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Down>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<2>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<1>));
