@@ -182,7 +182,7 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                T=s.T, layer_tflops=round(layer_flops / (ms * 1e-3) / 1e12, 1),
                layer_mfma_frac=round(layer_flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
                roofline={"bound": "mfma",
-                         "kernel": "q4_tile_kernel<GateUp>" if s.wdtype == "q4b32" else "ring_gemm_kernel<GateUp>",
+                         "kernel": "tile_q4_kernel<GateUp>" if s.wdtype == "q4b32" else "ring_gemm_kernel<GateUp>",
                          "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,

@@ -1,8 +1,7 @@
 // experts.hip -- per-expert gate/up (SiLU-gated) and down projections for
 // gfx950, three variants chosen per expert from its routed-token count only:
 //
-//  * tile path (bf16, > STREAM tokens): 256 x 256 MFMA tiles fed by a ring of
-//    LDS stages that buffer loads fill directly (gemm_ring.h).
+//  * tile path (bf16, > STREAM tokens): tiles.hip.
 //  * stream path (bf16, <= 16 tokens): weight streaming.  The weights are the
 //    MFMA A operand read straight from HBM in the 16x16x32 fragment layout
 //    (each wavefront owns 16 weight rows; each weight byte is read once), the
@@ -14,69 +13,9 @@
 // y[row, d] = row_weight * (act Wd^T), rows in permuted order, both rounded
 // to bf16 once (fp32 throughout for fp32 layers).
 #include "common.h"
-#include "gemm_ring.h"
-#include "gemm_tile.h"
 #include "kernels.h"
 
 namespace msi {
-
-// ============================================================== tile path
-
-int tiles_gateup_tile(int nrows, int d, int I)
-{
-    (void)d;
-    return ring_tiles_gateup(nrows, I);
-}
-
-int tiles_down_tile(int nrows, int d, int I)
-{
-    (void)I;
-    return ring_tiles_down(nrows, d);
-}
-
-hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
-{
-    if (L.n_tiles == 0)
-        return hipSuccess;
-    launch_k(ring_gemm_kernel<RingMode::GateUp>, L.n_tiles, ring::THREADS, 0, s, L);
-    return hipGetLastError();
-}
-
-hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
-{
-    if (L.n_tiles == 0)
-        return hipSuccess;
-    launch_k(ring_gemm_kernel<RingMode::Down>, L.n_tiles, ring::THREADS, 0, s, L);
-    return hipGetLastError();
-}
-
-hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, const float *bias, float *L, int T,
-                                     int d, int E, hipStream_t s)
-{
-    if (T == 0)
-        return hipSuccess;
-    TileArgs p{};
-    p.a = x;
-    p.lda = d;
-    p.perm = nullptr;
-    p.wbase = reinterpret_cast<const uint8_t *>(wr);
-    p.wstride = 0;
-    p.K = d;
-    p.n_valid = E;
-    p.n_tiles_n = (E + tile::BN - 1) / tile::BN;
-    p.d = d;
-    p.items = nullptr;
-    p.n_items = 1;
-    p.single = WorkItem{-1, -1, 0u, 0, T, 0};
-    p.gen_dev = nullptr;
-    p.status = nullptr;
-    p.out = L;
-    p.ldo = E;
-    p.bias = bias;
-    const int tiles = ((T + tile::BM - 1) / tile::BM) * p.n_tiles_n;
-    launch_k(tile_gemm_kernel<TileMode::Router>, tiles, tile::THREADS, tile::LDS_BYTES, s, p);
-    return hipGetLastError();
-}
 
 // ============================================================== stream path
 
@@ -535,10 +474,11 @@ hipError_t init_kernel_attributes()
         if (e == hipSuccess)
             e = allow_large_lds(f);
     };
-    set(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<4>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<2>));
     set(reinterpret_cast<const void *>(&stream_down_kernel<1>));
+    if (e == hipSuccess)
+        e = init_tile_attributes();
     if (e == hipSuccess)
         e = init_route_attributes();
     if (e == hipSuccess)

@@ -74,6 +74,7 @@ struct RouteOut {
 hipError_t launch_route_select(const float *L, const RouteOut &o, int32_t *blockhist, int T, int K, int E,
                                hipStream_t s);
 hipError_t init_route_attributes();
+hipError_t init_tile_attributes();
 // decode routing for 1 <= T <= 16 tokens (bf16) in one launch: logits plus
 // bias to L, then, in the last workgroup to finish, top-K, softmax and
 // permutation.  `arrive` is a zero device word that the launch leaves zero;
