@@ -24,8 +24,8 @@
 // stage s+1 are read while stage s is multiplied (weight fragments double
 // buffered, each row fragment right after its last use), two reads per eight
 // MFMAs.  The loop has no branches: stages past the end are loaded through a
-// buffer resource with no records (the loads return zeros and touch no
-// memory), so every step waits on the same counts.  Row blocks past the
+// buffer resource with no records (the loads touch no memory and write
+// zeros to their LDS destination), so every step waits on the same counts.  Row blocks past the
 // tile's valid rows are loaded the same way, and a wavefront whose 64 rows
 // are all past the end keeps its share of the copies and the barriers but
 // skips the MFMAs.
@@ -83,6 +83,68 @@ __device__ __forceinline__ float silu_hw(float z)
     return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
 }
 
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_hw_t;
+
+// two fp32 values -> packed bf16 pair, rounded to nearest even by the gfx950
+// conversion instruction (identical to f32_to_bf16 for every non-NaN input)
+__device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi)
+{
+    const bf16x2_hw_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// Tile epilogue: lane holds row 16 q + lane % 16 of the wavefront's 64 rows and
+// features 16 a + 4 (lane / 16) + j of its 128 weight rows.  Gate/up stores
+// act = silu(gate) * up; down stores y = row_weight * acc; bf16, 8 bytes per
+// lane and block.  Addresses: a uniform tile base plus 32-bit lane offsets.
+template <RingMode MODE>
+__device__ __forceinline__ void ring_store(const ExpertLaunch &L, const f32x4 (&acc)[8][4], int64_t rowbase, int nt,
+                                           int valid, bool sh, int wm, int wn, int lane_in)
+{
+    // (the lane index is made opaque so the store offsets are computed here, not kept live across the K loop)
+    int lane = lane_in;
+    asm volatile("" : "+v"(lane));
+    if constexpr (MODE == RingMode::GateUp) {
+        const int I = L.I;
+        uint8_t *base = reinterpret_cast<uint8_t *>(static_cast<uint16_t *>(sh ? L.act_s : L.act) + rowbase * I +
+                                                    nt * 128 + wn * 64);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int row = wm * 64 + q * 16 + (lane & 15);
+            if (row < valid) {
+                const uint32_t off = uint32_t(row * I + 4 * (lane >> 4)) * 2u;
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+                    uint2 v;
+                    v.x = pack_bf16x2_hw(silu_hw(acc[a][q][0]) * acc[a + 4][q][0], silu_hw(acc[a][q][1]) * acc[a + 4][q][1]);
+                    v.y = pack_bf16x2_hw(silu_hw(acc[a][q][2]) * acc[a + 4][q][2], silu_hw(acc[a][q][3]) * acc[a + 4][q][3]);
+                    *reinterpret_cast<uint2 *>(base + (off + uint32_t(a * 32))) = v;
+                }
+            }
+        }
+    } else {
+        const int d = L.d;
+        uint8_t *base = reinterpret_cast<uint8_t *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + rowbase * d +
+                                                    nt * ring::TN + wn * 128);
+        const float *rw = (sh || !L.row_weight) ? nullptr : L.row_weight + rowbase;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int row = wm * 64 + q * 16 + (lane & 15);
+            if (row < valid) {
+                const float wgt = rw ? rw[row] : 1.0f;
+                const uint32_t off = uint32_t(row * d + 4 * (lane >> 4)) * 2u;
+#pragma unroll
+                for (int a = 0; a < 8; ++a) {
+                    uint2 v;
+                    v.x = pack_bf16x2_hw(acc[a][q][0] * wgt, acc[a][q][1] * wgt);
+                    v.y = pack_bf16x2_hw(acc[a][q][2] * wgt, acc[a][q][3] * wgt);
+                    *reinterpret_cast<uint2 *>(base + (off + uint32_t(a * 32))) = v;
+                }
+            }
+        }
+    }
+}
+
 inline int ring_tiles_gateup(int nrows, int I) { return ((nrows + ring::TM - 1) / ring::TM) * (I / 128); }
 inline int ring_tiles_down(int nrows, int d) { return ((nrows + ring::TM - 1) / ring::TM) * (d / ring::TN); }
 
@@ -106,7 +168,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
     const int valid = min(TM, it.nrows - m0);
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);   // (uniform: scalar selects, no waterfall loops)
 
     // ---- copy addressing: instruction i of this wavefront covers stage rows
     // 16 (i WAVES + wave) + lane / 4; lane % 4 is the 16-byte slot it fills
@@ -229,41 +291,295 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
         step(s + 1, std::integral_constant<int, 1>{});
     }
 
-    // ---- epilogue: lane holds row 16 b + lane % 16, features 16 a + 4 (lane / 16) + j
-    const int64_t rowbase = int64_t(it.row0) + m0;
-    if constexpr (GU) {
-        uint16_t *out = static_cast<uint16_t *>(sh ? L.act_s : L.act);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int row = wm * 64 + b * 16 + (lane & 15);
-            if (row < valid) {
-                uint16_t *dst = out + (rowbase + row) * I + nt * 128 + wn * 64 + 4 * (lane >> 4);
-#pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    uint2 v;
-                    v.x = pack_bf16x2(silu_hw(acc[a][b][0]) * acc[a + 4][b][0], silu_hw(acc[a][b][1]) * acc[a + 4][b][1]);
-                    v.y = pack_bf16x2(silu_hw(acc[a][b][2]) * acc[a + 4][b][2], silu_hw(acc[a][b][3]) * acc[a + 4][b][3]);
-                    *reinterpret_cast<uint2 *>(dst + a * 16) = v;
-                }
-            }
-        }
+    ring_store<MODE>(L, acc, int64_t(it.row0) + m0, nt, valid, sh, wm, wn, lane);
+}
+
+
+// ---------------------------------------------------------------- persistent form
+//
+// One workgroup per CU walks a sequence of tiles: XCD x (workgroup b runs on
+// XCD b % 8) owns the contiguous tile range [x per, (x + 1) per) and its
+// workgroups interleave over it, so the tiles that share rows and weights run
+// together in one L2.  The stage stream runs on across tiles: the last three
+// steps of a tile already copy the first three stages of the next one, so the
+// pipeline never drains and the epilogue's stores overlap the next tile's
+// copies.  The next tile's item is found after each epilogue by walking
+// forward from the current item (scalar loads); for gate/up its 256 gather
+// indices reach LDS through one extra copy per wavefront per step (zero
+// records, into a spare LDS area, except at step 2, so every step still waits
+// on the same count) and
+// are turned into copy offsets at step nstage - 4.  Requires K / 32 >= 8.
+
+struct RingTile {
+    int ii;             // item index
+    int row0, m0, nt, valid, slot;
+    uint32_t gen;
+    bool sh;
+    const uint8_t *bbase;
+};
+
+template <RingMode MODE>
+__device__ __forceinline__ RingTile ring_tile_at(const ExpertLaunch &L, int t, int ii)
+{
+    while (ii + 1 < L.n_items && L.items[ii + 1].tile0 <= t)   // items are sorted by tile0
+        ++ii;
+    const WorkItem w = L.items[ii];
+    constexpr bool GU = MODE == RingMode::GateUp;
+    const int ntn = GU ? L.I / 128 : L.d / ring::TN;
+    RingTile r;
+    r.ii = ii;
+    const int local = t - w.tile0;
+    r.row0 = w.row0;
+    r.m0 = (local / ntn) * ring::TM;
+    r.nt = local % ntn;
+    r.valid = min(ring::TM, w.nrows - r.m0);
+    r.slot = w.slot;
+    r.gen = w.gen;
+    r.sh = w.slot < 0;
+    const uint8_t *wobj = r.sh ? L.shared_w : L.wbase + uint64_t(w.slot) * L.wstride;
+    r.bbase = GU ? wobj + uint64_t(r.nt) * 128 * L.d * 2
+                 : wobj + (uint64_t(2) * L.I * L.d + uint64_t(r.nt) * ring::TN * L.I) * 2;
+    return r;
+}
+
+template <RingMode MODE>
+__global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertLaunch L)
+{
+    using namespace ring;
+    constexpr bool GU = MODE == RingMode::GateUp;
+    constexpr int XP = GU ? 1 : 0;                          // extra copies per wavefront per step
+    constexpr int LP = LPS + XP;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * STAGE];
+    // next tile's gather indices; the second half takes the extra copies that carry nothing (a copy through a
+    // zero-record resource still writes its zeros to LDS)
+    __shared__ __attribute__((aligned(256))) int32_t permlds[2 * WAVES * 64];
+
+    const int d = L.d, I = L.I;
+    const int K = GU ? d : I;
+    const int nstage = K / SK;
+    const int n = L.n_tiles;
+    const int nwg = int(gridDim.x), b = int(blockIdx.x);
+    int t, tend, tstep;
+    if (nwg % 8 == 0) {
+        const int per = (n + 7) / 8, x = b % 8;
+        t = x * per + b / 8;
+        tend = min(n, (x + 1) * per);
+        tstep = nwg / 8;
     } else {
-        uint16_t *out = static_cast<uint16_t *>(sh ? L.ys : L.y);
+        t = b;
+        tend = n;
+        tstep = nwg;
+    }
+    if (t >= tend)
+        return;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);   // (uniform: scalar selects, no waterfall loops)
+    const int wm = wave >> 1, wn = wave & 1;
+    const int rl = lane >> 2;
+    const uint32_t cw = uint32_t(((lane & 3) ^ ((rl >> 2) & 3)) << 4);
+    uint32_t boff[LB];   // B rows of this lane's copies, relative to the tile's weight base
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int row = wm * 64 + b * 16 + (lane & 15);
-            if (row < valid) {
-                const float wgt = (sh || !L.row_weight) ? 1.0f : L.row_weight[rowbase + row];
-                uint16_t *dst = out + (rowbase + row) * d + nt * TN + wn * 128 + 4 * (lane >> 4);
+    for (int i = 0; i < LB; ++i) {
+        const int r = (i * WAVES + wave) * 16 + rl;
+        const int src = GU ? (r < 128 ? r : I + (r - 128)) : r;
+        boff[i] = uint32_t(src) * uint32_t(K * 2) + cw;
+    }
+    const __amdgpu_buffer_rsrc_t none = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(L.x), 0, 0, RSRC_FLAGS);
+    const uint32_t fofs = uint32_t((lane & 15) * ROWB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4));
+    auto wrow = [&](int a) { return GU ? (a < 4 ? wn * 64 + a * 16 : 128 + wn * 64 + (a - 4) * 16) : wn * 128 + a * 16; };
+    auto sync_stage = [&](auto waitn) {
+        __builtin_amdgcn_s_waitcnt(VMCNT_WAIT(decltype(waitn)::value));
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    // row index within the tile of this lane's copy i (rows past the end read the tile's first row); the
+    // lane index is made opaque so this is recomputed where used rather than kept live across the K loop
+    auto arow = [&](const RingTile &T, int i) {
+        int l = lane;
+        asm volatile("" : "+v"(l));
+        const int r = (i * WAVES + wave) * 16 + (l >> 2);
+        return r < T.valid ? r : 0;
+    };
+    // stage copies: tile T's stage st into ring buffer B; !real (or past the tile's rows): zero-record loads
+    auto issue = [&](const RingTile &T, const uint32_t (&ao)[LA], auto bufc, int st, bool real) {
+        constexpr int B = decltype(bufc)::value;
+        const void *abase = GU ? L.x : (T.sh ? L.act_s : L.act);
+        const __amdgpu_buffer_rsrc_t ar =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(abase), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
+        const __amdgpu_buffer_rsrc_t br =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(T.bbase), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
+        uint8_t *buf = lds + B * STAGE;
+        const int kb = st * ROWB;
 #pragma unroll
-                for (int a = 0; a < 8; ++a) {
-                    uint2 v;
-                    v.x = pack_bf16x2(acc[a][b][0] * wgt, acc[a][b][1] * wgt);
-                    v.y = pack_bf16x2(acc[a][b][2] * wgt, acc[a][b][3] * wgt);
-                    *reinterpret_cast<uint2 *>(dst + a * 16) = v;
-                }
+        for (int i = 0; i < LA; ++i)
+            dma16_lds(((i * WAVES + wave) * 16 < T.valid) ? ar : none, buf + (i * WAVES + wave) * 1024, ao[i], kb);
+#pragma unroll
+        for (int i = 0; i < LB; ++i)
+            dma16_lds(br, buf + TM * ROWB + (i * WAVES + wave) * 1024, boff[i], kb);
+    };
+    // the extra copy: at step 2 wavefront w brings the next tile's gather indices of rows 32 w .. 32 w + 31
+    // (lanes 32..63 repeat them) into permlds[64 w ..]; zero records otherwise
+    auto extra = [&](const RingTile &N, bool real) {
+        if constexpr (GU) {
+            const __amdgpu_buffer_rsrc_t pr =
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(L.perm), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
+            int l = lane;
+            asm volatile("" : "+v"(l));
+            const int r = 32 * wave + (l & 31);
+            const uint32_t off = uint32_t(N.row0 + N.m0 + (r < N.valid ? r : 0)) * 4u;
+#if defined(__HIP_DEVICE_COMPILE__)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(pr, (lds_void_t *)(permlds + (real ? 0 : WAVES * 64) + 64 * wave), 4,
+                                                     off, 0, 0, 0);
+#else
+            (void)pr, (void)off;
+#endif
+        }
+    };
+    auto a_offsets = [&](const RingTile &T, uint32_t (&ao)[LA], bool from_lds) {
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            const int r = arow(T, i);
+            uint32_t src;
+            if (GU)
+                src = T.sh ? uint32_t(T.m0 + r) : (from_lds ? uint32_t(permlds[64 * (r >> 5) + (r & 31)])
+                                                            : uint32_t(L.perm[T.row0 + T.m0 + r]));
+            else
+                src = uint32_t(T.row0 + T.m0 + r);
+            ao[i] = src * uint32_t(K * 2) + cw;
+        }
+    };
+    using W_STEADY = std::integral_constant<int, LP * (NBUF - 3)>;   // stage s+1 landed, s+2 in flight
+
+    // ---- first tile (blocking)
+    RingTile cur = ring_tile_at<MODE>(L, t, find_item(L.items, L.n_items, t));
+    bool cur_ok = cur.sh || L.gen_dev[cur.slot] == cur.gen;
+    uint32_t aoff[LA];
+    a_offsets(cur, aoff, false);
+    issue(cur, aoff, std::integral_constant<int, 0>{}, 0, true);
+    extra(cur, false);
+    issue(cur, aoff, std::integral_constant<int, 1>{}, 1, true);
+    extra(cur, false);
+    issue(cur, aoff, std::integral_constant<int, 2>{}, 2, true);
+    extra(cur, false);
+    sync_stage(std::integral_constant<int, LP * (NBUF - 2)>{});
+
+    u32x4 fw[8], fx[2][4];
+    f32x4 acc[8][4];
+    auto load_frags0 = [&]() {
+        const uint8_t *b0 = lds + fofs;
+#pragma unroll
+        for (int a = 0; a < 8; ++a)
+            fw[a] = *reinterpret_cast<const u32x4 *>(b0 + TM * ROWB + wrow(a) * ROWB);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            fx[0][q] = *reinterpret_cast<const u32x4 *>(b0 + (wm * 64 + q * 16) * ROWB);
+    };
+    // MFMAs of step s (fragments in fw / fx[H]), weight block by weight block; with PREF the fragments of
+    // stage s+1 are read in between: each weight fragment right after its last use, the row fragments into
+    // the other buffer
+    auto mma = [&](auto sbc, auto pref) {
+        constexpr int SB = decltype(sbc)::value;          // step index mod 4 (K / 32 is a multiple of 4)
+        constexpr int H = SB & 1;
+        constexpr bool PREF = decltype(pref)::value;
+        const uint8_t *nb = lds + ((SB + 1) % NBUF) * STAGE + fofs;
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[a][q] =
+                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fw[a]), as_bf16x8(fx[H][q]), acc[a][q], 0, 0, 0);
+            if (PREF) {
+                fw[a] = *reinterpret_cast<const u32x4 *>(nb + TM * ROWB + wrow(a) * ROWB);
+                if (a & 1)
+                    fx[H ^ 1][a >> 1] = *reinterpret_cast<const u32x4 *>(nb + (wm * 64 + (a >> 1) * 16) * ROWB);
             }
         }
+        if (PREF) {
+            // per weight block: four MFMAs, then its read (and every second block a row fragment read)
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+        }
+    };
+    using PF = std::true_type;
+    using NP = std::false_type;
+
+    load_frags0();
+    for (;;) {
+#pragma unroll
+        for (int a = 0; a < 8; ++a)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[a][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // the next tile's item (scalar loads; first used by step 2's extra copy)
+        const int tn = t + tstep;
+        const bool has_next = tn < tend;
+        const RingTile nxt = has_next ? ring_tile_at<MODE>(L, tn, cur.ii) : cur;
+        const bool nxt_ok = nxt.sh || !has_next || L.gen_dev[nxt.slot] == nxt.gen;
+
+        using S0 = std::integral_constant<int, 0>;
+        using S1 = std::integral_constant<int, 1>;
+        using S2 = std::integral_constant<int, 2>;
+        using S3 = std::integral_constant<int, 3>;
+        // steps 0 .. nstage-5 (four per pass): copies of this tile's stages 3 .. nstage-2
+        for (int s = 0; s < nstage - 4; s += 4) {
+            sync_stage(W_STEADY{});
+            issue(cur, aoff, S3{}, s + 3, true);
+            extra(nxt, false);
+            mma(S0{}, PF{});
+            sync_stage(W_STEADY{});
+            issue(cur, aoff, S0{}, s + 4, true);
+            extra(nxt, false);
+            mma(S1{}, PF{});
+            sync_stage(W_STEADY{});
+            issue(cur, aoff, S1{}, s + 5, true);
+            extra(nxt, has_next && s == 0);
+            mma(S2{}, PF{});
+            sync_stage(W_STEADY{});
+            issue(cur, aoff, S2{}, s + 6, true);
+            extra(nxt, false);
+            mma(S3{}, PF{});
+        }
+        // steps nstage-4 .. nstage-1: the last stage of this tile, then the next tile's stages 0 .. 2
+        uint32_t naoff[LA];
+        sync_stage(W_STEADY{});
+        a_offsets(nxt, naoff, true);                // (the indices landed by step 4's barrier)
+        issue(cur, aoff, S3{}, nstage - 1, true);
+        extra(nxt, false);
+        mma(S0{}, PF{});
+        sync_stage(W_STEADY{});
+        issue(nxt, naoff, S0{}, 0, has_next);
+        extra(nxt, false);
+        mma(S1{}, PF{});
+        sync_stage(W_STEADY{});
+        issue(nxt, naoff, S1{}, 1, has_next);
+        extra(nxt, false);
+        mma(S2{}, PF{});
+        sync_stage(W_STEADY{});
+        issue(nxt, naoff, S2{}, 2, has_next);
+        extra(nxt, false);
+        mma(S3{}, NP{});
+
+        // ---- epilogue of this tile (the next tile's first stages are in flight)
+        if (!cur_ok) {
+            if (threadIdx.x == 0)
+                atomicOr(L.status, STATUS_STALE);
+        } else {
+            ring_store<MODE>(L, acc, int64_t(cur.row0) + cur.m0, cur.nt, cur.valid, cur.sh, wm, wn, lane);
+        }
+        if (!has_next)
+            break;
+        t = tn;
+        cur = nxt;
+        cur_ok = nxt_ok;
+#pragma unroll
+        for (int i = 0; i < LA; ++i)
+            aoff[i] = naoff[i];
+        load_frags0();                               // stage 0 of the new tile (landed by the last barrier)
     }
 }
 

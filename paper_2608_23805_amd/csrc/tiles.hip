@@ -28,11 +28,19 @@ hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
     return hipGetLastError();
 }
 
+// workgroups of a persistent launch: one per compute unit
+static int g_persistent_wgs = 256;
+
 hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    launch_k(ring_gemm_kernel<RingMode::Down>, L.n_tiles, ring::THREADS, 0, s, L);
+    if (L.I / ring::SK >= 8 && L.n_tiles > g_persistent_wgs) {
+        // K loop long enough for the cross-tile pipeline: one workgroup per CU walks its tiles
+        launch_k(ring_gemm_persistent<RingMode::Down>, g_persistent_wgs, ring::THREADS, 0, s, L);
+    } else {
+        launch_k(ring_gemm_kernel<RingMode::Down>, L.n_tiles, ring::THREADS, 0, s, L);
+    }
     return hipGetLastError();
 }
 
@@ -66,6 +74,14 @@ hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, cons
 
 hipError_t init_tile_attributes()
 {
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess)
+        return e;
+    // a multiple of the 8 XCDs keeps each XCD's workgroups on its own tile range
+    g_persistent_wgs = cus >= 8 ? cus / 8 * 8 : 8;
     return allow_large_lds(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
 }
 
