@@ -62,7 +62,7 @@ constexpr int LPS = LA + LB;
 constexpr uint32_t RSRC_FLAGS = 0x00020000u; // raw buffer, 32-bit data format
 }  // namespace ring
 
-enum class RingMode : int { GateUp = 0, Down = 1 };
+enum class RingMode : int { GateUp = 0, Down = 1, Router = 2 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -122,6 +122,35 @@ __device__ __forceinline__ void ring_store(const ExpertLaunch &L, const f32x4 (&
                 }
             }
         }
+    } else if constexpr (MODE == RingMode::Router) {
+        const int E = L.E;
+        float *base = L.logits + rowbase * E;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int row = wm * 64 + q * 16 + (lane & 15);
+            if (row < valid) {
+#pragma unroll
+                for (int a = 0; a < 8; ++a) {
+                    const int c = nt * ring::TN + wn * 128 + a * 16 + 4 * (lane >> 4);
+                    float *dst = base + (row * E + c);
+                    if (c + 3 < E) {
+                        f32x4 v = acc[a][q];
+                        if (L.bias) {
+                            v[0] += L.bias[c];
+                            v[1] += L.bias[c + 1];
+                            v[2] += L.bias[c + 2];
+                            v[3] += L.bias[c + 3];
+                        }
+                        *reinterpret_cast<f32x4 *>(dst) = v;
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (c + j < E)
+                                dst[j] = acc[a][q][j] + (L.bias ? L.bias[c + j] : 0.0f);
+                    }
+                }
+            }
+        }
     } else {
         const int d = L.d;
         uint8_t *base = reinterpret_cast<uint8_t *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + rowbase * d +
@@ -153,15 +182,16 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
 {
     using namespace ring;
     constexpr bool GU = MODE == RingMode::GateUp;
+    constexpr bool RT = MODE == RingMode::Router;     // router logits: one item of T token rows, E router rows
     __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * STAGE];
 
     const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
-    if (!slot_current(it, L.gen_dev, L.status))
+    const WorkItem it = RT ? WorkItem{-1, -1, 0u, 0, L.T, 0} : L.items[find_item(L.items, L.n_items, t)];
+    if (!RT && !slot_current(it, L.gen_dev, L.status))
         return;
     const int d = L.d, I = L.I;
-    const int K = GU ? d : I;
-    const int ntn = GU ? I / 128 : d / TN;
+    const int K = (GU || RT) ? d : I;
+    const int ntn = RT ? (L.E + TN - 1) / TN : GU ? I / 128 : d / TN;
     const int local = t - it.tile0;
     const int m0 = (local / ntn) * TM;
     const int nt = local % ntn;
@@ -174,7 +204,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
     // 16 (i WAVES + wave) + lane / 4; lane % 4 is the 16-byte slot it fills
     const int rl = lane >> 2;
     const uint32_t cw = uint32_t(((lane & 3) ^ ((rl >> 2) & 3)) << 4);
-    const void *abase = GU ? L.x : (sh ? L.act_s : L.act);
+    const void *abase = (GU || RT) ? L.x : (sh ? L.act_s : L.act);   // router: token rows (no act buffers)
     uint32_t aoff[LA];
     bool areal[LA];
 #pragma unroll
@@ -183,16 +213,21 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
         areal[i] = blk * 16 < valid;
         const int r = blk * 16 + rl;
         const int m = m0 + (r < valid ? r : 0);
-        const uint32_t src = GU ? uint32_t(sh ? m : L.perm[it.row0 + m]) : uint32_t(it.row0 + m);
+        const uint32_t src = (GU && !sh) ? uint32_t(L.perm[it.row0 + m]) : uint32_t(it.row0 + m);
         aoff[i] = src * uint32_t(K * 2) + cw;
     }
-    const uint8_t *wobj = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
-    const uint8_t *bbase = GU ? wobj : wobj + uint64_t(2) * I * d * 2;   // Wd follows Wg, Wu
+    const uint8_t *wobj = RT ? L.wbase : sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
+    const uint8_t *bbase = (GU || RT) ? wobj : wobj + uint64_t(2) * I * d * 2;   // Wd follows Wg, Wu
     uint32_t boff[LB];
+    bool breal[LB];
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
         const int r = (i * WAVES + wave) * 16 + rl;   // stage B row
-        const int src = GU ? (r < 128 ? nt * 128 + r : I + nt * 128 + (r - 128)) : nt * TN + r;
+        int src = GU ? (r < 128 ? nt * 128 + r : I + nt * 128 + (r - 128)) : nt * TN + r;
+        // router rows past E: whole 16-row blocks load zeros, a partial block reads row E - 1 (never stored)
+        breal[i] = !RT || nt * TN + (i * WAVES + wave) * 16 < L.E;
+        if (RT && src >= L.E)
+            src = L.E - 1;
         boff[i] = uint32_t(src) * uint32_t(K * 2) + cw;
     }
     const int nstage = K / SK;
@@ -210,7 +245,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
             dma16_lds(areal[i] ? ar : none, buf + (i * WAVES + wave) * 1024, aoff[i], kb);
 #pragma unroll
         for (int i = 0; i < LB; ++i)
-            dma16_lds(br, buf + TM * ROWB + (i * WAVES + wave) * 1024, boff[i], kb);
+            dma16_lds(breal[i] ? br : none, buf + TM * ROWB + (i * WAVES + wave) * 1024, boff[i], kb);
     };
     auto sync_stage = [&](auto waitn) {
         __builtin_amdgcn_s_waitcnt(VMCNT_WAIT(decltype(waitn)::value));

@@ -108,6 +108,11 @@ struct ExpertLaunch {
     // the grid (n_tiles) is then an upper bound and workgroups past the last
     // item exit.  direct.demand null: `items` is the list.
     DirectList direct;
+    // router logits launches (ring tiles in router mode) only: x [T, d] tokens,
+    // wbase the router weight [E, d], logits[t, e] = x[t] . Wr[e] + bias[e]
+    const float *bias;
+    float *logits;
+    int T, E;
 };
 
 // tiles per item of each launch kind

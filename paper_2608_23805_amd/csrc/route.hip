@@ -17,7 +17,6 @@
 #include <algorithm>
 
 #include "common.h"
-#include "gemm_tile.h"
 #include "kernels.h"
 
 namespace msi {

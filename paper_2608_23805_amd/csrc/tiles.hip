@@ -1,9 +1,8 @@
-// tiles.hip -- launches of the tile kernels: the routed-expert gate/up and
-// down projections of experts with more than 16 routed rows (gemm_ring.h)
-// and the router logits of long batches (gemm_tile.h).
+// tiles.hip -- launches of the ring tile kernels (gemm_ring.h): the
+// routed-expert gate/up and down projections of experts with more than 16
+// routed rows, and the router logits of batches of more than 16 tokens.
 #include "common.h"
 #include "gemm_ring.h"
-#include "gemm_tile.h"
 #include "kernels.h"
 
 namespace msi {
@@ -49,26 +48,16 @@ hipError_t launch_router_logits_bf16(const uint16_t *x, const uint16_t *wr, cons
 {
     if (T == 0)
         return hipSuccess;
-    TileArgs p{};
-    p.a = x;
-    p.lda = d;
-    p.perm = nullptr;
-    p.wbase = reinterpret_cast<const uint8_t *>(wr);
-    p.wstride = 0;
-    p.K = d;
-    p.n_valid = E;
-    p.n_tiles_n = (E + tile::BN - 1) / tile::BN;
-    p.d = d;
-    p.items = nullptr;
-    p.n_items = 1;
-    p.single = WorkItem{-1, -1, 0u, 0, T, 0};
-    p.gen_dev = nullptr;
-    p.status = nullptr;
-    p.out = L;
-    p.ldo = E;
-    p.bias = bias;
-    const int tiles = ((T + tile::BM - 1) / tile::BM) * p.n_tiles_n;
-    launch_k(tile_gemm_kernel<TileMode::Router>, tiles, tile::THREADS, tile::LDS_BYTES, s, p);
+    ExpertLaunch R{};
+    R.x = x;
+    R.wbase = reinterpret_cast<const uint8_t *>(wr);
+    R.d = d;
+    R.bias = bias;
+    R.logits = L;
+    R.T = T;
+    R.E = E;
+    const int tiles = ((T + ring::TM - 1) / ring::TM) * ((E + ring::TN - 1) / ring::TN);
+    launch_k(ring_gemm_kernel<RingMode::Router>, tiles, ring::THREADS, 0, s, R);
     return hipGetLastError();
 }
 
@@ -82,7 +71,7 @@ hipError_t init_tile_attributes()
         return e;
     // a multiple of the 8 XCDs keeps each XCD's workgroups on its own tile range
     g_persistent_wgs = cus >= 8 ? cus / 8 * 8 : 8;
-    return allow_large_lds(reinterpret_cast<const void *>(&tile_gemm_kernel<TileMode::Router>));
+    return hipSuccess;
 }
 
 }  // namespace msi
