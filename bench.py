@@ -324,8 +324,13 @@ def main():
     cs = torch.cuda.current_stream()
     side = torch.cuda.Stream()
 
-    if "decode" in skip:            # profiling aid: prefill only
-        print(json.dumps({"prefill": bench_prefill(args, cs, side)}), flush=True)
+    if "decode" in skip:            # profiling aid: the prefill workloads only
+        res = {}
+        if "prefill" not in skip:
+            res["prefill"] = bench_prefill(args, cs, side)
+        if "q4" not in skip:
+            res["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
+        print(json.dumps(res), flush=True)
         return
     dec, li = bench_decode(args, cs, side)
     extra = {}
