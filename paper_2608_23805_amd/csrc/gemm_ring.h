@@ -93,10 +93,32 @@ __device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi)
     return __builtin_bit_cast(uint32_t, v);
 }
 
+// Output rows leave the MFMA tiles as 4-feature pieces: lane (i, j) (i = lane % 16, j = lane / 16) holds
+// features 16 a + 4 j .. 16 a + 4 j + 3 of row i for every 16-feature block a, two bf16 per dword (lo: the
+// first two, hi: the last two).  For two consecutive blocks a0, a0 + 1 this regroups the pieces so that
+// lane (i, j) holds the 16 contiguous bytes 16 j .. 16 j + 15 of the 64 bytes the two blocks cover (lanes
+// of rows j = 0, 1: block a0; j = 2, 3: block a0 + 1), and each store writes 64 contiguous bytes per row
+// instead of four 8-byte pieces 32 bytes apart.  The 32-lane swap exchanges lanes 32 apart, the 16-lane
+// swap lanes 16 apart (gfx950 lane permutes; every lane takes part, so they run outside row predicates).
+__device__ __forceinline__ uint4 gather16(uint32_t lo0, uint32_t hi0, uint32_t lo1, uint32_t hi1)
+{
+    const auto l32 = __builtin_amdgcn_permlane32_swap(lo0, lo1, false, false);
+    const auto h32 = __builtin_amdgcn_permlane32_swap(hi0, hi1, false, false);
+    const auto l16 = __builtin_amdgcn_permlane16_swap(l32[0], l32[1], false, false);
+    const auto h16 = __builtin_amdgcn_permlane16_swap(h32[0], h32[1], false, false);
+    uint4 v;
+    v.x = l16[0];
+    v.y = h16[0];
+    v.z = l16[1];
+    v.w = h16[1];
+    return v;
+}
+
 // Tile epilogue: lane holds row 16 q + lane % 16 of the wavefront's 64 rows and
 // features 16 a + 4 (lane / 16) + j of its 128 weight rows.  Gate/up stores
-// act = silu(gate) * up; down stores y = row_weight * acc; bf16, 8 bytes per
-// lane and block.  Addresses: a uniform tile base plus 32-bit lane offsets.
+// act = silu(gate) * up; down stores y = row_weight * acc; bf16, regrouped so
+// each lane stores 16 contiguous bytes.  Addresses: a uniform tile base plus
+// 32-bit lane offsets.
 template <RingMode MODE>
 __device__ __forceinline__ void ring_store(const ExpertLaunch &L, const f32x4 (&acc)[8][4], int64_t rowbase, int nt,
                                            int valid, bool sh, int wm, int wn, int lane_in)
@@ -110,16 +132,19 @@ __device__ __forceinline__ void ring_store(const ExpertLaunch &L, const f32x4 (&
                                                     nt * 128 + wn * 64);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int row = wm * 64 + q * 16 + (lane & 15);
-            if (row < valid) {
-                const uint32_t off = uint32_t(row * I + 4 * (lane >> 4)) * 2u;
+            uint32_t lo[4], hi[4];
 #pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    uint2 v;
-                    v.x = pack_bf16x2_hw(silu_hw(acc[a][q][0]) * acc[a + 4][q][0], silu_hw(acc[a][q][1]) * acc[a + 4][q][1]);
-                    v.y = pack_bf16x2_hw(silu_hw(acc[a][q][2]) * acc[a + 4][q][2], silu_hw(acc[a][q][3]) * acc[a + 4][q][3]);
-                    *reinterpret_cast<uint2 *>(base + (off + uint32_t(a * 32))) = v;
-                }
+            for (int a = 0; a < 4; ++a) {
+                lo[a] = pack_bf16x2_hw(silu_hw(acc[a][q][0]) * acc[a + 4][q][0], silu_hw(acc[a][q][1]) * acc[a + 4][q][1]);
+                hi[a] = pack_bf16x2_hw(silu_hw(acc[a][q][2]) * acc[a + 4][q][2], silu_hw(acc[a][q][3]) * acc[a + 4][q][3]);
+            }
+            const int row = wm * 64 + q * 16 + (lane & 15);
+            const uint32_t off = uint32_t(row * I) * 2u + uint32_t(16 * (lane >> 4));
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const uint4 v = gather16(lo[2 * k], hi[2 * k], lo[2 * k + 1], hi[2 * k + 1]);
+                if (row < valid)
+                    *reinterpret_cast<uint4 *>(base + (off + uint32_t(64 * k))) = v;
             }
         }
     } else if constexpr (MODE == RingMode::Router) {
@@ -156,19 +181,29 @@ __device__ __forceinline__ void ring_store(const ExpertLaunch &L, const f32x4 (&
         uint8_t *base = reinterpret_cast<uint8_t *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + rowbase * d +
                                                     nt * ring::TN + wn * 128);
         const float *rw = (sh || !L.row_weight) ? nullptr : L.row_weight + rowbase;
+        // all four row weights first, so one wait covers them (the stores below never wait on each other)
+        float wq[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int row = wm * 64 + q * 16 + (lane & 15);
-            if (row < valid) {
-                const float wgt = rw ? rw[row] : 1.0f;
-                const uint32_t off = uint32_t(row * d + 4 * (lane >> 4)) * 2u;
+            wq[q] = (rw && row < valid) ? rw[row] : 1.0f;
+        }
 #pragma unroll
-                for (int a = 0; a < 8; ++a) {
-                    uint2 v;
-                    v.x = pack_bf16x2_hw(acc[a][q][0] * wgt, acc[a][q][1] * wgt);
-                    v.y = pack_bf16x2_hw(acc[a][q][2] * wgt, acc[a][q][3] * wgt);
-                    *reinterpret_cast<uint2 *>(base + (off + uint32_t(a * 32))) = v;
-                }
+        for (int q = 0; q < 4; ++q) {
+            const int row = wm * 64 + q * 16 + (lane & 15);
+            const float wgt = wq[q];
+            uint32_t lo[8], hi[8];
+#pragma unroll
+            for (int a = 0; a < 8; ++a) {
+                lo[a] = pack_bf16x2_hw(acc[a][q][0] * wgt, acc[a][q][1] * wgt);
+                hi[a] = pack_bf16x2_hw(acc[a][q][2] * wgt, acc[a][q][3] * wgt);
+            }
+            const uint32_t off = uint32_t(row * d) * 2u + uint32_t(16 * (lane >> 4));
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint4 v = gather16(lo[2 * k], hi[2 * k], lo[2 * k + 1], hi[2 * k + 1]);
+                if (row < valid)
+                    *reinterpret_cast<uint4 *>(base + (off + uint32_t(64 * k))) = v;
             }
         }
     }
@@ -349,16 +384,31 @@ struct RingTile {
     int ii;             // item index
     int row0, m0, nt, valid, slot;
     uint32_t gen;
-    bool sh;
+    int sh;             // shared expert (an int: a struct without padding copies as plain registers)
     const uint8_t *bbase;
 };
+
+// The work list and the slot generations, read through the constant address space so the persistent
+// kernel's per-tile lookups are scalar loads: those wait on their own counter, not behind the tile copies
+// and output stores in flight.  (Generations are read once per tile, as a plain load would read them.)
+#if defined(__HIP_DEVICE_COMPILE__)
+#define MSI_SCALAR_AS __attribute__((address_space(4)))
+#else
+#define MSI_SCALAR_AS
+#endif
+template <class T>
+__device__ __forceinline__ const MSI_SCALAR_AS T *scalar_view(const T *p)
+{
+    return (const MSI_SCALAR_AS T *)p;
+}
 
 template <RingMode MODE>
 __device__ __forceinline__ RingTile ring_tile_at(const ExpertLaunch &L, int t, int ii)
 {
-    while (ii + 1 < L.n_items && L.items[ii + 1].tile0 <= t)   // items are sorted by tile0
+    const auto *items = scalar_view(L.items);
+    while (ii + 1 < L.n_items && items[ii + 1].tile0 <= t)   // items are sorted by tile0
         ++ii;
-    const WorkItem w = L.items[ii];
+    const WorkItem w = items[ii];
     constexpr bool GU = MODE == RingMode::GateUp;
     const int ntn = GU ? L.I / 128 : L.d / ring::TN;
     RingTile r;
@@ -480,14 +530,16 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
                                                             : uint32_t(L.perm[T.row0 + T.m0 + r]));
             else
                 src = uint32_t(T.row0 + T.m0 + r);
-            ao[i] = src * uint32_t(K * 2) + cw;
+            int l = lane;                               // (opaque: the chunk offset is recomputed here too)
+            asm volatile("" : "+v"(l));
+            ao[i] = src * uint32_t(K * 2) + uint32_t(((l & 3) ^ ((l >> 4) & 3)) << 4);
         }
     };
     using W_STEADY = std::integral_constant<int, LP * (NBUF - 3)>;   // stage s+1 landed, s+2 in flight
 
     // ---- first tile (blocking)
     RingTile cur = ring_tile_at<MODE>(L, t, find_item(L.items, L.n_items, t));
-    bool cur_ok = cur.sh || L.gen_dev[cur.slot] == cur.gen;
+    bool cur_ok = cur.sh || scalar_view(L.gen_dev)[cur.slot] == cur.gen;
     uint32_t aoff[LA];
     a_offsets(cur, aoff, false);
     issue(cur, aoff, std::integral_constant<int, 0>{}, 0, true);
@@ -554,7 +606,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
         const int tn = t + tstep;
         const bool has_next = tn < tend;
         const RingTile nxt = has_next ? ring_tile_at<MODE>(L, tn, cur.ii) : cur;
-        const bool nxt_ok = nxt.sh || !has_next || L.gen_dev[nxt.slot] == nxt.gen;
+        const bool nxt_ok = nxt.sh || !has_next || scalar_view(L.gen_dev)[nxt.slot] == nxt.gen;
 
         using S0 = std::integral_constant<int, 0>;
         using S1 = std::integral_constant<int, 1>;
