@@ -10,17 +10,18 @@
 // matching up rows; down: 256 output features), 8 wavefronts as 4 (rows) x 2
 // (features), each 64 rows x 128 weight rows as 4 x 8 blocks of
 // v_mfma_f32_16x16x32_bf16 with the weights as the A operand, so a lane ends
-// with 4 consecutive output features of one row (8-byte packed stores, and
-// SiLU(gate) * up formed in registers).  Two wavefronts per SIMD, fp32
+// with 4 consecutive output features of one row (SiLU(gate) * up formed in
+// registers).  Two wavefronts per SIMD, fp32
 // accumulators in VGPRs.
 //
 // K advances in stages of 32 elements.  A stage (256 A rows and 256 B rows of
 // 64 bytes, 32 KiB) is copied from memory straight into LDS by buffer loads
 // (no register staging), into a ring of four stage buffers: while stage s is
 // multiplied, stages s+1 .. s+3 are in flight.  Each 16-byte chunk c of a
-// stage row r sits at slot c ^ ((r >> 2) & 3) of the row, so both the copies
-// (16 rows x 64 bytes per instruction) and the fragment reads (16 rows x 16
-// bytes per 16 lanes) are free of LDS bank conflicts.  The fragments of
+// stage row r sits at slot c ^ ring_swz(r) of the row (ring_swz below), so
+// the fragment reads (16 rows x 16 bytes per 16 lanes) spread over all LDS
+// banks whether the banks serve 16 lanes of 16 bytes or 8 lanes per cycle;
+// the copies write 16 rows x 64 bytes per instruction.  The fragments of
 // stage s+1 are read while stage s is multiplied (weight fragments double
 // buffered, each row fragment right after its last use), two reads per eight
 // MFMAs.  The loop has no branches: stages past the end are loaded through a
@@ -46,6 +47,13 @@
 #include "kernels.h"
 
 namespace msi {
+
+// Slot permutation of the four 16-byte chunks of a 64-byte stage row, by the row's position within its
+// 16-row block.  A fragment read has 16 lanes read chunk c of 16 consecutive rows: rows 4 apart share their
+// 64-byte position modulo 256 bytes and rows 2 apart modulo 128 bytes, so the permutation gives distinct
+// slots to rows {a, a+4, a+8, a+12} (16 lanes per 256-byte bank cycle) and to rows of equal parity within
+// each half of 8 (8 lanes per 128-byte cycle).
+__device__ __forceinline__ int ring_swz(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | (((r >> 2) & 1) << 1); }
 
 namespace ring {
 constexpr int SK = 32;                       // K elements per stage
@@ -238,7 +246,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
     // ---- copy addressing: instruction i of this wavefront covers stage rows
     // 16 (i WAVES + wave) + lane / 4; lane % 4 is the 16-byte slot it fills
     const int rl = lane >> 2;
-    const uint32_t cw = uint32_t(((lane & 3) ^ ((rl >> 2) & 3)) << 4);
+    const uint32_t cw = uint32_t(((lane & 3) ^ ring_swz(rl & 15)) << 4);
     const void *abase = (GU || RT) ? L.x : (sh ? L.act_s : L.act);   // router: token rows (no act buffers)
     uint32_t aoff[LA];
     bool areal[LA];
@@ -292,7 +300,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
 
     // ---- fragment addressing: row lane % 16 of a 16-row block, chunk lane / 16
     const int wm = wave >> 1, wn = wave & 1;
-    const uint32_t fofs = uint32_t((lane & 15) * ROWB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4));
+    const uint32_t fofs = uint32_t((lane & 15) * ROWB + (((lane >> 4) ^ ring_swz(lane & 15)) << 4));
     auto wrow = [&](int a) { return GU ? (a < 4 ? wn * 64 + a * 16 : 128 + wn * 64 + (a - 4) * 16) : wn * 128 + a * 16; };
 
 #pragma unroll
@@ -461,7 +469,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);   // (uniform: scalar selects, no waterfall loops)
     const int wm = wave >> 1, wn = wave & 1;
     const int rl = lane >> 2;
-    const uint32_t cw = uint32_t(((lane & 3) ^ ((rl >> 2) & 3)) << 4);
+    const uint32_t cw = uint32_t(((lane & 3) ^ ring_swz(rl & 15)) << 4);
     uint32_t boff[LB];   // B rows of this lane's copies, relative to the tile's weight base
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
@@ -470,7 +478,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
         boff[i] = uint32_t(src) * uint32_t(K * 2) + cw;
     }
     const __amdgpu_buffer_rsrc_t none = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(L.x), 0, 0, RSRC_FLAGS);
-    const uint32_t fofs = uint32_t((lane & 15) * ROWB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4));
+    const uint32_t fofs = uint32_t((lane & 15) * ROWB + (((lane >> 4) ^ ring_swz(lane & 15)) << 4));
     auto wrow = [&](int a) { return GU ? (a < 4 ? wn * 64 + a * 16 : 128 + wn * 64 + (a - 4) * 16) : wn * 128 + a * 16; };
     auto sync_stage = [&](auto waitn) {
         __builtin_amdgcn_s_waitcnt(VMCNT_WAIT(decltype(waitn)::value));
@@ -532,7 +540,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
                 src = uint32_t(T.row0 + T.m0 + r);
             int l = lane;                               // (opaque: the chunk offset is recomputed here too)
             asm volatile("" : "+v"(l));
-            ao[i] = src * uint32_t(K * 2) + uint32_t(((l & 3) ^ ((l >> 4) & 3)) << 4);
+            ao[i] = src * uint32_t(K * 2) + uint32_t(((l & 3) ^ ring_swz((l >> 2) & 15)) << 4);
         }
     };
     using W_STEADY = std::integral_constant<int, LP * (NBUF - 3)>;   // stage s+1 landed, s+2 in flight
