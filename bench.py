@@ -36,6 +36,10 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 # only while the kernel's sources hash to the recorded value
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "stream_gateup_decode_bf16_traffic.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f) for f in ("experts.hip", "common.h")]
+# the same for the bf16 prefill gate/up launch (ring tile kernel)
+PREFILL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ring_gemm_prefill_bf16_traffic.md")
+PREFILL_KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f)
+                          for f in ("gemm_ring.h", "tiles.hip", "common.h")]
 
 
 def log(*a):
@@ -171,8 +175,14 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
     n_gu, ms_gu = t["gateup_tile"]
     avg_gu = ms_gu / max(n_gu, 1)
     c = r.counts.cpu().numpy()
-    rows_tile = int(c[c > 16].sum())          # rows taken by the tiled path (the rest stream)
+    # rows taken by the tiled path (experts with more than 16 rows; the rest stream), plus the shared
+    # expert's T rows, which ride in the same launch
+    rows_tile = int(c[c > 16].sum()) + s.T
     flops_gu = 2.0 * rows_tile * s.d * 2 * s.I
+    # algorithmic bytes of that launch: each tile expert's Wg and Wu (and the shared one's) once, every
+    # token's x row once, act written once
+    wbytes = 2 * s.I * s.d * 2 if s.wdtype != "q4b32" else 2 * s.I * (s.d // 2 + s.d // 32 * 2)
+    bytes_gu = (int((c > 16).sum()) + 1) * wbytes + s.T * s.d * 2 + rows_tile * s.I * 2
     layer_flops = 2.0 * s.T * (s.K * 3 * s.d * s.I + 3 * s.d * s.I + s.d * s.E)
     achieved = flops_gu / (avg_gu * 1e-3) / 1e12
     kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 1)} for k, (n, v) in t.items() if n}
@@ -185,8 +195,11 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                          "kernel": "tile_q4_kernel<GateUp>" if s.wdtype == "q4b32" else "ring_gemm_kernel<GateUp>",
                          "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
-                         "flops_per_launch": flops_gu, "avg_launch_us": round(avg_gu * 1e3, 1),
+                         "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "traffic": None if s.wdtype == "q4b32" else recorded_traffic(PREFILL_TRAFFIC_FILE,
+                                                                                      PREFILL_KERNEL_SOURCES),
+                         "flops_per_launch": flops_gu, "algorithmic_bytes_per_launch": bytes_gu,
+                         "avg_launch_us": round(avg_gu * 1e3, 1),
                          "note": "int4 weights unpacked to bf16 MFMA operands" if s.wdtype == "q4b32" else ""},
                kernels=kernels)
     log(f"[bench] prefill: {ms:.3f} ms/step, {res['value']:.0f} tok/s, layer {res['layer_tflops']} TFLOP/s, "
@@ -238,24 +251,25 @@ def bench_stack(args, cs, side):
     return res
 
 
-def kernel_sources_sha256():
+def kernel_sources_sha256(sources=None):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources or KERNEL_SOURCES:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def recorded_traffic():
-    """Measured HBM bytes per decode gate/up launch, or None when no
-    measurement exists or the kernel's sources changed since it was taken."""
+def recorded_traffic(path=TRAFFIC_FILE, sources=None):
+    """Measured HBM bytes per launch of the dominant kernel (decode gate/up by
+    default), or None when no measurement exists or the kernel's sources
+    changed since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             kv = dict(re.findall(r"^([a-z0-9_]+): *(\S+)$", fh.read(), re.M))
     except OSError:
         return None
-    if kv.get("kernel_sources_sha256") != kernel_sources_sha256():
+    if kv.get("kernel_sources_sha256") != kernel_sources_sha256(sources):
         return None
     try:
         return int(kv["traffic_bytes_per_launch"])
