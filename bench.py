@@ -29,7 +29,7 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 
 METRIC = "routed tokens/sec per MoE layer (decode T=16, prefill T=32K); % HBM / MFMA peak"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
-TIMING_PERIOD = 7               # decode: every 7th dominant-kernel launch carries events
+TIMING_PERIOD = 7               # decode: at most every 7th dominant-kernel launch carries events
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 # HBM traffic of the decode gate/up launch, from two hardware-counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by a plain copy kernel's counters; valid
@@ -92,6 +92,15 @@ def _run(plan, xs, dev, r, ws, out, steps, warmup, cs, side, on_step=None):
     return (time.perf_counter() - t0) * 1e3 / max(steps, 1)
 
 
+def timing_period(steps):
+    """Every how many steps the decode gate/up launch carries events: an odd
+    period (coprime with the 16-batch rotation, so every batch is sampled),
+    at most TIMING_PERIOD, and at least 6 timed launches when the run has
+    that many steps (each timed launch adds host time to the step)."""
+    p = max(1, min(TIMING_PERIOD, steps // 6))
+    return p if p % 2 else p - 1
+
+
 def bench_decode(args, cs, side):
     import synth
     wl = synth.WORKLOADS["decode_bf16"]
@@ -103,12 +112,18 @@ def bench_decode(args, cs, side):
     # costs host time on this latency-bound step, so only every
     # TIMING_PERIOD-th step of the timed region is timed (the period is
     # coprime with the 16 batches, so every batch is sampled).
-    _run(plan, xs, dev, r, ws, out, 0, args.warmup, cs, side)
+    # (at least one pass over the whole rotation, whatever --warmup says, so the timed region needs no fill)
+    _run(plan, xs, dev, r, ws, out, 0, max(args.warmup, len(xs)), cs, side)
     plan.set_timing(args.telemetry == "on", kinds=["gateup_stream"])
-    plan.set_timing_period(TIMING_PERIOD)
+    period = timing_period(args.steps)
+    plan.set_timing_period(period)
+    before = plan.stats()
     ms = _run(plan, xs, dev, r, ws, out, args.steps, 0, cs, side)
     t = plan.timings()
     st = plan.stats()
+    fills_timed = st["fills"] - before["fills"]
+    if fills_timed:
+        raise RuntimeError(f"decode: {fills_timed} fills inside the timed region of an all-resident run")
     # a further untimed pass with every launch carrying events: per-kernel durations
     plan.set_timing(args.telemetry == "on")
     plan.set_timing_period(1)
@@ -126,7 +141,7 @@ def bench_decode(args, cs, side):
         n_obj, n_rows = len(dem) + 1, int(dem.sum()) + s.T
         bytes_b.append(n_obj * 2 * s.I * s.d * 2 + n_rows * (s.d * 2 + s.I * 2))
         down_b.append(n_obj * s.d * s.I * 2 + n_rows * (s.I * 2 + s.d * 2))
-    per_step_bytes = [bytes_b[i % len(xs)] for i in range(0, args.steps, TIMING_PERIOD)]
+    per_step_bytes = [bytes_b[i % len(xs)] for i in range(0, args.steps, period)]
     n_gu, ms_gu = t["gateup_stream"]
     n_dn, ms_dn = t_all["down_stream"]
     avg_gu = ms_gu / max(n_gu, 1)
@@ -144,7 +159,7 @@ def bench_decode(args, cs, side):
                          "bytes_per_batch_mean": int(sum(bytes_b) / len(bytes_b))},
                down={"achieved_GBs": round(bytes_dn / (avg_dn * 1e-3) / 1e9, 1) if avg_dn > 0 else None,
                      "avg_launch_us": round(avg_dn * 1e3, 2), "bytes_per_launch": int(bytes_dn)},
-               stats={k: st[k] for k in ("fills", "hits", "misses", "rounds")})
+               stats={k: st[k] for k in ("fills", "hits", "misses", "rounds")}, fills_in_timed_region=fills_timed)
     log(f"[bench] decode: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s, gate/up {avg_gu * 1e3:.1f} us "
         f"= {achieved:.0f} GB/s, down {avg_dn * 1e3:.1f} us")
     return res, li
@@ -186,6 +201,7 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
     layer_flops = 2.0 * s.T * (s.K * 3 * s.d * s.I + 3 * s.d * s.I + s.d * s.E)
     achieved = flops_gu / (avg_gu * 1e-3) / 1e12
     kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 1)} for k, (n, v) in t.items() if n}
+    routed_idx = r.idx.cpu().numpy()
     plan.close()
     res = dict(workload=name, value=round(s.T / (ms * 1e-3), 1), unit="routed tokens/s per layer",
                ms_per_step=round(ms, 3),
@@ -201,7 +217,7 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                          "flops_per_launch": flops_gu, "algorithmic_bytes_per_launch": bytes_gu,
                          "avg_launch_us": round(avg_gu * 1e3, 1),
                          "note": "int4 weights unpacked to bf16 MFMA operands" if s.wdtype == "q4b32" else ""},
-               kernels=kernels)
+               kernels=kernels, _routed_idx=routed_idx)
     log(f"[bench] prefill: {ms:.3f} ms/step, {res['value']:.0f} tok/s, layer {res['layer_tflops']} TFLOP/s, "
         f"gate/up {avg_gu * 1e3:.0f} us = {achieved:.0f} TFLOP/s")
     return res
@@ -212,9 +228,15 @@ def bench_decode_q4(args, cs, side):
     import synth
     wl = synth.WORKLOADS["decode_q4"]
     li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=16)
-    ms = _run(plan, xs, dev, r, ws, out, args.steps, args.warmup, cs, side)
+    _run(plan, xs, dev, r, ws, out, 0, max(args.warmup, len(xs)), cs, side)
+    before = plan.stats()
+    ms = _run(plan, xs, dev, r, ws, out, args.steps, 0, cs, side)
+    fills_timed = plan.stats()["fills"] - before["fills"]
     plan.close()
-    res = dict(workload="decode_q4", ms=round(ms, 4), tokens_per_s=round(wl.shape.T / (ms * 1e-3), 1))
+    if fills_timed:
+        raise RuntimeError(f"decode_q4: {fills_timed} fills inside the timed region of an all-resident run")
+    res = dict(workload="decode_q4", ms=round(ms, 4), tokens_per_s=round(wl.shape.T / (ms * 1e-3), 1),
+               fills_in_timed_region=fills_timed)
     log(f"[bench] decode_q4: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s")
     return res
 
@@ -292,9 +314,22 @@ def copy_calibration():
                                            "launches": 4}}), flush=True)
 
 
-def cpu_baseline(li, budget_s):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(li, budget_s, prefill_idx=None):
     """The fp64 oracle, as it stands, on the decode batch 0 (16 tokens), repeated
-    until about budget_s seconds of wall time."""
+    until about budget_s seconds of wall time.  With ``prefill_idx`` (the
+    GPU's routed sets of the 32K prefill batch) the oracle also routes that
+    whole batch and the sets are compared, near ties counted."""
     import oracle
     s = li.wl.shape
     o = oracle.Oracle()
@@ -307,8 +342,18 @@ def cpu_baseline(li, budget_s):
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return {"value": round(reps * s.T / el, 2), "unit": "routed tokens/s per layer", "cores": o.max_threads(),
-            "kind": "oracle", "sample": f"decode layer T=16 (one seeded batch), {reps} repetitions, {el:.1f} s"}
+    res = {"value": round(reps * s.T / el, 2), "unit": "routed tokens/s per layer", "cores": o.max_threads(),
+           "cpu_model": cpu_model(), "kind": "oracle",
+           "sample": f"decode layer T=16 (one seeded batch), {reps} repetitions, {el:.1f} s"}
+    if prefill_idx is not None:
+        import synth
+        from _gpu_helpers import check_all_sets
+        t1 = time.perf_counter()
+        pli = synth.layer_inputs(synth.WORKLOADS["prefill_bf16"], lazy=True)
+        res["prefill_routed_sets"] = check_all_sets(o, pli, prefill_idx)
+        res["prefill_routed_sets"]["oracle_s"] = round(time.perf_counter() - t1, 1)
+        log(f"[bench] prefill routed sets vs oracle: {res['prefill_routed_sets']}")
+    return res
 
 
 def main():
@@ -342,8 +387,10 @@ def main():
         res = {}
         if "prefill" not in skip:
             res["prefill"] = bench_prefill(args, cs, side)
+            res["prefill"].pop("_routed_idx")
         if "q4" not in skip:
             res["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
+            res["prefill_q4"].pop("_routed_idx")
         print(json.dumps(res), flush=True)
         return
     dec, li = bench_decode(args, cs, side)
@@ -357,7 +404,10 @@ def main():
         extra["decode_q4"] = bench_decode_q4(args, cs, side)
     if "stack" not in skip:
         extra["stack"] = bench_stack(args, cs, side)
-    cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds)
+    pidx = extra["prefill"].pop("_routed_idx") if "prefill" in extra else None
+    if "prefill_q4" in extra:
+        extra["prefill_q4"].pop("_routed_idx")
+    cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds, pidx)
 
     s = li.wl.shape
     line = {
@@ -369,6 +419,7 @@ def main():
                    "T": s.T, "d": s.d, "E": s.E, "top_k": s.K, "d_ff": s.I, "shared_experts": 1,
                    "slots_per_layer": 512, "batches_in_rotation": 16},
         "roofline": dec["roofline"], "cpu_baseline": cpu,
+        "fills_in_timed_region": dec["fills_in_timed_region"],
         "kernels_separate_pass": dec["kernels"], "down": dec["down"],
     }
     line.update(extra)

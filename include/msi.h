@@ -240,7 +240,13 @@ msi_status msi_plan_destroy(msi_plan *plan);
  * DeviceReady slots stay valid.  MSI_E_BUSY if a consumer is held. */
 msi_status msi_plan_reset(msi_plan *plan);
 
-/* Bytes of device workspace msi_route and msi_moe_forward need for T tokens. */
+/* Bytes of device workspace msi_route and msi_moe_forward need for T tokens.
+ * Layout (each part starts on a 256-byte boundary; ab = 4 for MSI_W_F32,
+ * else 2): router logits [T, E] f32 | per-block expert histograms
+ * [ceil(T / 256), E] i32 | act [T * K, d_ff] (permuted rows) | shared-expert
+ * act [T, d_ff] | y [T * K, d_model] (weighted expert outputs, permuted
+ * rows) | shared-expert output [T, d_model]; act, y and their shared parts
+ * in ab-byte elements (bf16 or f32).  Contents are scratch between calls. */
 msi_status msi_workspace_size(const msi_plan *plan, uint32_t n_tokens, uint64_t *bytes);
 
 /* Make expert `expert` of `layer` resident (Section 3.3; Section 4 scheduling).

@@ -8,7 +8,7 @@ product package.
 Every function follows the plain definition written at the top of
 ``moe_oracle.c`` (router logits, top-K with lower-id tie-break, restricted
 softmax, gated-SiLU experts, shared expert plus ascending-id combine, stable
-counting-sort permutation).
+counting-sort permutation, and the residual stream of a layer stack).
 """
 from __future__ import annotations
 
@@ -56,6 +56,7 @@ def _bind(lib):
     lib.msio_expert_ffn.argtypes = [i64, i64, i32, vp, vp, vp, vp]
     lib.msio_moe_layer.argtypes = [i64, i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp,
                                    i64, vp, vp, vp, vp, vp, vp, vp]
+    lib.msio_residual_step.argtypes = [i64, i64, vp, vp, vp, vp]
     lib.msio_max_threads.restype = i32
     lib.msio_mutant.restype = i32
     return lib
@@ -197,6 +198,34 @@ class Oracle:
         if want_logits:
             res["logits"] = lg
         return res
+
+    def residual_step(self, h: np.ndarray, out: Optional[np.ndarray] = None):
+        """Step 6 for one layer boundary: h_next = h + out (out None: h_next =
+        h), x_next = bf16 bits of h_next / rms(h_next) per row.  Returns
+        (h_next fp64, x_next uint16)."""
+        h = np.ascontiguousarray(h, dtype=np.float64)
+        rows, cols = h.shape
+        o = None if out is None else np.ascontiguousarray(out, dtype=np.float64)
+        hn = np.empty_like(h)
+        x = np.empty((rows, cols), dtype=np.uint16)
+        self.lib.msio_residual_step(rows, cols, _p(h), _p(o), _p(hn), _p(x))
+        return hn, x
+
+    def stack(self, h0: np.ndarray, layers: Sequence[dict], K: int, I: int, wdtype: str):
+        """Step 6 over a stack: h_0 = h0 (fp64 [T, d]); layer l reads x_l =
+        bf16(h_l / rms(h_l)) and h_{l+1} = h_l + out_l(x_l).  ``layers`` holds
+        per layer dict(wr, bias, experts, shared).  Returns dict with h (the
+        final residual stream), xs (each layer's bf16 input), idx and gap
+        (each layer's selection and top-K logit gap)."""
+        h, x = self.residual_step(h0)
+        xs, idxs, gaps = [], [], []
+        for ly in layers:
+            r = self.moe_layer(x, ly["wr"], ly["bias"], ly["experts"], ly["shared"], K, I, wdtype, "bf16")
+            xs.append(x)
+            idxs.append(r["idx"])
+            gaps.append(r["gap"])
+            h, x = self.residual_step(h, r["out"])
+        return {"h": h, "x": x, "xs": xs, "idx": idxs, "gap": gaps}
 
     def max_threads(self) -> int:
         return int(self.lib.msio_max_threads())

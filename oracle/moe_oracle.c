@@ -13,16 +13,23 @@
  *                     equal to a full softmax renormalised over S_t)
  *   4. expert FFN     y = Wd (silu(Wg x) * (Wu x)),  silu(z) = z/(1+e^-z)
  *   5. combine        out_t = y_shared + sum_{e in S_t, ascending e} w_e y_e
+ *   6. layer stack    h_0 = the stack's input; layer l reads
+ *                     x_l = bf16(h_l / rms(h_l)), rms(h) = sqrt(mean_i h_i^2
+ *                     + 1e-6) per row, and h_{l+1} = h_l + out_l(x_l)
+ *                     (attention omitted; an unweighted RMS normalisation of
+ *                     each layer's input, as a transformer block applies)
  * plus the token-by-expert permutation (a stable counting sort of the T*K
  * assignments by (expert, token)).
  *
- * The paper runs the stock router and "the complete gate, up, and down
- * projections" of every selected expert (Section 5.4, principal experiment);
- * it does not print the MoE formulas.  Steps 1-5 are the standard
+ * The paper runs the stock router and the complete gate, up and down
+ * projections of every selected expert (the principal experiment, "Output-
+ * Exact Execution Beyond the Full-Residency Envelope", over a 48-layer
+ * model); it does not print the MoE formulas.  Steps 1-5 are the standard
  * softmax/top-k gated-SiLU MoE with an always-on shared expert; the readings
  * taken where the paper is silent (softmax then renormalise, ungated shared
  * expert, bias added before selection, lower id wins ties, fp32/bf16/int4
- * storage upcast exactly) are listed in the design notes.
+ * storage upcast exactly, the stack's input normalisation) are listed in the
+ * design notes.
  *
  * Inputs are read in their stored formats and upcast exactly to double:
  *   dtype 0 f32, 1 bf16 (uint16 = top half of binary32), 2 q4b32 (nibbles
@@ -155,13 +162,23 @@ void msio_dequant(int dtype, int64_t rows, int64_t cols, const void *src, double
 
 /* ---- step 1: router logits ---------------------------------------------- */
 
-static void logits_one(int64_t d, int64_t E, const wmat *x, int64_t t, const wmat *wr,
-                       const float *bias, double *L)
+/* The stored router weight [E, d] upcast once to fp64 (exact); caller frees. */
+static double *upcast_router(int64_t d, int64_t E, const wmat *wr)
+{
+    double *w = (double *)malloc(sizeof(double) * (size_t)(E * d));
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t i = 0; i < d; ++i)
+            w[e * d + i] = wmat_at(wr, e, i);
+    return w;
+}
+
+/* l_e = sum_i x_i Wr[e, i] (i ascending) + b_e for one token's upcast row x. */
+static void logits_one(int64_t d, int64_t E, const double *x, const double *wr, const float *bias, double *L)
 {
     for (int64_t e = 0; e < E; ++e) {
         double acc = 0.0;
         for (int64_t i = 0; i < d; ++i)
-            acc += wmat_at(x, t, i) * wmat_at(wr, e, i);
+            acc += x[i] * wr[e * d + i];
 #if MSIO_MUTANT == 1
         (void)bias;                                   /* bias dropped */
 #else
@@ -177,9 +194,19 @@ void msio_router_logits(int64_t T, int64_t d, int64_t E, int xdtype, const void 
 {
     wmat X = {xdtype, (const uint8_t *)x, T, d};
     wmat W = {xdtype, (const uint8_t *)wr, E, d};
-#pragma omp parallel for schedule(dynamic, 1)
-    for (int64_t t = 0; t < T; ++t)
-        logits_one(d, E, &X, t, &W, bias, L + t * E);
+    double *w = upcast_router(d, E, &W);
+#pragma omp parallel
+    {
+        double *xt = (double *)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t t = 0; t < T; ++t) {
+            for (int64_t i = 0; i < d; ++i)
+                xt[i] = wmat_at(&X, t, i);
+            logits_one(d, E, xt, w, bias, L + t * E);
+        }
+        free(xt);
+    }
+    free(w);
 }
 
 /* ---- step 2: top-K selection, ties to the lower expert id ----------------- */
@@ -351,6 +378,7 @@ void msio_moe_layer(int64_t T, int64_t d, int64_t E, int64_t K, int64_t I, int w
 {
     wmat X = {xdtype, (const uint8_t *)x, T, d};
     wmat W = {xdtype, (const uint8_t *)wr, E, d};
+    double *wrd = upcast_router(d, E, &W);
 #pragma omp parallel
     {
         double *L = (double *)malloc(sizeof(double) * (size_t)E);
@@ -365,7 +393,7 @@ void msio_moe_layer(int64_t T, int64_t d, int64_t E, int64_t K, int64_t I, int w
             int64_t t = tokens ? tokens[s] : s;
             for (int64_t i = 0; i < d; ++i)
                 xt[i] = wmat_at(&X, t, i);
-            logits_one(d, E, &X, t, &W, bias, L);
+            logits_one(d, E, xt, wrd, bias, L);
             double gap = NAN;
             if (forced_idx)
                 memcpy(idx, forced_idx + s * K, sizeof(int32_t) * (size_t)K);
@@ -406,6 +434,42 @@ void msio_moe_layer(int64_t T, int64_t d, int64_t E, int64_t K, int64_t I, int w
         free(xt);
         free(y);
         free(act);
+    }
+    free(wrd);
+}
+
+/* ---- step 6: the residual stream between stacked layers ------------------- */
+/*
+ * One row-wise step of the stack for `rows` tokens of `cols` features:
+ *   h_next = h + out   (out == NULL: h_next = h, the stack's input)
+ *   x_next = bf16_rne(h_next / sqrt(mean(h_next^2) + 1e-6))
+ * with the mean summed in column order in fp64.  h_next may alias h.
+ */
+void msio_residual_step(int64_t rows, int64_t cols, const double *h, const double *out, double *h_next,
+                        uint16_t *x_next)
+{
+    for (int64_t r = 0; r < rows; ++r) {
+        const double *hr = h + r * cols;
+        double *hn = h_next + r * cols;
+        double ss = 0.0;
+        for (int64_t c = 0; c < cols; ++c) {
+#if MSIO_MUTANT == 12
+            const double v = out ? out[r * cols + c] : hr[c];   /* residual dropped */
+#else
+            const double v = out ? hr[c] + out[r * cols + c] : hr[c];
+#endif
+            hn[c] = v;
+            ss += v * v;
+        }
+#if MSIO_MUTANT == 10
+        const double rms = sqrt(ss / (double)cols);              /* epsilon dropped */
+#elif MSIO_MUTANT == 11
+        const double rms = sqrt(ss + 1e-6);                      /* sum, not mean */
+#else
+        const double rms = sqrt(ss / (double)cols + 1e-6);
+#endif
+        for (int64_t c = 0; c < cols; ++c)
+            x_next[r * cols + c] = msio_f64_to_bf16(hn[c] / rms);
     }
 }
 

@@ -247,7 +247,12 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
     // 16 (i WAVES + wave) + lane / 4; lane % 4 is the 16-byte slot it fills
     const int rl = lane >> 2;
     const uint32_t cw = uint32_t(((lane & 3) ^ ring_swz(rl & 15)) << 4);
-    const void *abase = (GU || RT) ? L.x : (sh ? L.act_s : L.act);   // router: token rows (no act buffers)
+    // A rows: gate/up and router gather token rows of x by their row index (the caller keeps x under 2^31
+    // bytes); down reads the tile's own act rows, addressed from the tile's first row so the offsets stay
+    // small for any number of rows
+    const void *abase = (GU || RT) ? L.x
+                                   : static_cast<const uint8_t *>(sh ? L.act_s : L.act) +
+                                         (int64_t(it.row0) + m0) * int64_t(I) * 2;
     uint32_t aoff[LA];
     bool areal[LA];
 #pragma unroll
@@ -256,7 +261,8 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
         areal[i] = blk * 16 < valid;
         const int r = blk * 16 + rl;
         const int m = m0 + (r < valid ? r : 0);
-        const uint32_t src = (GU && !sh) ? uint32_t(L.perm[it.row0 + m]) : uint32_t(it.row0 + m);
+        const uint32_t src = !(GU || RT) ? uint32_t(m - m0) : !sh && GU ? uint32_t(L.perm[it.row0 + m])
+                                                                         : uint32_t(it.row0 + m);
         aoff[i] = src * uint32_t(K * 2) + cw;
     }
     const uint8_t *wobj = RT ? L.wbase : sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
@@ -394,6 +400,7 @@ struct RingTile {
     uint32_t gen;
     int sh;             // shared expert (an int: a struct without padding copies as plain registers)
     const uint8_t *bbase;
+    const uint8_t *abase;   // A rows: x (gate/up, gathered) or the tile's first act row (down)
 };
 
 // The work list and the slot generations, read through the constant address space so the persistent
@@ -432,6 +439,8 @@ __device__ __forceinline__ RingTile ring_tile_at(const ExpertLaunch &L, int t, i
     const uint8_t *wobj = r.sh ? L.shared_w : L.wbase + uint64_t(w.slot) * L.wstride;
     r.bbase = GU ? wobj + uint64_t(r.nt) * 128 * L.d * 2
                  : wobj + (uint64_t(2) * L.I * L.d + uint64_t(r.nt) * ring::TN * L.I) * 2;
+    r.abase = GU ? static_cast<const uint8_t *>(L.x)
+                 : static_cast<const uint8_t *>(r.sh ? L.act_s : L.act) + (int64_t(w.row0) + r.m0) * int64_t(L.I) * 2;
     return r;
 }
 
@@ -496,9 +505,8 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
     // stage copies: tile T's stage st into ring buffer B; !real (or past the tile's rows): zero-record loads
     auto issue = [&](const RingTile &T, const uint32_t (&ao)[LA], auto bufc, int st, bool real) {
         constexpr int B = decltype(bufc)::value;
-        const void *abase = GU ? L.x : (T.sh ? L.act_s : L.act);
         const __amdgpu_buffer_rsrc_t ar =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(abase), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(T.abase), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
         const __amdgpu_buffer_rsrc_t br =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(T.bbase), 0, real ? 0x7fffffff : 0, RSRC_FLAGS);
         uint8_t *buf = lds + B * STAGE;
@@ -537,7 +545,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
                 src = T.sh ? uint32_t(T.m0 + r) : (from_lds ? uint32_t(permlds[64 * (r >> 5) + (r & 31)])
                                                             : uint32_t(L.perm[T.row0 + T.m0 + r]));
             else
-                src = uint32_t(T.row0 + T.m0 + r);
+                src = uint32_t(r);                      // (down: rows relative to the tile's first row)
             int l = lane;                               // (opaque: the chunk offset is recomputed here too)
             asm volatile("" : "+v"(l));
             ao[i] = src * uint32_t(K * 2) + uint32_t(((l & 3) ^ ring_swz((l >> 2) & 15)) << 4);

@@ -506,8 +506,9 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
         return fail(MSI_E_INVALID_ARG, "null argument");
     const msi_plan_desc &d = p->desc;
     const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model);
-    if (a->n_tokens > (1u << 24))
-        return fail(MSI_E_INVALID_ARG, "n_tokens too large");
+    const std::string lim = batch_limit_error(d, a->n_tokens);
+    if (!lim.empty())
+        return fail(MSI_E_INVALID_ARG, lim);
     if (!routing_ok(a->r) || (T > 0 && (!a->x || !a->w_router)))
         return fail(MSI_E_INVALID_ARG, "null routing or input pointer");
     const Workspace ws = workspace_layout(d, a->n_tokens);
@@ -553,8 +554,9 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
     const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model), I = int(d.d_ff);
     if (a->layer >= d.n_layers)
         return fail(MSI_E_INVALID_ARG, "layer out of range");
-    if (a->n_tokens > (1u << 24))
-        return fail(MSI_E_INVALID_ARG, "n_tokens too large");
+    const std::string lim = batch_limit_error(d, a->n_tokens);
+    if (!lim.empty())
+        return fail(MSI_E_INVALID_ARG, lim);
     if (!routing_ok(a->r) || !a->out || (T > 0 && !a->x))
         return fail(MSI_E_INVALID_ARG, "null routing, input or output pointer");
     const Workspace ws = workspace_layout(d, a->n_tokens);

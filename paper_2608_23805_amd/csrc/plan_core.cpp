@@ -10,6 +10,16 @@
 
 namespace msi {
 
+std::string batch_limit_error(const msi_plan_desc &d, uint64_t n_tokens)
+{
+    if (n_tokens > (uint64_t(1) << 24))
+        return "n_tokens above 2^24";
+    if (d.wdtype != MSI_W_F32 && n_tokens * d.d_model * 2 > uint64_t(0x7fffffff))
+        return "n_tokens * d_model * 2 bytes of hidden states must stay below 2^31 (token rows are addressed "
+               "with 32-bit offsets)";
+    return "";
+}
+
 PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
 {
     auto fail = [&](msi_status st, std::string m) { set_error(st, std::move(m)); };

@@ -63,6 +63,12 @@ struct Schedule {
     std::vector<SchedRound> rounds;
 };
 
+// Batch-size limit of a plan's kernels: "" if T tokens are addressable, else
+// why not.  The tile kernels gather token rows of x through 32-bit byte
+// offsets from the start of x, so T * d_model * (element bytes) must stay
+// below 2^31 for bf16 and 4-bit layers; every layer keeps T <= 2^24.
+std::string batch_limit_error(const msi_plan_desc &d, uint64_t n_tokens);
+
 struct ObjectInfo {
     uint32_t window;
     uint64_t offset, nbytes;

@@ -104,6 +104,35 @@ def check_selection(gpu_idx: np.ndarray, ora: dict, tokens: Sequence[int]):
     return near
 
 
+def check_all_sets(o, li: synth.LayerInputs, gpu_idx: np.ndarray) -> dict:
+    """Routed sets of every token against the oracle's fp64 logits and top-K
+    (the near-tie rule of check_selection).  Returns the counts: tokens,
+    exact matches, accepted near-tie differences, oracle near ties (top-K
+    logit gap < NEAR_TIE), ties within 1e-4, and probability-gap near ties
+    (restricted-softmax weight of the K-th expert within 1e-5 of the next
+    expert's, both over the same normaliser)."""
+    s = li.wl.shape
+    L = o.router_logits(li.x, li.wr, li.bias, s.xdtype)
+    idx, gap = o.select_topk(L, s.K)
+    T = L.shape[0]
+    g = np.sort(gpu_idx, axis=1)
+    same = np.all(g == idx, axis=1)
+    moved = []
+    for t in np.nonzero(~same)[0]:
+        kth = np.sort(L[t])[::-1][s.K - 1]
+        diff = set(g[t].tolist()) ^ set(idx[t].tolist())
+        ok = gap[t] < NEAR_TIE and all(abs(L[t][e] - kth) < NEAR_TIE for e in diff)
+        assert ok, f"token {t}: gpu {g[t]} oracle {idx[t]} gap {gap[t]:.3e}"
+        moved.append(int(t))
+    srt = -np.sort(-L, axis=1)
+    m = srt[:, :1]
+    z = np.exp(srt[:, :s.K] - m).sum(axis=1)
+    pgap = (np.exp(srt[:, s.K - 1] - m[:, 0]) - np.exp(srt[:, s.K] - m[:, 0])) / z
+    return {"tokens": int(T), "exact": int(same.sum()), "near_tie_moved": len(moved), "moved_tokens": moved[:16],
+            "oracle_near_ties_1e-5": int((gap < NEAR_TIE).sum()), "oracle_gaps_below_1e-4": int((gap < 1e-4).sum()),
+            "prob_gap_below_1e-5": int((pgap < 1e-5).sum())}
+
+
 def rel_err(a: np.ndarray, ref: np.ndarray) -> float:
     den = float(np.abs(ref).max())
     return float(np.abs(np.asarray(a, np.float64) - ref).max() / (den if den > 0 else 1.0))
@@ -128,3 +157,16 @@ def oracle_compare(o, li: synth.LayerInputs, res: dict, tokens: Sequence[int], t
     err = rel_err(got, ref)
     assert err <= tol, f"max-abs/max|ref| {err:.3e} > {tol:.1e}"
     return err, near, ora
+
+
+def workspace_parts(T: int, E: int, K: int, d: int, I: int, wdtype: str) -> dict:
+    """Byte offsets of the workspace parts (the layout msi.h documents)."""
+    a256 = lambda v: (v + 255) // 256 * 256  # noqa: E731
+    ab = 4 if wdtype == "f32" else 2
+    off, parts = 0, {}
+    for name, n in (("logits", T * E * 4), ("blockhist", max((T + 255) // 256, 1) * E * 4),
+                    ("act", T * K * I * ab), ("act_s", T * I * ab), ("y", T * K * d * ab), ("ys", T * d * ab)):
+        parts[name] = off
+        off += a256(n)
+    parts["total"] = off
+    return parts

@@ -12,7 +12,8 @@ Sources of truth used here (none of them is the oracle's own code):
 * numpy / scipy library routines for special cases that reduce to them
   (matrix products, ``scipy.special.softmax`` / ``expit``);
 * closed forms and invariants (zero input, power-of-two scaling, relabeling,
-  restricted softmax ratios, weights summing to one).
+  restricted softmax ratios, weights summing to one, unit mean square after
+  the stack's input normalisation).
 """
 from __future__ import annotations
 
@@ -300,9 +301,75 @@ def pin_layer_invariants(o):
     assert np.array_equal(r6["out"], base["out"])
 
 
+# ---------------------------------------------------------------- layer stack (residual stream)
+
+def pin_residual_rows(o):
+    """Hand-derived rows of the residual step (golden fixture)."""
+    with open(os.path.join(GOLDEN, "residual_rows.txt")) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            hs, outs, want = (p.split() for p in line.split("|"))
+            h = np.array([[float(v) for v in hs]])
+            out = None if outs == ["-"] else np.array([[float(v) for v in outs]])
+            hn, x = o.residual_step(h, out)
+            assert [int(b, 16) for b in want] == x[0].tolist(), (line, [hex(v) for v in x[0]])
+            assert np.array_equal(hn, h if out is None else h + out), line
+
+
+def pin_residual_invariants(o):
+    """Normalised rows have unit mean square (up to bf16 rounding); scaling a
+    row by a power of two leaves x unchanged when the epsilon is negligible;
+    the residual stream itself is the plain sum, exact in fp64."""
+    g = np.random.default_rng(21)
+    h = g.standard_normal((16, 512)) * 100.0
+    out = g.standard_normal((16, 512)) * 30.0
+    hn, x = o.residual_step(h, out)
+    assert np.array_equal(hn, h + out)
+    xv = synth.bf16_bits_to_f32(x).astype(np.float64)
+    ms = (xv ** 2).mean(axis=1)
+    assert np.all(np.abs(ms - 1.0) <= 2 * 2.0 ** -8), ms
+    for k in (-4, 3, 10):
+        _, xk = o.residual_step(h * 2.0 ** k, out * 2.0 ** k)
+        assert np.array_equal(xk, x), k
+    # each element is the nearest bf16 of h / rms: within half a bf16 step (2^-8 relative, plus the rms's
+    # own relative error bound from fp64)
+    ref = hn / np.sqrt((hn ** 2).mean(axis=1, keepdims=True))
+    assert np.all(np.abs(xv - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-300)
+
+
+def pin_stack_chain(o):
+    """Two stacked layers equal their steps applied by hand: the second
+    layer's input is the normalised sum of the first layer's input stream
+    and output, and a layer with every routed and shared down projection zero
+    leaves the residual stream unchanged."""
+    s = SMALL_BF16
+    li = _tiny_inputs(s, bias=True)
+    ly = dict(wr=li.wr, bias=li.bias, experts=li.experts, shared=li.shared)
+    h0 = synth.bf16_bits_to_f32(li.x).astype(np.float64) * 3.0
+    r = o.stack(h0, [ly, ly], s.K, s.I, s.wdtype)
+    x0 = o.f64_to_bf16_array(h0 / np.sqrt((h0 ** 2).mean(axis=1, keepdims=True) + 1e-6))
+    assert np.array_equal(r["xs"][0], x0)
+    out0 = o.moe_layer(x0, li.wr, li.bias, li.experts, li.shared, s.K, s.I, s.wdtype, "bf16")["out"]
+    h1 = h0 + out0
+    assert np.array_equal(r["xs"][1], o.f64_to_bf16_array(h1 / np.sqrt((h1 ** 2).mean(axis=1, keepdims=True)
+                                                                         + 1e-6)))
+    out1 = o.moe_layer(r["xs"][1], li.wr, li.bias, li.experts, li.shared, s.K, s.I, s.wdtype, "bf16")["out"]
+    assert np.array_equal(r["h"], h1 + out1)
+    nb = o.matrix_nbytes(s.wdtype, s.I, s.d)
+
+    def no_down(obj):
+        z = np.array(obj, dtype=np.uint8, copy=True)
+        z[2 * nb:] = 0
+        return z
+    quiet = dict(wr=li.wr, bias=li.bias, experts=[no_down(e) for e in li.experts], shared=no_down(li.shared))
+    rq = o.stack(h0, [quiet, quiet, quiet], s.K, s.I, s.wdtype)
+    assert np.array_equal(rq["h"], h0) and np.array_equal(rq["xs"][2], x0)
+
+
 ALL_PINS = [
     pin_formats, pin_bf16_rounding, pin_q4_block, pin_q4_quantizer_bound,
     pin_router_matches_matmul, pin_topk_bruteforce, pin_topk_zero_router, pin_gate_weights,
     pin_permutation, pin_expert_ffn_special, pin_expert_ffn_matmul, pin_layer_dense,
-    pin_layer_invariants,
+    pin_layer_invariants, pin_residual_rows, pin_residual_invariants, pin_stack_chain,
 ]

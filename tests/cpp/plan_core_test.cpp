@@ -218,9 +218,34 @@ static void test_rounds(uint32_t slots, uint32_t transient, size_t ndem)
         CHECK(st.hits == 0);
 }
 
+// Batch limits: 2^24 tokens, and under 2^31 bytes of bf16 / 4-bit hidden
+// states (token rows are addressed with 32-bit offsets); fp32 layers only
+// the token count.
+static void test_batch_limits()
+{
+    Fixture f(1, 4, 2);
+    msi_plan_desc d = f.d;
+    d.d_model = 2048;
+    d.wdtype = MSI_W_BF16;
+    CHECK(batch_limit_error(d, 0).empty());
+    CHECK(batch_limit_error(d, 32768).empty());
+    CHECK(batch_limit_error(d, 524287).empty());           // 524287 * 4096 B = 2^31 - 4096
+    CHECK(!batch_limit_error(d, 524288).empty());          // exactly 2^31 bytes
+    d.wdtype = MSI_W_Q4B32;
+    CHECK(!batch_limit_error(d, 600000).empty());
+    d.wdtype = MSI_W_F32;
+    CHECK(batch_limit_error(d, 600000).empty());
+    CHECK(!batch_limit_error(d, (1u << 24) + 1).empty());
+    d.d_model = 256;
+    d.wdtype = MSI_W_BF16;
+    CHECK(batch_limit_error(d, (1u << 22) - 1).empty());   // 2^31 - 512 bytes
+    CHECK(!batch_limit_error(d, 1u << 22).empty());        // exactly 2^31 bytes
+}
+
 int main()
 {
     test_manifest();
+    test_batch_limits();
     test_fill_hit_lru();
     test_holds();
     test_epoch_reset();

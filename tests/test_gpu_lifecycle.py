@@ -198,3 +198,96 @@ def test_explicit_fill_hit_keeps_generation(li):
     torch.cuda.synchronize()
     balanced(plan)
     plan.close()
+
+
+def _stale_tile_cell(li, capacity, persistent):
+    """Stale generation on an expert of the tiled MFMA path: the forward
+    returns MSI_E_STALE with the output untouched, and neither tile kernel
+    wrote that expert's rows (its act and y rows keep a canary pattern while
+    another tile-path expert's rows are overwritten), so both the gate/up
+    tile check and the down tile check fired.  The next forward refills and
+    is exact."""
+    import torch
+    import paper_2608_23805_amd as msi
+    from _gpu_helpers import workspace_parts
+    s = li.wl.shape
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=capacity)
+    ctrl = run_layer(plan, dl)
+    counts, offsets = ctrl["counts"], ctrl["offsets"]
+    tile = [e for e in range(s.E) if counts[e] > 16]
+    down_tiles = sum((int(counts[e]) + 255) // 256 * (s.d // 256) for e in tile) + (s.T + 255) // 256 * (s.d // 256)
+    log(f"stale tile cell: T={s.T} tile experts={len(tile)} down tiles={down_tiles} persistent={persistent}")
+    assert (down_tiles > 256) == persistent, down_tiles
+    bad, other = tile[0], tile[-1]
+    slot = next(q for q in range(capacity) if plan.query(0, q).expert == bad)
+    plan.debug_set_device_gen(0, slot, plan.query(0, slot).generation + 1000)
+    r = msi.Routing.alloc(s.T, s.K, s.E)
+    ws = plan.workspace(s.T)
+    cs = torch.cuda.current_stream()
+    plan.route(dl.x, dl.wr, dl.bias, r, ws, cs)
+    torch.cuda.synchronize()
+    P = workspace_parts(s.T, s.E, s.K, s.d, s.I, s.wdtype)
+
+    def rows(part, e, width):
+        a = P[part] + int(offsets[e]) * width * 2
+        return ws[a:a + int(counts[e]) * width * 2]
+    for e in (bad, other):
+        rows("act", e, s.I).fill_(0x5A)
+        rows("y", e, s.d).fill_(0x5A)
+    canary = torch.full((s.T, s.d), 6.25, device="cuda")
+    st = plan.forward_status(0, dl.x, r, dl.shared, canary, ws, cs, torch.cuda.Stream())
+    torch.cuda.synchronize()
+    assert st == msi.MSI_E_STALE, st
+    assert torch.all(canary == 6.25), "output written despite a stale slot"
+    assert torch.all(rows("act", bad, s.I) == 0x5A), "gate/up tiles wrote rows of a stale slot"
+    assert torch.all(rows("y", bad, s.d) == 0x5A), "down tiles wrote rows of a stale slot"
+    assert not torch.all(rows("act", other, s.I) == 0x5A) and not torch.all(rows("y", other, s.d) == 0x5A)
+    st = balanced(plan)
+    assert st["stale_detected"] == 1
+    again = run_layer(plan, dl)
+    assert again["out"].cpu().numpy().tobytes() == ctrl["out"].cpu().numpy().tobytes()
+    balanced(plan)
+    plan.close()
+
+
+def test_stale_generation_tile_path():
+    """Tile path, down launch under one tile per CU (non-persistent kernel)."""
+    log("cell stale_generation_tile")
+    wl = synth.Workload("cells_tile_bf16", 19, synth.LayerShape(300, 512, 32, 4, 256, "bf16"),
+                        prior="dirichlet", prior_param=0.5, tau=0.6)
+    _stale_tile_cell(synth.layer_inputs(wl), capacity=32, persistent=False)
+
+
+def test_stale_generation_persistent_down():
+    """Prefill-shaped layer whose down launch exceeds one tile per CU, so the
+    persistent down kernel runs (T = 2048, d = 2048, E = 16, K = 4)."""
+    log("cell stale_generation_persistent")
+    wl = synth.Workload("cells_persistent_bf16", 20, synth.LayerShape(2048, 2048, 16, 4, 512, "bf16"),
+                        prior="dirichlet", prior_param=2.0, tau=0.2)
+    _stale_tile_cell(synth.layer_inputs(wl), capacity=16, persistent=True)
+
+
+def test_batch_limit_rejected():
+    """A batch whose hidden states reach 2^31 bytes is rejected before any
+    device work (the tile kernels address token rows with 32-bit offsets)."""
+    import ctypes
+    import torch
+    import paper_2608_23805_amd as msi
+    log("cell batch_limit")
+    s = WL.shape
+    li = synth.layer_inputs(WL)
+    plan = make_plan(li, capacity=12, per_window=4)
+    T = (1 << 31) // (s.d * 2)
+    r = msi.Routing.alloc(1, s.K, s.E)
+    ws = torch.empty(256, dtype=torch.uint8, device="cuda")
+    dummy = torch.empty(16, dtype=torch.int16, device="cuda")
+    a = msi.msi_route_args(n_tokens=T, reserved=0, x=dummy.data_ptr(), w_router=dummy.data_ptr(), bias=None,
+                           r=r.c(), workspace=ws.data_ptr(), workspace_bytes=ws.numel())
+    assert msi.lib.msi_route(plan.h, ctypes.byref(a), None) == msi.MSI_E_INVALID_ARG
+    assert "2^31" in msi.last_error()
+    f = msi.msi_forward_args(layer=0, n_tokens=T, x=dummy.data_ptr(), r=r.c(), shared_object=None,
+                             out=dummy.data_ptr(), workspace=ws.data_ptr(), workspace_bytes=ws.numel())
+    assert msi.lib.msi_moe_forward(plan.h, ctypes.byref(f), None, None) == msi.MSI_E_INVALID_ARG
+    balanced(plan)
+    plan.close()

@@ -1,7 +1,7 @@
 """GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
 
 Bars: selected sets bit-exact except reported near-ties (oracle logit gap
-< 1e-5); max-abs / max|ref| <= 1e-5 for fp32 layers and <= 1e-2 for bf16
+< 1e-5), for every token also at T = 32768; max-abs / max|ref| <= 1e-5 for fp32 layers and <= 1e-2 for bf16
 layers; permutation arrays bit-exact against the oracle's counting sort of
 the GPU's own selection; outputs byte-identical across slot capacities.
 """
@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import synth
-from _gpu_helpers import (device_layer, log, make_plan, oracle_compare, rel_err, run_layer)
+from _gpu_helpers import (check_all_sets, device_layer, log, make_plan, oracle_compare, rel_err, run_layer)
 
 pytestmark = pytest.mark.gpu
 
@@ -194,7 +194,7 @@ def test_decode_full_parity_and_capacities(o, dec):
     assert outs[0].tobytes() == outs[512].tobytes()
 
 
-# ------------------------------------------------------------------ full-size prefill (sampled)
+# ------------------------------------------------------------------ full-size prefill (all routed sets, sampled outputs)
 
 PRE = synth.WORKLOADS["prefill_bf16"]
 
@@ -209,13 +209,18 @@ def test_prefill_full_sampled(o):
     log(f"prefill counts min={counts.min()} max={counts.max()} zero={(counts == 0).sum()}")
     _check_permutation(o, res, PRE.shape.E)
     assert np.all(np.abs(res["w"].sum(axis=1) - 1.0) <= 1e-6)
-    # oracle on a sample: first/last tokens, tokens of the rarest and busiest experts
+    # routed sets of all 32768 tokens against the oracle's selection
+    sets = check_all_sets(o, li, res["idx"])
+    log(f"prefill routed sets: {sets}")
+    # outputs on a sample: first/last tokens, tokens of the rarest and busiest experts, every token whose
+    # set moved on a near tie (the oracle recomputes those with the GPU's set)
     g = np.random.default_rng(7)
     rare = int(np.argmin(np.where(counts > 0, counts, 1 << 30)))
     busy = int(np.argmax(counts))
-    toks = sorted(set([0, 1, PRE.shape.T - 1] + g.choice(PRE.shape.T, 40, replace=False).tolist()
-                      + res["perm"][res["offsets"][rare]:res["offsets"][rare] + 4].tolist()
-                      + res["perm"][res["offsets"][busy]:res["offsets"][busy] + 4].tolist()))
+    toks = sorted(set([0, 1, PRE.shape.T - 1] + g.choice(PRE.shape.T, 96, replace=False).tolist()
+                      + res["perm"][res["offsets"][rare]:res["offsets"][rare] + 8].tolist()
+                      + res["perm"][res["offsets"][busy]:res["offsets"][busy] + 8].tolist()
+                      + sets["moved_tokens"]))
     err, near, ora = oracle_compare(o, li, res, toks, TOL_BF16)
     log(f"prefill sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
     _check_weights(res, ora, toks)
@@ -282,10 +287,13 @@ def test_prefill_q4_full_sampled(o):
     counts = res["counts"]
     log(f"prefill_q4 counts min={counts.min()} max={counts.max()} zero={(counts == 0).sum()}")
     _check_permutation(o, res, wl.shape.E)
+    sets = check_all_sets(o, li, res["idx"])
+    log(f"prefill_q4 routed sets: {sets}")
     g = np.random.default_rng(8)
     busy = int(np.argmax(counts))
-    toks = sorted(set([0, wl.shape.T - 1] + g.choice(wl.shape.T, 30, replace=False).tolist()
-                      + res["perm"][res["offsets"][busy]:res["offsets"][busy] + 4].tolist()))
+    toks = sorted(set([0, wl.shape.T - 1] + g.choice(wl.shape.T, 64, replace=False).tolist()
+                      + res["perm"][res["offsets"][busy]:res["offsets"][busy] + 8].tolist()
+                      + sets["moved_tokens"]))
     err, near, _ = oracle_compare(o, li, res, toks, TOL_BF16)
     log(f"prefill_q4 sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
     plan.close()

@@ -1,7 +1,8 @@
 """Each planted mistake in the oracle (compiled with -DMSIO_MUTANT=n) must be
 caught by at least one pin.  The mistakes cover the bias term, the tie-break
 direction, the renormalisation, the SiLU sign, the gate/up operand, the shared
-expert, the 4-bit nibble order and the stability of the permutation."""
+expert, the 4-bit nibble order, the stability of the permutation and the
+three parts of the layer stack's residual step (epsilon, mean, residual add)."""
 import os
 
 import pytest
@@ -18,6 +19,9 @@ MUTANTS = {
     6: "shared expert dropped",
     8: "nibble order swapped",
     9: "permutation walks tokens in reverse",
+    10: "stack normalisation without its epsilon",
+    11: "stack normalisation by the sum of squares instead of the mean",
+    12: "stack residual add dropped",
 }
 
 
