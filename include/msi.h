@@ -296,6 +296,25 @@ msi_status msi_route(msi_plan *plan, const msi_route_args *args, void *stream);
 msi_status msi_moe_forward(msi_plan *plan, const msi_forward_args *args,
                            void *compute_stream, void *side_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * forward as msi_moe_forward, with the same result, but its act / y scratch
+ * (the workspace parts after the histograms, see msi_workspace_size) is a
+ * static device array of the library, MSI_NOALLOC_SCRATCH_BYTES per device,
+ * held from the library's load until the process ends.  args->workspace must
+ * be NULL and args->workspace_bytes 0.  It calls no hipMalloc / hipFree and
+ * no allocating library routine.  Every call on one device shares that
+ * device's array and leaves its contents behind (nothing in it needs to
+ * start zeroed: a forward writes every row it reads), so calls that overlap
+ * on one device race: order them on one stream or serialise them.  Errors:
+ * those of msi_moe_forward; MSI_E_INVALID_ARG when T tokens need more than
+ * MSI_NOALLOC_SCRATCH_BYTES (T * (K + 1) * (d_ff + d_model) * 2 bytes plus
+ * alignment for bf16 / 4-bit layers: about 1,190 tokens at d_model 2048,
+ * d_ff 512, K 10) or a workspace is passed. */
+#define MSI_NOALLOC_SCRATCH_BYTES (64u << 20)
+msi_status msi_moe_forward_noalloc(msi_plan *plan, const msi_forward_args *args, void *compute_stream,
+                                   void *side_stream);
+
 /* Hold / release one external consumer on a slot (a consumer ticket that
  * outlives a forward; a held slot is never chosen as a victim and cannot be
  * refilled).  MSI_E_STATE when unholding a slot with no holds. */

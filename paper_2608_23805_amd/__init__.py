@@ -31,6 +31,7 @@ STATUS_NAMES = {0: "MSI_OK", -1: "MSI_E_INVALID_ARG", -2: "MSI_E_SHORT", -3: "MS
                 -8: "MSI_E_STATE"}
 
 MSI_W_F32, MSI_W_BF16, MSI_W_Q4B32 = 0, 1, 2
+MSI_NOALLOC_SCRATCH_BYTES = 64 << 20
 WDTYPE = {"f32": MSI_W_F32, "bf16": MSI_W_BF16, "q4b32": MSI_W_Q4B32}
 SLOT_STATES = {0: "Vacant", 1: "Loading", 2: "DeviceReady", 3: "InUse", 4: "Recyclable"}
 
@@ -95,6 +96,7 @@ EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_
            "msi_plan_timings", "msi_last_error", "msi_abi_version", "msi_plan_create", "msi_plan_destroy",
            "msi_plan_reset",
            "msi_workspace_size", "msi_slot_fill", "msi_plan_poll", "msi_route", "msi_moe_forward",
+           "msi_moe_forward_noalloc",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
            "msi_debug_set_device_gen", "msi_stream_threshold"]
 
@@ -120,6 +122,7 @@ def _load():
     L.msi_plan_poll.argtypes = [_vp]
     L.msi_route.argtypes = [_vp, P(msi_route_args), _vp]
     L.msi_moe_forward.argtypes = [_vp, P(msi_forward_args), _vp, _vp]
+    L.msi_moe_forward_noalloc.argtypes = [_vp, P(msi_forward_args), _vp, _vp]
     L.msi_slot_hold.argtypes = [_vp, _u32, _u32]
     L.msi_slot_unhold.argtypes = [_vp, _u32, _u32]
     L.msi_slot_query.argtypes = [_vp, _u32, _u32, P(msi_slot_info)]
@@ -318,6 +321,14 @@ class Plan:
                              shared_object=_ptr(shared), out=_ptr(out), workspace=_ptr(workspace),
                              workspace_bytes=workspace.numel())
         return int(lib.msi_moe_forward(self.h, ctypes.byref(a), _stream(compute_stream), _stream(side_stream)))
+
+    def forward_noalloc_status(self, layer: int, x, routing: Routing, shared, out, compute_stream=None,
+                               side_stream=None) -> int:
+        """msi_moe_forward_noalloc: the library's static scratch instead of a workspace."""
+        a = msi_forward_args(layer=layer, n_tokens=x.shape[0], x=_ptr(x), r=routing.c(),
+                             shared_object=_ptr(shared), out=_ptr(out), workspace=None, workspace_bytes=0)
+        return int(lib.msi_moe_forward_noalloc(self.h, ctypes.byref(a), _stream(compute_stream),
+                                               _stream(side_stream)))
 
     def forward(self, layer: int, x, routing: Routing, shared, out, workspace, compute_stream=None,
                 side_stream=None):

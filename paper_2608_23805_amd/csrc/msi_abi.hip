@@ -10,8 +10,10 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/msi.h"
@@ -82,6 +84,43 @@ Workspace workspace_layout(const msi_plan_desc &d, uint64_t T)
     return w;
 }
 
+// act / y scratch of one forward (device pointers)
+struct FwdBufs {
+    uint8_t *act, *act_s, *y, *ys;
+};
+
+}  // namespace
+
+// Scratch of msi_moe_forward_noalloc: the act and y parts of a forward's
+// workspace live here, so that entry point needs no allocation.  Each device
+// the library runs on holds its own copy for the life of the process; host
+// code uses only the per-device address from scratch_address(), never the
+// array's name (which in host code is a stand-in, not a device address).
+static __device__ __align__(256) uint8_t scratch[MSI_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on `device`, looked up once per device with
+// that device current (at plan creation).
+hipError_t scratch_address(int device, void **out)
+{
+    static std::mutex mu;
+    static std::unordered_map<int, void *> addr;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = addr.find(device);
+    if (it != addr.end()) {
+        *out = it->second;
+        return hipSuccess;
+    }
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess)
+        return e;
+    addr.emplace(device, ptr);
+    *out = ptr;
+    return hipSuccess;
+}
+
 }  // namespace
 
 struct msi_plan {
@@ -90,6 +129,7 @@ struct msi_plan {
     uint64_t object_bytes = 0;
     PlanCore *core = nullptr;
     int device = 0;
+    void *scratch = nullptr;            // this device's copy of the static scratch (msi_moe_forward_noalloc)
     uint32_t *gen_dev = nullptr;        // [n_layers * pool_slots]
     uint32_t *status_dev = nullptr;     // [status, counts copy [E]] (device work-list path)
     WorkItem *table_dev = nullptr;
@@ -365,6 +405,8 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         return cleanup(MSI_E_DEVICE, "no HIP device");
     if (init_kernel_attributes() != hipSuccess)
         return cleanup(MSI_E_DEVICE, "hipFuncSetAttribute failed");
+    if (scratch_address(p->device, &p->scratch) != hipSuccess)
+        return cleanup(MSI_E_DEVICE, "hipGetSymbolAddress of the static scratch failed");
     const size_t E = desc->n_experts, NL = desc->n_layers;
     p->res_version.assign(NL, 0);
     p->direct_ok.assign(NL, 0);
@@ -545,27 +587,33 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
     return MSI_OK;
 }
 
-msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute_stream, void *side_stream)
+// Argument checks shared by both forward entry points (before any device work).
+static msi_status forward_check(const msi_plan *p, const msi_forward_args *a)
 {
     if (!p || !a)
         return fail(MSI_E_INVALID_ARG, "null argument");
     const msi_plan_desc &d = p->desc;
-    PlanCore &core = *p->core;
-    const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model), I = int(d.d_ff);
     if (a->layer >= d.n_layers)
         return fail(MSI_E_INVALID_ARG, "layer out of range");
     const std::string lim = batch_limit_error(d, a->n_tokens);
     if (!lim.empty())
         return fail(MSI_E_INVALID_ARG, lim);
-    if (!routing_ok(a->r) || !a->out || (T > 0 && !a->x))
+    if (!routing_ok(a->r) || !a->out || (a->n_tokens > 0 && !a->x))
         return fail(MSI_E_INVALID_ARG, "null routing, input or output pointer");
-    const Workspace ws = workspace_layout(d, a->n_tokens);
-    if (!a->workspace || a->workspace_bytes < ws.total)
-        return fail(MSI_E_NOMEM, "workspace smaller than msi_workspace_size");
+    return MSI_OK;
+}
+
+// The forward itself; B holds the act / y scratch of T tokens (from the
+// caller's workspace or the library's static scratch).
+static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const FwdBufs &B, void *compute_stream,
+                               void *side_stream)
+{
+    const msi_plan_desc &d = p->desc;
+    PlanCore &core = *p->core;
+    const int T = int(a->n_tokens), E = int(d.n_experts), K = int(d.top_k), D = int(d.d_model), I = int(d.d_ff);
     HIP_OK(hipSetDevice(p->device));
     hipStream_t cs = static_cast<hipStream_t>(compute_stream);
     hipStream_t side = static_cast<hipStream_t>(side_stream);
-    uint8_t *wsb = static_cast<uint8_t *>(a->workspace);
     poll_fills(p);
 
     // ---- layer entry, device work list: when the layer's last forward needed
@@ -601,12 +649,12 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         X.wstride = d.slot_stride;
         X.gen_dev = p->gen_dev;
         X.status = p->status_dev;
-        X.act = wsb + ws.act;
-        X.y = wsb + ws.y;
+        X.act = B.act;
+        X.y = B.y;
         X.row_weight = a->r.row_weight;
         X.shared_w = static_cast<const uint8_t *>(a->shared_object);
-        X.act_s = wsb + ws.act_s;
-        X.ys = wsb + ws.ys;
+        X.act_s = B.act_s;
+        X.ys = B.ys;
         X.d = D;
         X.I = I;
         X.direct = DirectList{a->r.demand, p->res_slot_dev + size_t(L0) * E, p->res_gen_dev + size_t(L0) * E,
@@ -620,7 +668,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
                                [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
         const CombinePublish pub{p->status_dev, p->arrive_dev + ARRIVE_COMBINE, p->tail_hdev, a->r.demand};
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
-            return launch_combine(wsb + ws.y, has_sh ? wsb + ws.ys : nullptr, false, a->r.inv, a->out, pub, T, K,
+            return launch_combine(B.y, has_sh ? B.ys : nullptr, false, a->r.inv, a->out, pub, T, K,
                                   D, cs);
         }));
         p->status_clean = true;
@@ -790,12 +838,12 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
             L.perm = a->r.perm;
             L.wbase = static_cast<const uint8_t *>(d.slot_pool);
             L.wstride = d.slot_stride;
-            L.act = wsb + ws.act;
-            L.y = wsb + ws.y;
+            L.act = B.act;
+            L.y = B.y;
             L.row_weight = a->r.row_weight;
             L.shared_w = static_cast<const uint8_t *>(a->shared_object);
-            L.act_s = wsb + ws.act_s;
-            L.ys = wsb + ws.ys;
+            L.act_s = B.act_s;
+            L.ys = B.ys;
             static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
                                              MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32,
                                              MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_DOWN_TILE,
@@ -840,7 +888,7 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         // no arrival counter: one counter update per workgroup of a large grid costs more than the clear
         const CombinePublish pub{p->status_dev, nullptr, p->status_hdev, nullptr};
         if (p->timed_launch(MSI_K_COMBINE, cs, [&] {
-                return launch_combine(wsb + ws.y, has_shared ? wsb + ws.ys : nullptr, f32w, a->r.inv,
+                return launch_combine(B.y, has_shared ? B.ys : nullptr, f32w, a->r.inv,
                                       a->out, pub, T, K, D, cs);
             }) != hipSuccess)
             rst = fail(MSI_E_DEVICE, "combine launch failed");
@@ -885,6 +933,41 @@ msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute
         return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
     }
     return MSI_OK;
+}
+
+msi_status msi_moe_forward(msi_plan *p, const msi_forward_args *a, void *compute_stream, void *side_stream)
+{
+    const msi_status st = forward_check(p, a);
+    if (st != MSI_OK)
+        return st;
+    const Workspace ws = workspace_layout(p->desc, a->n_tokens);
+    if (!a->workspace || a->workspace_bytes < ws.total)
+        return fail(MSI_E_NOMEM, "workspace smaller than msi_workspace_size");
+    uint8_t *w = static_cast<uint8_t *>(a->workspace);
+    return forward_impl(p, a, FwdBufs{w + ws.act, w + ws.act_s, w + ws.y, w + ws.ys}, compute_stream, side_stream);
+}
+
+msi_status msi_moe_forward_noalloc(msi_plan *p, const msi_forward_args *a, void *compute_stream, void *side_stream)
+{
+    const msi_status st = forward_check(p, a);
+    if (st != MSI_OK)
+        return st;
+    if (a->workspace || a->workspace_bytes)
+        return fail(MSI_E_INVALID_ARG, "msi_moe_forward_noalloc takes no workspace (workspace must be NULL and "
+                                       "workspace_bytes 0)");
+    const Workspace ws = workspace_layout(p->desc, a->n_tokens);
+    const uint64_t need = ws.total - ws.act;     // act, shared act, y, shared y
+    if (need > MSI_NOALLOC_SCRATCH_BYTES)
+        return fail(MSI_E_INVALID_ARG, "forward of " + std::to_string(a->n_tokens) + " tokens needs " +
+                                           std::to_string(need) + " bytes of scratch, above the " +
+                                           std::to_string(uint64_t(MSI_NOALLOC_SCRATCH_BYTES)) +
+                                           " bytes of msi_moe_forward_noalloc");
+    uint8_t *base = static_cast<uint8_t *>(p->scratch);
+    if (!base)
+        return fail(MSI_E_DEVICE, "static scratch address unknown for this device");
+    return forward_impl(p, a,
+                        FwdBufs{base, base + (ws.act_s - ws.act), base + (ws.y - ws.act), base + (ws.ys - ws.act)},
+                        compute_stream, side_stream);
 }
 
 msi_status msi_slot_hold(msi_plan *p, uint32_t layer, uint32_t slot)
