@@ -273,6 +273,101 @@ def bench_stack(args, cs, side):
     return res
 
 
+def bench_source_df(args, cs, side, pool=None):
+    """The paper's matched source experiment on synthetic canonical files:
+    a fixed decode workload (T = 16, fresh hidden states per step, E = 512,
+    LRU64 per layer over several layers, each with its own router and bias)
+    whose expert objects are read from one canonical file of 512
+    Qwen3-Next-shaped objects (gate, up, down as three unaligned extents
+    each), once with the blocking arm D (one staging window, one read in
+    flight) and once with the asynchronous arm F (eight windows, eight reads
+    in flight), in pairs of both orders.  Both arms must produce
+    byte-identical outputs; reported: complete wall per arm, the F/D wall
+    ratio, the time forwards waited on the source, reads and bytes."""
+    import numpy as np
+    import torch
+    import synth
+    import paper_2608_23805_amd as msi
+    from _gpu_helpers import to_device
+    wl = synth.WORKLOADS["stack_bf16"]
+    s = wl.shape
+    L, steps, T = args.df_layers, args.df_steps, 16
+    t0 = time.time()
+    if pool is None:
+        pool = synth.layer_inputs(wl, layer=0)
+    tmpdir = os.environ.get("TMPDIR", "/tmp")
+    path = os.path.join(tmpdir, f"msi_canonical_{os.getpid()}.bin")
+    comps = synth.component_sizes(s)
+    ext = synth.write_canonical_file(path, [pool.expert(e) for e in range(s.E)], comps, seed=1)
+    loc = {}
+    for (i, c, off, n) in ext:
+        loc.setdefault(i, []).append((c, off, n))
+    extents = []
+    for l in range(L):
+        m = synth.stack_expert_map(wl, l)
+        for e in range(s.E):
+            extents += [(l, e, c, 0, off, n) for (c, off, n) in loc[int(m[e])]]
+    wbytes = (s.object_bytes() + 3 * 8192 + 4095) // 4096 * 4096
+    wr = [to_device(synth.router_weight(wl, l), s.xdtype) for l in range(L)]
+    bias = [torch.from_numpy(synth.router_bias(wl, l)).cuda() for l in range(L)]
+    shared = [torch.from_numpy(synth.expert_object(wl, l, 0, shared=True)).cuda() for l in range(L)]
+    xs = [to_device(synth.hidden_states(wl, 0, 100 + st, T), s.xdtype) for st in range(steps)]
+    log(f"[bench] source D/F: canonical file {os.path.getsize(path) / 2**30:.2f} GiB, {L} layers x {steps} "
+        f"decode steps, set up in {time.time() - t0:.1f}s")
+
+    def arm(n_windows, inflight):
+        src = msi.Source([path], extents, n_windows=n_windows, window_bytes=wbytes, inflight=inflight)
+        plan = msi.Plan(n_layers=L, n_experts=s.E, d_model=s.d, d_ff=s.I, top_k=s.K, wdtype=s.wdtype,
+                        slots_per_layer=64, windows=[], objects=[], source=src)
+        r = msi.Routing.alloc(T, s.K, s.E)
+        ws = plan.workspace(T)
+        out = torch.empty((T, s.d), dtype=torch.float32, device="cuda")
+        outs = []
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for st in range(steps):
+            for l in range(L):
+                plan.route(xs[st], wr[l], bias[l], r, ws, cs)
+                plan.forward(l, xs[st], r, shared[l], out, ws, cs, side)
+                outs.append(out.cpu().numpy().tobytes())
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t1
+        stt, ss = plan.stats(), plan.source_stats()
+        plan.close()
+        return wall, outs, stt, ss
+
+    pairs = []
+    try:
+        for order in ("DF", "FD")[:args.df_pairs]:
+            res = {}
+            for a in order:
+                res[a] = arm(1, 1) if a == "D" else arm(8, 8)
+                log(f"[bench] source arm {a}: {res[a][0]:.2f} s, fills {res[a][2]['fills']}, "
+                    f"waited {res[a][3]['wait_seconds']:.2f} s, peak depth {res[a][3]['peak_depth']}")
+            assert res["D"][1] == res["F"][1], "D and F outputs differ"
+            pairs.append((order, res["D"], res["F"]))
+    finally:
+        os.remove(path)
+    d_w = [p[1][0] for p in pairs]
+    f_w = [p[2][0] for p in pairs]
+    ratio = float(np.exp(np.mean(np.log(np.array(f_w) / np.array(d_w)))))
+    ss_f, ss_d, st_f = pairs[0][2][3], pairs[0][1][3], pairs[0][2][2]
+    res = {"workload": f"decode T={T}, {L} layers x {steps} steps, LRU64 per layer, E=512, canonical file of "
+                       f"512 objects x 3 extents", "pairs": [{"order": o, "D_s": round(d[0], 3), "F_s": round(f[0], 3),
+                                                              "F_over_D": round(f[0] / d[0], 4)}
+                                                             for o, d, f in pairs],
+           "F_over_D_geomean": round(ratio, 4), "D_over_F": round(1 / ratio, 3),
+           "outputs_identical": True, "fills_per_arm": st_f["fills"],
+           "F_wait_s": round(ss_f["wait_seconds"], 3), "D_wait_s": round(ss_d["wait_seconds"], 3),
+           "F_peak_depth": ss_f["peak_depth"], "D_peak_depth": ss_d["peak_depth"],
+           "reads_per_arm": ss_f["reads_issued"], "logical_GB": round(ss_f["logical_bytes"] / 1e9, 2),
+           "physical_GB": round(ss_f["physical_bytes"] / 1e9, 2),
+           "F_read_GBs": round(ss_f["physical_bytes"] / min(f_w) / 1e9, 2),
+           "direct_io": bool(ss_f["direct_files"]), "windows_free_at_end": True}
+    log(f"[bench] source D/F: F/D wall {ratio:.3f} ({1 / ratio:.2f}x), D {d_w} s, F {f_w} s")
+    return res
+
+
 def kernel_sources_sha256(sources=None):
     import hashlib
     h = hashlib.sha256()
@@ -366,7 +461,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--telemetry", default="on", choices=["on", "off"],
                     help="HIP-event timing around each launch inside the decode timed region")
-    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4,stack")
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4,stack,source")
+    ap.add_argument("--df-layers", type=int, default=2, help="source D/F experiment: layers")
+    ap.add_argument("--df-steps", type=int, default=6, help="source D/F experiment: decode steps")
+    ap.add_argument("--df-pairs", type=int, default=2, help="source D/F experiment: pairs (1 or 2)")
+    ap.add_argument("--only-source", action="store_true", help="run only the source D/F experiment")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB copy kernel (hardware-counter scale) and exit")
     args = ap.parse_args()
@@ -383,6 +482,9 @@ def main():
     cs = torch.cuda.current_stream()
     side = torch.cuda.Stream()
 
+    if args.only_source:
+        print(json.dumps({"source_df": bench_source_df(args, cs, side)}), flush=True)
+        return
     if "decode" in skip:            # profiling aid: the prefill workloads only
         res = {}
         if "prefill" not in skip:
@@ -404,6 +506,8 @@ def main():
         extra["decode_q4"] = bench_decode_q4(args, cs, side)
     if "stack" not in skip:
         extra["stack"] = bench_stack(args, cs, side)
+    if "source" not in skip:
+        extra["source_df"] = bench_source_df(args, cs, side)
     pidx = extra["prefill"].pop("_routed_idx") if "prefill" in extra else None
     if "prefill_q4" in extra:
         extra["prefill_q4"].pop("_routed_idx")

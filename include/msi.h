@@ -9,18 +9,21 @@
  * copy with a generation, and the compute kernels check the generation of
  * each slot they read, failing closed on a mismatch.
  *
- * The plan abstraction follows the paper's Section 3 (Design): an immutable
- * manifest of objects, extents, windows and slots with stable addresses
- * (Section 3.1), slot generations and bundle publication (Section 3.3), the
- * separate window / GPU-slot state machines with tickets, epochs and consumer
- * counts (Section 3.4, state sequences), replacement policy kept apart from
- * the lifecycle (Section 3.1), and the scheduling loop of Section 4 ("Scheduling
- * and copies": layer entry requests the bundle, misses are copied into
- * reserved slots, a device event publishes readiness, layer exit releases the
- * consumer ticket).  The lifetime obligations of Table 2 (row L) are the error
- * behaviour below.  The MoE arithmetic itself is the layer every selected
- * expert executes in the paper's principal experiment (Section 5.4: the stock
- * router, then the complete gate, up and down projections).
+ * The plan abstraction follows the paper's Design section: an immutable
+ * manifest of objects, extents, windows and slots with stable addresses, and
+ * replacement policy kept apart from the lifecycle ("A Shared Cross-Adapter
+ * Plan Core"); slot generations and bundle publication ("Stable Slots and
+ * Bundle Publication"); the separate window / GPU-slot state machines with
+ * tickets, epochs and consumer counts ("Separate Window and GPU-Slot
+ * Lifecycles"); and the scheduling loop of the Implementation section
+ * ("Scheduling and copies": layer entry requests the bundle, misses are
+ * copied into reserved slots, a device event publishes readiness, layer exit
+ * releases the consumer ticket).  The lifetime row (L) of the paper's table
+ * of certificate obligations is the error behaviour below.  The MoE
+ * arithmetic itself is the layer every selected expert executes in the
+ * paper's principal experiment ("Output-Exact Execution Beyond the
+ * Full-Residency Envelope": the stock router, then the complete gate, up and
+ * down projections).
  *
  * Conventions
  *  - Every call returns msi_status (0 = MSI_OK, negative = error).  The text
@@ -56,7 +59,7 @@
 extern "C" {
 #endif
 
-#define MSI_ABI_VERSION 2u
+#define MSI_ABI_VERSION 3u
 
 typedef int32_t msi_status;
 
@@ -69,6 +72,7 @@ typedef int32_t msi_status;
 #define MSI_E_DEVICE (-6)       /* HIP runtime error                                  */
 #define MSI_E_NOMEM (-7)        /* workspace too small or host allocation failed      */
 #define MSI_E_STATE (-8)        /* lifecycle transition not allowed in this state     */
+#define MSI_E_IO (-9)           /* a source read completed with a negative status (EIO...) */
 
 typedef enum { MSI_W_F32 = 0, MSI_W_BF16 = 1, MSI_W_Q4B32 = 2 } msi_wdtype;
 
@@ -85,7 +89,34 @@ typedef struct {
     uint64_t nbytes;
 } msi_object_desc;
 
-/* Immutable manifest (Section 3.1).  Slot s (0 <= s < pool_slots) of layer l
+/* Canonical source of expert objects (the bounded source service of the
+ * Design section, "Bounded Source Service"): one extent of one object in a
+ * canonical file.  An object is the concatenation of its extents in
+ * component order (e.g. three components: Wg, Wu, Wd, read and checked
+ * separately and published together as one bundle). */
+typedef struct {
+    uint32_t layer;
+    uint32_t expert;
+    uint32_t component;          /* 0, 1, ... without gaps, at most 4 per object */
+    uint32_t file;               /* index into msi_source_desc.files             */
+    uint64_t offset;             /* byte offset of the extent in the file        */
+    uint64_t nbytes;             /* logical bytes                                */
+} msi_extent_desc;
+
+#define MSI_SOURCE_BUFFERED_OK 1u   /* read through the page cache where direct I/O is refused */
+
+typedef struct {
+    const char *const *files;    /* canonical files, read only                   */
+    uint32_t n_files;
+    uint32_t inflight;           /* reads in flight at most, 1..8                */
+    uint32_t flags;              /* MSI_SOURCE_*                                 */
+    uint32_t align;              /* direct-I/O block, power of two (0 -> 4096)   */
+    const msi_extent_desc *extents;
+    uint32_t n_extents;
+    uint32_t reserved;
+} msi_source_desc;
+
+/* Immutable manifest ("A Shared Cross-Adapter Plan Core").  Slot s (0 <= s < pool_slots) of layer l
  * lives at slot_pool + (l * pool_slots + s) * slot_stride for the life of the
  * plan, where pool_slots = slots_per_layer, or transient_slots when
  * slots_per_layer == 0 (zero-cache: every use refills, nothing is retained
@@ -110,9 +141,17 @@ typedef struct {
     uint32_t n_objects;
     uint64_t window_bytes;       /* size of every window                      */
     const msi_object_desc *objects;
+    /* NULL: every object lives in a window (objects[]).  Otherwise objects
+     * are read from canonical files (source->extents, n_objects must be 0)
+     * and the windows are the source's staging windows: n_windows buffers of
+     * window_bytes (a multiple of source->align) aligned to source->align,
+     * each holding one object's covering reads while it is read and then
+     * copied to its slot (states Free -> Reading -> HostReady -> Copying ->
+     * Free), so the source holds at most n_windows * window_bytes. */
+    const msi_source_desc *source;
 } msi_plan_desc;
 
-/* Ticket of a fill (Section 3.4: tickets carry object, generation, epoch and
+/* Ticket of a fill ("Separate Window and GPU-Slot Lifecycles": tickets carry object, generation, epoch and
  * resource identity). */
 typedef struct {
     uint32_t layer;
@@ -223,21 +262,30 @@ const char *msi_last_error(void);
 uint32_t msi_abi_version(void);
 
 /* Validate the manifest and create a plan on the current HIP device
- * (Section 3.1; stable addresses, Section 3.3; extent rejection conditions,
- * Section 3.2).  Errors: MSI_E_INVALID_ARG (shape, alignment, pool too small,
+ * ("A Shared Cross-Adapter Plan Core"; stable addresses, "Stable Slots and
+ * Bundle Publication"; extent rejection conditions, "Bounded Source
+ * Service").  Errors: MSI_E_INVALID_ARG (shape, alignment, pool too small,
  * duplicate (layer, expert), window index out of range), MSI_E_SHORT (extent
  * past its window, or nbytes != object size for wdtype and shape),
- * MSI_E_DEVICE.  All slots start Vacant with generation 0, epoch 0. */
+ * MSI_E_DEVICE.  With a source: MSI_E_INVALID_ARG (a file that cannot be
+ * opened, component gaps or duplicates, misaligned or too small windows,
+ * in-flight limit outside 1..8), MSI_E_SHORT (an extent past its file's end,
+ * or an object whose extents do not add up to the object size).  All slots
+ * start Vacant with generation 0, epoch 0. */
 msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out);
 
-/* Drain in-flight fills and free plan-owned memory.  MSI_E_BUSY (plan kept)
+/* Drain in-flight fills (and every submitted source read) and free
+ * plan-owned memory.  MSI_E_BUSY (plan kept)
  * if a consumer is still held through msi_slot_hold (shutdown with a live
- * consumer, Section 3.4 / Table 5). */
+ * consumer: "Separate Window and GPU-Slot Lifecycles" and the fault-mode
+ * table of "Integrated Deterministic Faults"). */
 msi_status msi_plan_destroy(msi_plan *plan);
 
-/* Advance the request epoch (Section 3.4).  Fills still in flight become
- * unpublishable: their completion leaves the slot Vacant.  Resident
- * DeviceReady slots stay valid.  MSI_E_BUSY if a consumer is held. */
+/* Advance the request epoch ("Separate Window and GPU-Slot Lifecycles").
+ * Fills still in flight, including source reads, become unpublishable: their
+ * completion leaves the slot Vacant (a read completing later frees its
+ * window without any copy).  Resident DeviceReady slots stay valid.
+ * MSI_E_BUSY if a consumer is held. */
 msi_status msi_plan_reset(msi_plan *plan);
 
 /* Bytes of device workspace msi_route and msi_moe_forward need for T tokens.
@@ -249,7 +297,8 @@ msi_status msi_plan_reset(msi_plan *plan);
  * in ab-byte elements (bf16 or f32).  Contents are scratch between calls. */
 msi_status msi_workspace_size(const msi_plan *plan, uint32_t n_tokens, uint64_t *bytes);
 
-/* Make expert `expert` of `layer` resident (Section 3.3; Section 4 scheduling).
+/* Make expert `expert` of `layer` resident ("Stable Slots and Bundle
+ * Publication"; Implementation, "Scheduling and copies").
  * slot = -1 lets the replacement policy choose (least recently used slot
  * without consumers); slot >= 0 forces that slot.  If the object is already
  * resident and ready (in `slot` when forced) this is a hit: the ticket
@@ -277,7 +326,8 @@ msi_status msi_plan_poll(msi_plan *plan);
  * Errors: MSI_E_INVALID_ARG, MSI_E_NOMEM (workspace), MSI_E_DEVICE. */
 msi_status msi_route(msi_plan *plan, const msi_route_args *args, void *stream);
 
-/* One MoE layer against the slot pool (Section 4 scheduling).  Reads the
+/* One MoE layer against the slot pool (Implementation, "Scheduling and
+ * copies").  Reads the
  * per-expert counts (one device-to-host copy), resolves the demanded set
  * against the residency state (hits first, then misses in ascending expert
  * id, in rounds of at most the pool size), fills misses on `side_stream`
@@ -349,6 +399,36 @@ msi_status msi_residual_init(const uint16_t *x0_bf16, float *h, uint16_t *x_bf16
                              void *stream);
 msi_status msi_residual_add(const float *out, float *h, uint16_t *x_bf16, uint32_t rows, uint32_t cols,
                             void *stream);
+
+/* Source-service counters (plans with a source; zeros otherwise). */
+typedef struct {
+    uint64_t reads_issued, reads_completed, reads_failed;
+    uint64_t requests, requests_ready, requests_failed, requests_stale;
+    uint64_t logical_bytes, physical_bytes, padding_bytes;   /* physical: aligned covering reads */
+    uint64_t peak_depth;         /* most reads in flight at once                       */
+    uint64_t windows_busy;       /* staging windows not Free now                       */
+    double read_seconds;         /* summed latency of the reads                        */
+    double wait_seconds;         /* time forwards spent blocked on the source          */
+    uint32_t direct_files;       /* files read with direct I/O                         */
+    uint32_t buffered_files;     /* files read through the page cache (fallback)       */
+    uint64_t bounced_reads;      /* direct reads staged through a 4 MiB bounce buffer per I/O
+                                    worker because the windows' pages refuse direct reads */
+} msi_source_stats;
+msi_status msi_source_stats_get(const msi_plan *plan, msi_source_stats *stats);
+
+/* Test hooks of the source's rejection conditions: the next read of extent
+ * `component` of (layer, expert) returns short (MSI_FAULT_SHORT), fails with
+ * EIO (MSI_FAULT_EIO) or is held until msi_debug_source_release
+ * (MSI_FAULT_HOLD; a held read completes by itself after 30 s).  The request
+ * then fails closed: its window returns to Free, no copy is made and nothing
+ * is published; a forward that needed it returns MSI_E_SHORT / MSI_E_IO with
+ * out untouched. */
+#define MSI_FAULT_SHORT 1u
+#define MSI_FAULT_EIO 2u
+#define MSI_FAULT_HOLD 3u
+msi_status msi_debug_source_fault(msi_plan *plan, uint32_t layer, uint32_t expert, uint32_t component,
+                                  uint32_t mode);
+msi_status msi_debug_source_release(msi_plan *plan);
 
 /* Test hook: overwrite one slot's device generation word (synchronously). */
 msi_status msi_debug_set_device_gen(msi_plan *plan, uint32_t layer, uint32_t slot, uint32_t gen);

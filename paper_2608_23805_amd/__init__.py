@@ -16,7 +16,7 @@ from typing import List, Optional, Sequence, Tuple
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmsi.so")
 
-MSI_ABI_VERSION = 2
+MSI_ABI_VERSION = 3
 MSI_OK = 0
 MSI_E_INVALID_ARG = -1
 MSI_E_SHORT = -2
@@ -26,9 +26,12 @@ MSI_E_STALE = -5
 MSI_E_DEVICE = -6
 MSI_E_NOMEM = -7
 MSI_E_STATE = -8
+MSI_E_IO = -9
 STATUS_NAMES = {0: "MSI_OK", -1: "MSI_E_INVALID_ARG", -2: "MSI_E_SHORT", -3: "MSI_E_WRONG_OBJECT",
                 -4: "MSI_E_BUSY", -5: "MSI_E_STALE", -6: "MSI_E_DEVICE", -7: "MSI_E_NOMEM",
-                -8: "MSI_E_STATE"}
+                -8: "MSI_E_STATE", -9: "MSI_E_IO"}
+MSI_SOURCE_BUFFERED_OK = 1
+FAULTS = {"short": 1, "eio": 2, "hold": 3}
 
 MSI_W_F32, MSI_W_BF16, MSI_W_Q4B32 = 0, 1, 2
 MSI_NOALLOC_SCRATCH_BYTES = 64 << 20
@@ -43,13 +46,32 @@ class msi_object_desc(ctypes.Structure):
                 ("offset", _u64), ("nbytes", _u64)]
 
 
+class msi_extent_desc(ctypes.Structure):
+    _fields_ = [("layer", _u32), ("expert", _u32), ("component", _u32), ("file", _u32),
+                ("offset", _u64), ("nbytes", _u64)]
+
+
+class msi_source_desc(ctypes.Structure):
+    _fields_ = [("files", ctypes.POINTER(ctypes.c_char_p)), ("n_files", _u32), ("inflight", _u32),
+                ("flags", _u32), ("align", _u32), ("extents", ctypes.POINTER(msi_extent_desc)),
+                ("n_extents", _u32), ("reserved", _u32)]
+
+
+class msi_source_stats(ctypes.Structure):
+    _fields_ = [(n, _u64) for n in ("reads_issued", "reads_completed", "reads_failed", "requests",
+                                    "requests_ready", "requests_failed", "requests_stale", "logical_bytes",
+                                    "physical_bytes", "padding_bytes", "peak_depth", "windows_busy")] + \
+               [("read_seconds", ctypes.c_double), ("wait_seconds", ctypes.c_double),
+                ("direct_files", _u32), ("buffered_files", _u32), ("bounced_reads", _u64)]
+
+
 class msi_plan_desc(ctypes.Structure):
     _fields_ = [("abi_version", _u32), ("n_layers", _u32), ("n_experts", _u32), ("d_model", _u32),
                 ("d_ff", _u32), ("top_k", _u32), ("wdtype", _u32), ("slots_per_layer", _u32),
                 ("transient_slots", _u32), ("reserved0", _u32), ("slot_pool", _vp),
                 ("slot_pool_bytes", _u64), ("slot_stride", _u64), ("windows", ctypes.POINTER(_vp)),
                 ("n_windows", _u32), ("n_objects", _u32), ("window_bytes", _u64),
-                ("objects", ctypes.POINTER(msi_object_desc))]
+                ("objects", ctypes.POINTER(msi_object_desc)), ("source", ctypes.POINTER(msi_source_desc))]
 
 
 class msi_ticket(ctypes.Structure):
@@ -98,7 +120,8 @@ EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_
            "msi_workspace_size", "msi_slot_fill", "msi_plan_poll", "msi_route", "msi_moe_forward",
            "msi_moe_forward_noalloc",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
-           "msi_debug_set_device_gen", "msi_stream_threshold"]
+           "msi_debug_set_device_gen", "msi_stream_threshold", "msi_source_stats_get",
+           "msi_debug_source_fault", "msi_debug_source_release"]
 
 
 class MsiError(RuntimeError):
@@ -128,6 +151,9 @@ def _load():
     L.msi_slot_query.argtypes = [_vp, _u32, _u32, P(msi_slot_info)]
     L.msi_plan_stats.argtypes = [_vp, P(msi_stats)]
     L.msi_debug_set_device_gen.argtypes = [_vp, _u32, _u32, _u32]
+    L.msi_source_stats_get.argtypes = [_vp, P(msi_source_stats)]
+    L.msi_debug_source_fault.argtypes = [_vp, _u32, _u32, _u32, _u32]
+    L.msi_debug_source_release.argtypes = [_vp]
     L.msi_plan_set_timing.argtypes = [_vp, ctypes.c_int]
     L.msi_plan_set_timing_period.argtypes = [_vp, _u32]
     L.msi_residual_init.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
@@ -232,12 +258,14 @@ class Plan:
 
     objects: sequence of (layer, expert, window, offset, nbytes).
     windows: pinned uint8 CPU tensors, all of the same size.
+    source: None, or a Source (objects read from canonical files; windows
+    are then its staging windows and ``objects`` must be empty).
     """
 
     def __init__(self, *, n_layers: int, n_experts: int, d_model: int, d_ff: int, top_k: int,
                  wdtype: str, slots_per_layer: int, windows: Sequence, objects: Sequence[Tuple],
                  transient_slots: int = 0, slot_stride: Optional[int] = None, device="cuda",
-                 slot_pool=None):
+                 slot_pool=None, source: Optional["Source"] = None):
         import torch
         self.wdtype = wdtype
         self.n_layers, self.n_experts, self.d, self.I, self.K = n_layers, n_experts, d_model, d_ff, top_k
@@ -253,7 +281,10 @@ class Plan:
         self.slot_pool_ptr = (base + 255) // 256 * 256
         self.slot_pool_bytes = slot_pool.numel() - (self.slot_pool_ptr - base)
         self.windows = list(windows)
-        self._win_ptrs = (_vp * len(self.windows))(*[w.data_ptr() for w in self.windows])
+        self.source = source
+        if source is not None:
+            self.windows = source.windows
+        self._win_ptrs = (_vp * len(self.windows))(*[_window_ptr(w) for w in self.windows])
         self._objs = (msi_object_desc * max(1, len(objects)))(
             *[msi_object_desc(int(l), int(e), int(w), 0, int(o), int(n)) for (l, e, w, o, n) in objects])
         desc = msi_plan_desc(
@@ -262,8 +293,11 @@ class Plan:
             transient_slots=transient_slots, reserved0=0, slot_pool=self.slot_pool_ptr,
             slot_pool_bytes=self.slot_pool_bytes, slot_stride=self.slot_stride,
             windows=ctypes.cast(self._win_ptrs, ctypes.POINTER(_vp)), n_windows=len(self.windows),
-            n_objects=len(objects), window_bytes=self.windows[0].numel() if self.windows else 0,
-            objects=ctypes.cast(self._objs, ctypes.POINTER(msi_object_desc)))
+            n_objects=len(objects),
+            window_bytes=(source.window_bytes if source is not None else
+                          (self.windows[0].numel() if self.windows else 0)),
+            objects=ctypes.cast(self._objs, ctypes.POINTER(msi_object_desc)),
+            source=ctypes.pointer(source.c()) if source is not None else None)
         h = _vp()
         _check(lib.msi_plan_create(ctypes.byref(desc), ctypes.byref(h)))
         self.h = h
@@ -373,6 +407,59 @@ class Plan:
 
     def debug_set_device_gen(self, layer: int, slot: int, gen: int):
         _check(lib.msi_debug_set_device_gen(self.h, layer, slot, gen))
+
+    def source_stats(self) -> dict:
+        s = msi_source_stats()
+        _check(lib.msi_source_stats_get(self.h, ctypes.byref(s)))
+        return {n: getattr(s, n) for n, _ in msi_source_stats._fields_}
+
+    def source_fault(self, layer: int, expert: int, component: int, mode: str):
+        """Test hook: the next read of that object's component is short / fails with EIO / is held."""
+        _check(lib.msi_debug_source_fault(self.h, layer, expert, component, FAULTS[mode]))
+
+    def source_release(self):
+        _check(lib.msi_debug_source_release(self.h))
+
+
+def _window_ptr(w) -> int:
+    return w[1] if isinstance(w, tuple) else w.data_ptr()
+
+
+class Source:
+    """Canonical files plus the staging windows of a plan's source service.
+
+    extents: (layer, expert, component, file, offset, nbytes) tuples;
+    n_windows pinned staging windows of window_bytes (a multiple of align),
+    each aligned to ``align``; inflight: reads in flight at most (1..8)."""
+
+    def __init__(self, files: Sequence[str], extents: Sequence[Tuple], n_windows: int, window_bytes: int,
+                 inflight: int, align: int = 4096, buffered_ok: bool = True):
+        import torch
+        self.files = [os.fsencode(f) for f in files]
+        self.extents = list(extents)
+        self.window_bytes = int(window_bytes)
+        self.align = int(align)
+        self.inflight = int(inflight)
+        self.flags = MSI_SOURCE_BUFFERED_OK if buffered_ok else 0
+        self._bufs, self.windows = [], []
+        for _ in range(n_windows):
+            b = torch.empty(self.window_bytes + self.align, dtype=torch.uint8, pin_memory=True)
+            ptr = (b.data_ptr() + self.align - 1) // self.align * self.align
+            self._bufs.append(b)
+            self.windows.append((b, ptr))
+        self._c = None
+
+    def c(self) -> msi_source_desc:
+        if self._c is None:
+            self._fnames = (ctypes.c_char_p * len(self.files))(*self.files)
+            self._ext = (msi_extent_desc * max(1, len(self.extents)))(
+                *[msi_extent_desc(int(l), int(e), int(c), int(f), int(o), int(n))
+                  for (l, e, c, f, o, n) in self.extents])
+            self._c = msi_source_desc(files=self._fnames, n_files=len(self.files), inflight=self.inflight,
+                                      flags=self.flags, align=self.align,
+                                      extents=ctypes.cast(self._ext, ctypes.POINTER(msi_extent_desc)),
+                                      n_extents=len(self.extents), reserved=0)
+        return self._c
 
 
 def pack_windows(objects: Sequence, per_window: int, layer: int = 0, first_expert: int = 0,

@@ -2,8 +2,9 @@
 //
 // The combine is the only kernel that writes the caller's output, and it does
 // so only when the status word is clean: an invalid completion never makes
-// data visible (lifetime obligations, Table 2 row L; fatal fault cells publish
-// nothing, Section 5.7).  out[t] = shared(x_t) + sum over the token's
+// data visible (the lifetime row of the paper's table of certificate
+// obligations; its fatal fault cells publish nothing, "Integrated
+// Deterministic Faults").  out[t] = shared(x_t) + sum over the token's
 // experts in ascending id of the weighted contributions, summed in fp32 in
 // that fixed order so the result does not depend on slot capacity.
 #include <algorithm>

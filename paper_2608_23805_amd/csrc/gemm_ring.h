@@ -2,7 +2,7 @@
 // experts on the tile path (experts with more than 16 routed rows), gfx950.
 //
 // The complete gate, up and down projections of every selected expert are
-// computed (Section 5.4); outputs are the same per-row quantities as the
+// computed ("Output-Exact Execution Beyond the Full-Residency Envelope"); outputs are the same per-row quantities as the
 // stream path: act[row, I] = silu(x Wg^T) * (x Wu^T) and
 // y[row, d] = row_weight * (act Wd^T), rows in permuted order, bf16.
 //

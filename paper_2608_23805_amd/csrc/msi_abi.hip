@@ -1,6 +1,7 @@
 // msi_abi.hip -- C ABI of the slot-backed MoE layer (declared in include/msi.h).
 //
-// Host side of the paper's Section 4 scheduling loop: layer entry requests
+// Host side of the paper's scheduling loop (Implementation, "Scheduling and
+// copies"): layer entry requests
 // the bundle of demanded experts, misses are copied from their host windows
 // into reserved slots on a side stream, a device event publishes readiness,
 // the expert kernels consume the slots at stable addresses, and layer exit
@@ -9,7 +10,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cstring>
+#include <deque>
 #include <mutex>
 #include <new>
 #include <string>
@@ -19,6 +22,7 @@
 #include "../../include/msi.h"
 #include "kernels.h"
 #include "plan_core.hpp"
+#include "source.hpp"
 
 using namespace msi;
 
@@ -128,6 +132,25 @@ struct msi_plan {
     std::vector<const void *> windows;
     uint64_t object_bytes = 0;
     PlanCore *core = nullptr;
+    SourceService *src = nullptr;       // bounded source service (plans whose objects live in files)
+    // A fill whose bytes come from the source: queued, reading into a staging
+    // window, copying window -> slot, then done; or failed (never published).
+    struct SrcFill {
+        FillRecord rec;
+        hipStream_t side = nullptr;
+        int round = -1;                 // forward round it serves; -1: an explicit fill (copied when ready)
+        int window = -1;
+        int state = 0;                  // SF_* below
+        bool cancel = false;            // its forward failed: never copy it
+        hipEvent_t ev = nullptr;        // copy complete (owned)
+    };
+    std::deque<SrcFill> sfills;         // submission order
+    int src_round = -1;                 // rounds <= this may be copied (the forward's current round)
+    struct FaultReq {
+        uint32_t layer, expert, component, mode;
+    };
+    std::vector<FaultReq> src_faults;   // test hooks, applied at the object's next request
+    double src_wait_s = 0.0;            // forwards blocked on the source
     int device = 0;
     void *scratch = nullptr;            // this device's copy of the static scratch (msi_moe_forward_noalloc)
     uint32_t *gen_dev = nullptr;        // [n_layers * pool_slots]
@@ -280,6 +303,227 @@ void poll_fills(msi_plan *p)
             observe_fill(p, gs);
 }
 
+// ---- source-backed fills --------------------------------------------------
+// States of a SrcFill.
+constexpr int SF_QUEUED = 0, SF_READING = 1, SF_READY = 2, SF_COPYING = 3, SF_DONE = 4, SF_FAILED = 5;
+
+msi_status source_error_status(SourceError e)
+{
+    switch (e) {
+    case SourceError::Short: return MSI_E_SHORT;
+    case SourceError::Io: return MSI_E_IO;
+    case SourceError::Stale: return MSI_E_STALE;
+    default: return MSI_E_SHORT;
+    }
+}
+
+// Copy a HostReady window into its slot on the fill's side stream: after the
+// slot's earlier fill and its last readers, invalidate the generation word,
+// copy each extent from its place in the window to its offset in the slot,
+// publish the generation, record the fill's event.
+msi_status copy_window(msi_plan *p, msi_plan::SrcFill &f)
+{
+    const PlanCore &c = *p->core;
+    const uint32_t gs = c.global_slot(f.rec.layer, f.rec.slot);
+    const SourceObject *so = c.source_object(f.rec.layer, f.rec.expert);
+    uint64_t place[SourceService::MAX_EXTENTS];
+    if (!so || !p->src->layout(so->ext, so->n, place, nullptr))
+        return fail(MSI_E_INVALID_ARG, "internal: source object layout");
+    if (p->fill_ev[gs] && p->fill_ev[gs] != f.ev)
+        HIP_OK(hipStreamWaitEvent(f.side, p->fill_ev[gs], 0));
+    if (p->release_ev[gs])
+        HIP_OK(hipStreamWaitEvent(f.side, p->release_ev[gs], 0));
+    GenBatch inval{}, pub{};
+    inval.n = pub.n = 1;
+    inval.slot[0] = pub.slot[0] = gs;
+    inval.value[0] = 0u;
+    pub.value[0] = f.rec.gen;
+    HIP_OK(launch_set_gens(p->gen_dev, inval, f.side));
+    uint8_t *dst = static_cast<uint8_t *>(p->desc.slot_pool) + uint64_t(gs) * p->desc.slot_stride;
+    for (int i = 0; i < so->n; ++i) {
+        HIP_OK(hipMemcpyAsync(dst, p->src->window(uint32_t(f.window)) + place[i], so->ext[i].nbytes,
+                              hipMemcpyHostToDevice, f.side));
+        dst += so->ext[i].nbytes;
+    }
+    HIP_OK(launch_set_gens(p->gen_dev, pub, f.side));
+    if (!f.ev && !(f.ev = p->get_event()))
+        return fail(MSI_E_DEVICE, "event creation failed");
+    HIP_OK(hipEventRecord(f.ev, f.side));
+    p->src->set_copying(uint32_t(f.window));
+    // the slot's pending fill is now this copy (the plan observes it through the event)
+    if (p->fill_ev[gs] && !p->fill_ev_shared[gs])
+        p->free_events.push_back(p->fill_ev[gs]);
+    p->fill_ev[gs] = f.ev;
+    p->fill_ev_id[gs] = f.rec.id;
+    p->fill_ev_shared[gs] = 1;
+    f.state = SF_COPYING;
+    return MSI_OK;
+}
+
+// Whether a source fill may still be published: a forward's fill while the
+// epoch holds (a later round of the same forward may reuse its slot, which
+// supersedes the plan's record but not this round's copy); an explicit fill
+// while it is its slot's current version.
+bool sf_current(const msi_plan *p, const msi_plan::SrcFill &f)
+{
+    return f.round >= 0 ? f.rec.epoch == p->core->epoch() : p->core->fill_current(f.rec.id, f.rec.epoch, f.rec.gen);
+}
+
+// One step of the source engine: finished copies free their windows,
+// completed reads are judged (a stale ticket, short read or negative status
+// fails the fill closed: its window is freed, nothing is copied), ready
+// windows whose round has come are copied, and queued fills are submitted
+// into free windows (at most the service's in-flight limit reads at once).
+// With wait_ms > 0 and no progress, waits for a read or the oldest copy.
+// Returns the first failure of a fill that serves a forward round.
+msi_status source_progress(msi_plan *p, int wait_ms)
+{
+    SourceService &S = *p->src;
+    PlanCore &c = *p->core;
+    msi_status first_err = MSI_OK;
+    bool moved = false;
+    for (msi_plan::SrcFill &f : p->sfills)
+        if (f.state == SF_COPYING && hipEventQuery(f.ev) == hipSuccess) {
+            S.set_free(uint32_t(f.window));
+            const uint32_t gs = c.global_slot(f.rec.layer, f.rec.slot);
+            if (p->fill_ev[gs] == f.ev) {
+                p->core->complete_fill(f.rec.id);
+                p->fill_ev[gs] = nullptr;
+                p->fill_ev_id[gs] = -1;
+                p->fill_ev_shared[gs] = 0;
+            }
+            f.state = SF_DONE;
+            moved = true;
+        }
+    auto judge = [&](const std::vector<SourceService::Done> &done) {
+        for (const SourceService::Done &d : done) {
+            moved = true;
+            for (msi_plan::SrcFill &f : p->sfills) {
+                if (f.state != SF_READING || f.rec.id != int64_t(d.tag))
+                    continue;
+                if (d.error == SourceError::None && !f.cancel) {
+                    f.state = SF_READY;
+                } else {
+                    if (d.error == SourceError::None)
+                        S.set_free(d.window);               // cancelled: ready but never copied
+                    c.fail_fill(f.rec.id);
+                    f.state = SF_FAILED;
+                    if (f.round >= 0 && !f.cancel && first_err == MSI_OK)
+                        first_err = fail(source_error_status(d.error),
+                                         std::string("source read of expert ") + std::to_string(f.rec.expert) +
+                                             " failed (" +
+                                             (d.error == SourceError::Short ? "short read"
+                                              : d.error == SourceError::Io ? std::string("errno ") + std::to_string(d.sys_errno)
+                                                                            : "stale ticket") +
+                                             "); nothing published");
+                }
+                break;
+            }
+        }
+    };
+    auto current = [&](uint64_t tag, uint32_t, uint32_t) {
+        for (const msi_plan::SrcFill &f : p->sfills)
+            if (f.rec.id == int64_t(tag))
+                return sf_current(p, f);
+        return false;
+    };
+    judge(S.collect(0, current));
+    for (msi_plan::SrcFill &f : p->sfills)
+        if (f.state == SF_READY && (f.round < 0 || f.round <= p->src_round)) {
+            if (!sf_current(p, f)) {                // superseded or reset meanwhile
+                S.set_free(uint32_t(f.window));
+                c.fail_fill(f.rec.id);
+                f.state = SF_FAILED;
+            } else {
+                const msi_status st = copy_window(p, f);
+                if (st != MSI_OK)
+                    return st;
+            }
+            moved = true;
+        }
+    for (msi_plan::SrcFill &f : p->sfills) {
+        if (f.state != SF_QUEUED)
+            continue;
+        if (f.cancel || !sf_current(p, f)) {
+            c.fail_fill(f.rec.id);
+            f.state = SF_FAILED;
+            moved = true;
+            continue;
+        }
+        const int w = S.free_window();
+        if (w < 0)
+            break;
+        const SourceObject *so = c.source_object(f.rec.layer, f.rec.expert);
+        for (auto it = p->src_faults.begin(); it != p->src_faults.end();)
+            if (it->layer == f.rec.layer && it->expert == f.rec.expert) {
+                S.inject(uint64_t(f.rec.id), int(it->component), SourceFault(it->mode));
+                it = p->src_faults.erase(it);
+            } else {
+                ++it;
+            }
+        if (!so || !S.submit(uint32_t(w), so->ext, so->n, uint64_t(f.rec.id), f.rec.epoch, f.rec.gen))
+            return fail(MSI_E_INVALID_ARG, "internal: source submission refused");
+        f.window = w;
+        f.state = SF_READING;
+        moved = true;
+    }
+    while (!p->sfills.empty() && (p->sfills.front().state == SF_DONE || p->sfills.front().state == SF_FAILED)) {
+        if (p->sfills.front().ev)
+            p->free_events.push_back(p->sfills.front().ev);
+        p->sfills.pop_front();
+    }
+    if (!moved && wait_ms > 0) {
+        const auto t0 = std::chrono::steady_clock::now();
+        if (S.outstanding()) {
+            judge(S.collect(wait_ms, current));
+        } else {
+            for (msi_plan::SrcFill &f : p->sfills)
+                if (f.state == SF_COPYING) {
+                    (void)hipEventSynchronize(f.ev);
+                    break;
+                }
+        }
+        p->src_wait_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    }
+    return first_err;
+}
+
+// Drive the engine until `done()` holds; stops at the first failure.
+template <typename Pred>
+msi_status source_until(msi_plan *p, Pred done)
+{
+    const auto t0 = std::chrono::steady_clock::now();
+    while (!done()) {
+        const msi_status st = source_progress(p, 5);
+        if (st != MSI_OK)
+            return st;
+        if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(120))
+            return fail(MSI_E_DEVICE, "source service made no progress for 120 s");
+    }
+    return MSI_OK;
+}
+
+// Cancel every forward fill not yet copied and drain the reads in flight:
+// their windows return to Free and nothing of theirs is published.
+void source_cancel_forward(msi_plan *p)
+{
+    for (msi_plan::SrcFill &f : p->sfills)
+        if (f.round >= 0 && (f.state == SF_QUEUED || f.state == SF_READING || f.state == SF_READY))
+            f.cancel = true;
+    for (msi_plan::SrcFill &f : p->sfills)
+        if (f.cancel && f.state == SF_READY) {
+            p->src->set_free(uint32_t(f.window));
+            p->core->fail_fill(f.rec.id);
+            f.state = SF_FAILED;
+        }
+    (void)source_until(p, [&] {
+        for (const msi_plan::SrcFill &f : p->sfills)
+            if (f.state == SF_QUEUED || f.state == SF_READING || f.state == SF_COPYING)
+                return false;
+        return true;
+    });
+}
+
 // Enqueue on `side` the invalidate -> copy -> publish sequence of a batch of
 // fills (all ids already recorded by the core).  The side stream first waits
 // for every earlier fill and every reading round of each target slot.
@@ -371,26 +615,72 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         return fail(MSI_E_INVALID_ARG, "null argument");
     *out = nullptr;
     const uint64_t ob = object_bytes_of(*desc);
-    PlanCore *core = new (std::nothrow) PlanCore(*desc, ob);
-    if (!core)
+    // the source service first: its files' sizes bound the manifest's extents
+    SourceService *src = nullptr;
+    std::vector<uint64_t> fsizes;
+    if (desc->source) {
+        const msi_source_desc &sd = *desc->source;
+        if (!sd.files || sd.n_files == 0 || !desc->windows || desc->n_windows == 0)
+            return fail(MSI_E_INVALID_ARG, "a source needs files and staging windows");
+        std::vector<std::string> files;
+        for (uint32_t f = 0; f < sd.n_files; ++f) {
+            if (!sd.files[f])
+                return fail(MSI_E_INVALID_ARG, "null source file name");
+            files.emplace_back(sd.files[f]);
+        }
+        std::vector<void *> wins;
+        for (uint32_t w = 0; w < desc->n_windows; ++w)
+            wins.push_back(const_cast<void *>(desc->windows[w]));
+        src = new (std::nothrow) SourceService(files, wins, desc->window_bytes, sd.inflight, sd.align ? sd.align : 4096,
+                                               (sd.flags & MSI_SOURCE_BUFFERED_OK) != 0);
+        if (!src)
+            return fail(MSI_E_NOMEM, "host allocation failed");
+        if (!src->ok()) {
+            const std::string m = src->error();
+            delete src;
+            return fail(MSI_E_INVALID_ARG, m);
+        }
+        for (uint32_t f = 0; f < sd.n_files; ++f)
+            fsizes.push_back(src->file_size(f));
+    }
+    PlanCore *core = new (std::nothrow) PlanCore(*desc, ob, fsizes);
+    if (!core) {
+        delete src;
         return fail(MSI_E_NOMEM, "host allocation failed");
+    }
     if (core->status() != MSI_OK) {
         const msi_status st = core->status();
         const std::string m = core->error();
         delete core;
+        delete src;
         return fail(st, m);
     }
+    if (src)
+        for (uint32_t l = 0; l < desc->n_layers; ++l)
+            for (uint32_t e = 0; e < desc->n_experts; ++e) {
+                const SourceObject *so = core->source_object(l, e);
+                uint64_t place[SourceService::MAX_EXTENTS];
+                if (so && !src->layout(so->ext, so->n, place, nullptr)) {
+                    delete core;
+                    delete src;
+                    return fail(MSI_E_INVALID_ARG, "window_bytes is smaller than the covering reads of (layer " +
+                                                       std::to_string(l) + ", expert " + std::to_string(e) + ")");
+                }
+            }
     msi_plan *p = new (std::nothrow) msi_plan();
     if (!p) {
         delete core;
+        delete src;
         return fail(MSI_E_NOMEM, "host allocation failed");
     }
     p->desc = *desc;
     p->windows.assign(desc->windows, desc->windows + desc->n_windows);
     p->desc.windows = nullptr;
     p->desc.objects = nullptr;
+    p->desc.source = nullptr;
     p->object_bytes = ob;
     p->core = core;
+    p->src = src;
     const size_t nslots = size_t(core->n_layers()) * core->pool_slots();
     p->fill_ev.assign(nslots, nullptr);
     p->fill_ev_id.assign(nslots, -1);
@@ -440,6 +730,12 @@ msi_status msi_plan_destroy(msi_plan *p)
     if (!p)
         return MSI_OK;
     p->resolve_timings();
+    if (p->src && p->core) {
+        // shutdown drains the source: held reads are let go, every submitted
+        // request completes and its window returns to Free
+        p->src->release_holds();
+        (void)source_until(p, [&] { return p->sfills.empty(); });
+    }
     if (p->core) {
         for (uint32_t gs = 0; gs < p->fill_ev.size(); ++gs)
             if (p->fill_ev[gs]) {
@@ -475,6 +771,7 @@ msi_status msi_plan_destroy(msi_plan *p)
         (void)hipHostFree(p->counts_host);
     if (p->status_host)
         (void)hipHostFree(p->status_host);
+    delete p->src;
     delete p->core;
     delete p;
     return MSI_OK;
@@ -502,6 +799,12 @@ msi_status msi_plan_poll(msi_plan *p)
 {
     if (!p)
         return fail(MSI_E_INVALID_ARG, "null plan");
+    if (p->src) {
+        HIP_OK(hipSetDevice(p->device));
+        const msi_status st = source_progress(p, 0);
+        if (st != MSI_OK && st != MSI_E_SHORT && st != MSI_E_IO && st != MSI_E_STALE)
+            return st;
+    }
     poll_fills(p);
     return MSI_OK;
 }
@@ -520,6 +823,18 @@ msi_status msi_slot_fill(msi_plan *p, uint32_t layer, uint32_t expert, int32_t s
     if (ticket->hit)
         return MSI_OK;
     hipStream_t side = static_cast<hipStream_t>(side_stream);
+    if (p->src) {
+        // asynchronous: the read runs on the source's workers; the copy into
+        // the slot is enqueued on `side` once the read completes (driven by
+        // later calls on this plan)
+        msi_plan::SrcFill f;
+        f.rec = *p->core->fill(id);
+        f.side = side;
+        f.round = -1;
+        p->sfills.push_back(f);
+        const msi_status pst = source_progress(p, 0);
+        return pst == MSI_OK || pst == MSI_E_SHORT || pst == MSI_E_IO || pst == MSI_E_STALE ? MSI_OK : pst;
+    }
     const uint32_t gs = p->core->global_slot(layer, uint32_t(ticket->slot));
     const std::vector<FillRecord> fills{*p->core->fill(id)};
     msi_status est = enqueue_fills(p, layer, fills, side);
@@ -791,8 +1106,47 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         return e;
     };
     msi_status rst = MSI_OK;
+    if (p->src) {
+        // source-backed: earlier explicit fills first (rounds may count them
+        // as hits), then every round's misses go to the source at once, in
+        // round order (reads run as staging windows allow); a round's copies
+        // into its slots are enqueued when the loop below reaches it
+        rst = source_until(p, [&] {
+            for (const msi_plan::SrcFill &f : p->sfills)
+                if (f.round < 0 && f.state <= SF_READY)
+                    return false;
+            return true;
+        });
+        for (size_t r = 0; r < sched.rounds.size(); ++r)
+            for (const FillRecord &fr : sched.rounds[r].fills) {
+                msi_plan::SrcFill f;
+                f.rec = fr;
+                f.side = side;
+                f.round = int(r);
+                p->sfills.push_back(f);
+            }
+    }
+    auto round_copied = [&](const SchedRound &round) {
+        for (const FillRecord &fr : round.fills)
+            for (const msi_plan::SrcFill &f : p->sfills)
+                if (f.rec.id == fr.id && f.round >= 0 && f.state < SF_COPYING)
+                    return false;
+        return true;
+    };
     for (size_t r = 0; r < launches.size() && rst == MSI_OK; ++r) {
-        if (r < sched.rounds.size()) {
+        if (r < sched.rounds.size() && p->src) {
+            const SchedRound &round = sched.rounds[r];
+            p->src_round = int(r);
+            rst = source_until(p, [&] { return round_copied(round); });
+            if (rst != MSI_OK)
+                break;
+            // the copies set each filled slot's pending event; the kernels wait on them below
+            for (const SchedItem &si : round.items) {
+                const uint32_t gs = core.global_slot(a->layer, uint32_t(si.slot));
+                if (p->fill_ev[gs])
+                    HIP_OK(hipStreamWaitEvent(cs, p->fill_ev[gs], 0));
+            }
+        } else if (r < sched.rounds.size()) {
             const SchedRound &round = sched.rounds[r];
             if (!round.fills.empty()) {
                 msi_status fst = MSI_OK;
@@ -901,6 +1255,12 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
     const uint32_t hst = __atomic_load_n(p->status_host, __ATOMIC_ACQUIRE);
     p->status_clean = rst == MSI_OK && hst == STATUS_DONE;
 
+    if (p->src) {
+        p->src_round = -1;
+        if (rst != MSI_OK)
+            source_cancel_forward(p);     // nothing more of this forward is copied; reads drain
+        (void)source_progress(p, 0);      // finished copies free their windows
+    }
     // ---- layer exit: observe this forward's fills, release consumers
     for (const SchedRound &round : sched.rounds)
         for (const FillRecord &f : round.fills) {
@@ -1003,7 +1363,7 @@ msi_status msi_plan_stats(const msi_plan *p, msi_stats *st)
         return fail(MSI_E_INVALID_ARG, "null argument");
     *st = p->core->stats();
     st->fills_in_flight = p->core->fills_in_flight();
-    st->windows_busy = p->core->windows_busy();
+    st->windows_busy = p->src ? p->src->busy_windows() : p->core->windows_busy();
     st->consumers_live = p->core->consumers_live();
     st->epoch = p->core->epoch();
     return MSI_OK;
@@ -1059,6 +1419,40 @@ msi_status msi_residual_add(const float *out, float *h, uint16_t *x, uint32_t ro
     if (uint64_t(rows) * cols && (!out || !h || !x))
         return fail(MSI_E_INVALID_ARG, "null pointer");
     HIP_OK(launch_residual(nullptr, out, h, x, int(rows), int(cols), static_cast<hipStream_t>(stream)));
+    return MSI_OK;
+}
+
+msi_status msi_source_stats_get(const msi_plan *p, msi_source_stats *st)
+{
+    if (!p || !st)
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    *st = msi_source_stats{};
+    if (!p->src)
+        return MSI_OK;
+    const SourceStats s = p->src->stats();
+    *st = msi_source_stats{s.reads_issued, s.reads_completed, s.reads_failed, s.requests, s.requests_ready,
+                           s.requests_failed, s.requests_stale, s.logical_bytes, s.physical_bytes, s.padding_bytes,
+                           s.peak_depth, p->src->busy_windows(), s.read_seconds, p->src_wait_s, s.direct, s.buffered,
+                           s.bounced};
+    return MSI_OK;
+}
+
+msi_status msi_debug_source_fault(msi_plan *p, uint32_t layer, uint32_t expert, uint32_t component, uint32_t mode)
+{
+    if (!p || !p->src)
+        return fail(MSI_E_INVALID_ARG, "null plan or plan without a source");
+    const SourceObject *so = p->core->source_object(layer, expert);
+    if (!so || component >= uint32_t(so->n) || mode < MSI_FAULT_SHORT || mode > MSI_FAULT_HOLD)
+        return fail(MSI_E_INVALID_ARG, "no such source object / component, or unknown fault mode");
+    p->src_faults.push_back(msi_plan::FaultReq{layer, expert, component, mode});
+    return MSI_OK;
+}
+
+msi_status msi_debug_source_release(msi_plan *p)
+{
+    if (!p || !p->src)
+        return fail(MSI_E_INVALID_ARG, "null plan or plan without a source");
+    p->src->release_holds();
     return MSI_OK;
 }
 

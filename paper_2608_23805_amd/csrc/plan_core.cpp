@@ -1,8 +1,10 @@
 // plan_core.cpp -- residency planner: manifest checks, slot lifecycle,
 // generations and epochs, LRU / zero-cache policies, forward round schedule.
-// Section 3.1 (manifest and mutable state), Section 3.2 (extent rejection
-// conditions), Section 3.3 (stable slots, publication), Section 3.4 (state
-// sequences, tickets, reset), Section 4 (scheduling and copies).
+// The paper's Design section: "A Shared Cross-Adapter Plan Core" (manifest
+// and mutable state), "Bounded Source Service" (extent rejection
+// conditions), "Stable Slots and Bundle Publication", "Separate Window and
+// GPU-Slot Lifecycles" (state sequences, tickets, reset); Implementation,
+// "Scheduling and copies".
 #include "plan_core.hpp"
 
 #include <algorithm>
@@ -20,7 +22,7 @@ std::string batch_limit_error(const msi_plan_desc &d, uint64_t n_tokens)
     return "";
 }
 
-PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
+PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes, const std::vector<uint64_t> &file_sizes)
 {
     auto fail = [&](msi_status st, std::string m) { set_error(st, std::move(m)); };
     if (d.abi_version != MSI_ABI_VERSION)
@@ -53,11 +55,56 @@ PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes)
             { fail(MSI_E_INVALID_ARG, "null window " + std::to_string(w)); return; }
     if (d.n_objects && !d.objects)
         { fail(MSI_E_INVALID_ARG, "objects missing"); return; }
+    if (d.source && d.n_objects)
+        { fail(MSI_E_INVALID_ARG, "a plan with a source takes its objects from the source's extents"); return; }
 
     n_layers_ = d.n_layers;
     n_experts_ = d.n_experts;
     objects_.assign(size_t(n_layers_) * n_experts_, ObjectInfo{0, 0, 0});
     has_object_.assign(size_t(n_layers_) * n_experts_, 0);
+    if (d.source) {
+        const msi_source_desc &sd = *d.source;
+        if (sd.n_extents && !sd.extents)
+            { fail(MSI_E_INVALID_ARG, "source extents missing"); return; }
+        if (file_sizes.size() != sd.n_files)
+            { fail(MSI_E_INVALID_ARG, "source file sizes unknown"); return; }
+        source_backed_ = true;
+        src_.assign(size_t(n_layers_) * n_experts_, SourceObject{});
+        std::vector<uint32_t> seen(size_t(n_layers_) * n_experts_, 0);   // component bit mask
+        for (uint32_t i = 0; i < sd.n_extents; ++i) {
+            const msi_extent_desc &x = sd.extents[i];
+            const std::string who = "extent " + std::to_string(i);
+            if (x.layer >= n_layers_ || x.expert >= n_experts_ || x.file >= sd.n_files)
+                { fail(MSI_E_INVALID_ARG, who + ": layer/expert/file out of range"); return; }
+            if (x.component >= uint32_t(SourceService::MAX_EXTENTS) || x.nbytes == 0)
+                { fail(MSI_E_INVALID_ARG, who + ": component must be < 4 and the extent non-empty"); return; }
+            if (x.offset > file_sizes[x.file] || x.nbytes > file_sizes[x.file] - x.offset)
+                { fail(MSI_E_SHORT, who + ": extent runs past the end of its file"); return; }
+            const size_t k = size_t(x.layer) * n_experts_ + x.expert;
+            if (seen[k] & (1u << x.component))
+                { fail(MSI_E_INVALID_ARG, who + ": duplicate component of (layer " + std::to_string(x.layer) +
+                                             ", expert " + std::to_string(x.expert) + ")"); return; }
+            seen[k] |= 1u << x.component;
+            src_[k].ext[x.component] = SourceExtent{x.file, x.offset, x.nbytes};
+        }
+        for (size_t k = 0; k < seen.size(); ++k) {
+            if (!seen[k])
+                continue;
+            const uint32_t m = seen[k];
+            if (m & (m + 1))
+                { fail(MSI_E_INVALID_ARG, "object " + std::to_string(k) + ": component indices have a gap"); return; }
+            int n = 0;
+            uint64_t total = 0;
+            while (n < SourceService::MAX_EXTENTS && (m >> n) & 1u)
+                total += src_[k].ext[n++].nbytes;
+            src_[k].n = n;
+            if (total != object_bytes)
+                { fail(MSI_E_SHORT, "object " + std::to_string(k) + ": extents add up to " + std::to_string(total) +
+                                        " bytes, not the object size " + std::to_string(object_bytes)); return; }
+            has_object_[k] = 1;
+            objects_[k] = ObjectInfo{SOURCE_WINDOW, 0, object_bytes};
+        }
+    }
     for (uint32_t i = 0; i < d.n_objects; ++i) {
         const msi_object_desc &o = d.objects[i];
         if (o.layer >= n_layers_ || o.expert >= n_experts_ || o.window >= d.n_windows)
@@ -144,6 +191,42 @@ const FillRecord *PlanCore::fill(int64_t id) const
     return it == fills_.end() ? nullptr : &it->second;
 }
 
+const SourceObject *PlanCore::source_object(uint32_t layer, uint32_t expert) const
+{
+    if (!source_backed_ || layer >= n_layers_ || expert >= n_experts_)
+        return nullptr;
+    const size_t k = size_t(layer) * n_experts_ + expert;
+    return has_object_[k] ? &src_[k] : nullptr;
+}
+
+bool PlanCore::fill_current(int64_t id, uint32_t epoch, uint32_t gen) const
+{
+    auto it = fills_.find(id);
+    if (it == fills_.end() || epoch != epoch_)
+        return false;
+    const Slot &sl = slot(it->second.layer, it->second.slot);
+    return sl.fill_id == id && sl.gen == gen && sl.state == SlotState::Loading;
+}
+
+void PlanCore::fail_fill(int64_t id)
+{
+    auto it = fills_.find(id);
+    if (it == fills_.end())
+        return;
+    const FillRecord rec = it->second;
+    fills_.erase(it);
+    if (rec.window != SOURCE_WINDOW)
+        window_busy_[rec.window]--;
+    stats_.fills_discarded++;
+    Slot &sl = slot(rec.layer, rec.slot);
+    if (sl.fill_id != id)
+        return;
+    sl.fill_id = -1;
+    sl.state = SlotState::Vacant;
+    sl.expert = -1;
+    layer_version_[rec.layer]++;
+}
+
 void PlanCore::rebuild_res_index(uint32_t layer) const
 {
     int32_t *ix = res_index_.data() + size_t(layer) * n_experts_;
@@ -214,7 +297,8 @@ int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
         else
             stats_.fills_published++;
         if (it != fills_.end()) {
-            window_busy_[it->second.window]--;
+            if (it->second.window != SOURCE_WINDOW)
+                window_busy_[it->second.window]--;
             fills_.erase(it);
         }
     }
@@ -235,7 +319,8 @@ int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
     sl.fill_id = r.id;
     layer_version_[layer]++;
     sl.last_use = ++tick_;
-    window_busy_[o.window]++;
+    if (o.window != SOURCE_WINDOW)
+        window_busy_[o.window]++;
     stats_.fills++;
     stats_.h2d_bytes += o.nbytes;
     fills_.emplace(r.id, r);
@@ -310,7 +395,8 @@ void PlanCore::complete_fill(int64_t id)
         return;
     const FillRecord rec = it->second;
     fills_.erase(it);
-    window_busy_[rec.window]--;
+    if (rec.window != SOURCE_WINDOW)
+        window_busy_[rec.window]--;
     Slot &sl = slot(rec.layer, rec.slot);
     if (sl.fill_id != id)
         return;

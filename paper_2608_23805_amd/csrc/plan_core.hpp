@@ -3,10 +3,10 @@
 // Pure C++17, no HIP: the HIP layer (msi_abi.cpp) owns events, streams and
 // device memory and drives this class with explicit calls.  It holds the
 // immutable manifest and the mutable per-slot / per-window state of the
-// paper's Plan (Section 3.1: object, generation, request epoch, readiness,
+// paper's Plan ("A Shared Cross-Adapter Plan Core": object, generation, request epoch, readiness,
 // live-consumer count; replacement policy kept apart from the lifecycle) and
 // the GPU-slot state sequence Vacant -> Loading -> DeviceReady -> InUse ->
-// Recyclable -> Vacant of Section 3.4, with tickets carrying object,
+// Recyclable -> Vacant of "Separate Window and GPU-Slot Lifecycles", with tickets carrying object,
 // generation, epoch and slot.  Host windows are caller-owned pinned buffers
 // that always hold their extents, so of the window sequence only
 // HostReady <-> Copying is tracked (a window is busy while a copy reads it).
@@ -18,6 +18,7 @@
 #include <vector>
 
 #include "../../include/msi.h"
+#include "source.hpp"
 
 namespace msi {
 
@@ -69,15 +70,25 @@ struct Schedule {
 // below 2^31 for bf16 and 4-bit layers; every layer keeps T <= 2^24.
 std::string batch_limit_error(const msi_plan_desc &d, uint64_t n_tokens);
 
+// window of an object that the source service reads from canonical files
+constexpr uint32_t SOURCE_WINDOW = 0xFFFFFFFFu;
+
 struct ObjectInfo {
-    uint32_t window;
+    uint32_t window;           // SOURCE_WINDOW: read from its extents
     uint64_t offset, nbytes;
+};
+
+// Extents of a source-backed object, in component order.
+struct SourceObject {
+    int n = 0;
+    SourceExtent ext[SourceService::MAX_EXTENTS];
 };
 
 class PlanCore {
 public:
-    // Validates the manifest; on failure status() != MSI_OK and error() says why.
-    PlanCore(const msi_plan_desc &d, uint64_t object_bytes);
+    // Validates the manifest; on failure status() != MSI_OK and error() says
+    // why.  file_sizes: sizes of the source's files (plans with a source).
+    PlanCore(const msi_plan_desc &d, uint64_t object_bytes, const std::vector<uint64_t> &file_sizes = {});
 
     msi_status status() const { return status_; }
     const std::string &error() const { return err_; }
@@ -94,7 +105,12 @@ public:
     Slot &slot(uint32_t layer, uint32_t s) { return slots_[layer * pool_slots_ + s]; }
     uint32_t global_slot(uint32_t layer, uint32_t s) const { return layer * pool_slots_ + s; }
     const ObjectInfo *object(uint32_t layer, uint32_t expert) const;
+    const SourceObject *source_object(uint32_t layer, uint32_t expert) const;
+    bool source_backed() const { return source_backed_; }
     const FillRecord *fill(int64_t id) const;
+    // True while fill `id` is the slot's current, same-epoch version (a source
+    // completion carrying this ticket may still be published).
+    bool fill_current(int64_t id, uint32_t epoch, uint32_t gen) const;
 
     // Slot holding a published (or same-epoch loading) version of the object,
     // usable as a hit; -1 if none.  Zero-cache plans never report hits.
@@ -111,6 +127,9 @@ public:
 
     // Completion of a submitted fill observed by the device layer.
     void complete_fill(int64_t fill_id);
+    // A fill whose source request failed (short read, EIO, stale ticket):
+    // never published; its slot goes Vacant.
+    void fail_fill(int64_t fill_id);
 
     // Resolve the demanded experts (ascending ids) of one forward into
     // rounds: hits first, then misses in ascending id; rounds hold at most
@@ -162,6 +181,8 @@ private:
     std::vector<Slot> slots_;
     std::vector<ObjectInfo> objects_;          // [layer * E + expert]
     std::vector<uint8_t> has_object_;
+    std::vector<SourceObject> src_;            // [layer * E + expert], source-backed plans
+    bool source_backed_ = false;
     std::vector<uint32_t> window_busy_;
     std::unordered_map<int64_t, FillRecord> fills_;   // unobserved fills
     std::vector<uint64_t> layer_version_;

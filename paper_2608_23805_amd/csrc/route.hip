@@ -2,7 +2,9 @@
 // token-by-expert permutation, for gfx950.
 //
 // The routed set of each token is the layer's route event (the paper compares
-// every recorded route event bit for bit, Section 2.2 and Section 5.4); here
+// every recorded route event bit for bit: "Exactness Is Scoped by Identity
+// and Horizon" and "Output-Exact Execution Beyond the Full-Residency
+// Envelope"); here
 // it is produced deterministically: fp32 logits (bf16 MFMA products, fp32
 // accumulation, or fp32 FMA for fp32 layers), selection by (logit desc,
 // expert id asc) with one wavefront per token, softmax restricted to the

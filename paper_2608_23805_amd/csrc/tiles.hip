@@ -19,22 +19,24 @@ int tiles_down_tile(int nrows, int d, int I)
     return ring_tiles_down(nrows, d);
 }
 
+// workgroups of a persistent launch: one per compute unit
+static int g_persistent_wgs = 256;
+
 hipError_t launch_gateup_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
+    // (the persistent form is slower for gate/up: its extra state spills registers, and the spill reloads
+    // wait for every copy in flight)
     launch_k(ring_gemm_kernel<RingMode::GateUp>, L.n_tiles, ring::THREADS, 0, s, L);
     return hipGetLastError();
 }
-
-// workgroups of a persistent launch: one per compute unit
-static int g_persistent_wgs = 256;
 
 hipError_t launch_down_tile(const ExpertLaunch &L, hipStream_t s)
 {
     if (L.n_tiles == 0)
         return hipSuccess;
-    if (L.I / ring::SK >= 8 && L.n_tiles > g_persistent_wgs) {
+    if ((L.I / ring::SK) % 4 == 0 && L.I / ring::SK >= 8 && L.n_tiles > g_persistent_wgs) {
         // K loop long enough for the cross-tile pipeline: one workgroup per CU walks its tiles
         launch_k(ring_gemm_persistent<RingMode::Down>, g_persistent_wgs, ring::THREADS, 0, s, L);
     } else {

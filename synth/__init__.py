@@ -23,7 +23,8 @@ An expert object is the concatenation [Wg | Wu | Wd] with Wg, Wu of shape
 (reduction axis I contiguous).  The router weight is stored [E, d].
 
 Workload shapes follow the paper's model (48 MoE layers of 512 experts,
-Section 4 and Section 5.4); expert popularity priors (Dirichlet, Zipf) and
+Implementation, and "Output-Exact Execution Beyond the Full-Residency
+Envelope"); expert popularity priors (Dirichlet, Zipf) and
 the bias temperature are this build's recipe for "every expert receives
 tokens, with uneven counts".
 """
@@ -284,3 +285,43 @@ def layer_inputs(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] =
         shared=expert_object(wl, layer, 0, shared=True) if s.shared else None,
     )
     return li if lazy else li.prefetch()
+
+
+# ----------------------------------------------------------------------------
+# canonical files (storage layout only)
+# ----------------------------------------------------------------------------
+
+def component_sizes(shape: LayerShape):
+    """Byte sizes of an expert object's components [Wg, Wu, Wd]."""
+    if shape.wdtype == "f32":
+        m = lambda r, c: r * c * 4  # noqa: E731
+    elif shape.wdtype == "bf16":
+        m = lambda r, c: r * c * 2  # noqa: E731
+    else:
+        m = q4b32_matrix_nbytes
+    return [m(shape.I, shape.d), m(shape.I, shape.d), m(shape.d, shape.I)]
+
+
+def write_canonical_file(path: str, objects, comp_sizes, seed: int = 0, gap: int = 1000):
+    """Write objects (uint8 arrays, each the concatenation of its components)
+    to one canonical file with every component at its own offset: components
+    in a seeded shuffled order, each followed by ``gap`` filler bytes so that
+    no extent is aligned to the direct-I/O block.  Returns the extents as
+    (object index, component, offset, nbytes) tuples."""
+    import numpy as np
+    order = [(i, c) for i in range(len(objects)) for c in range(len(comp_sizes))]
+    perm = np.random.Generator(np.random.PCG64(np.random.SeedSequence([MASTER, 900, seed]))).permutation(len(order))
+    starts = [0]
+    for c in comp_sizes[:-1]:
+        starts.append(starts[-1] + c)
+    extents, off = [], 0
+    with open(path, "wb") as fh:
+        for j in perm:
+            i, c = order[j]
+            obj = np.asarray(objects[i], dtype=np.uint8)
+            fh.write(obj[starts[c]:starts[c] + comp_sizes[c]].tobytes())
+            extents.append((i, c, off, comp_sizes[c]))
+            off += comp_sizes[c]
+            fh.write(b"\xa5" * gap)
+            off += gap
+    return sorted(extents)

@@ -170,3 +170,21 @@ def workspace_parts(T: int, E: int, K: int, d: int, I: int, wdtype: str) -> dict
         off += a256(n)
     parts["total"] = off
     return parts
+
+
+def make_source_plan(li: synth.LayerInputs, capacity: int, path: str, n_windows: int = 8, inflight: int = 8,
+                     transient: int = 8, seed: int = 0):
+    """Plan over one layer whose expert objects are read from a canonical
+    file (written here: gate, up and down of every expert as separate
+    extents at shuffled, unaligned offsets) through ``n_windows`` staging
+    windows with at most ``inflight`` reads in flight."""
+    import paper_2608_23805_amd as msi
+    s = li.wl.shape
+    comps = synth.component_sizes(s)
+    ext = synth.write_canonical_file(path, [li.expert(e) for e in range(s.E)], comps, seed=seed)
+    extents = [(0, i, c, 0, off, n) for (i, c, off, n) in ext]
+    wbytes = (s.object_bytes() + len(comps) * 8192 + 4095) // 4096 * 4096
+    src = msi.Source([path], extents, n_windows=n_windows, window_bytes=wbytes, inflight=inflight)
+    return msi.Plan(n_layers=1, n_experts=s.E, d_model=s.d, d_ff=s.I, top_k=s.K, wdtype=s.wdtype,
+                    slots_per_layer=capacity, transient_slots=transient if capacity == 0 else 0,
+                    windows=[], objects=[], source=src)

@@ -1,5 +1,6 @@
 """Lifecycle fault cells through the C ABI on the GPU, after the paper's fault
-matrix (Table 5): each cell names the invariant it exercises and checks the
+matrix (the table of prespecified fault modes in "Integrated Deterministic
+Faults"): each cell names the invariant it exercises and checks the
 required observation; every cell ends with a balanced terminal state (no fill
 in flight, no busy window, no live consumer).
 
@@ -216,9 +217,11 @@ def _stale_tile_cell(li, capacity, persistent):
     ctrl = run_layer(plan, dl)
     counts, offsets = ctrl["counts"], ctrl["offsets"]
     tile = [e for e in range(s.E) if counts[e] > 16]
-    down_tiles = sum((int(counts[e]) + 255) // 256 * (s.d // 256) for e in tile) + (s.T + 255) // 256 * (s.d // 256)
-    log(f"stale tile cell: T={s.T} tile experts={len(tile)} down tiles={down_tiles} persistent={persistent}")
-    assert (down_tiles > 256) == persistent, down_tiles
+    row_tiles = sum((int(counts[e]) + 255) // 256 for e in tile) + (s.T + 255) // 256
+    down_tiles, gu_tiles = row_tiles * (s.d // 256), row_tiles * (s.I // 128)
+    log(f"stale tile cell: T={s.T} tile experts={len(tile)} gate/up tiles={gu_tiles} down tiles={down_tiles} "
+        f"persistent={persistent}")
+    assert (down_tiles > 256) == persistent and (gu_tiles > 256) == persistent, (gu_tiles, down_tiles)
     bad, other = tile[0], tile[-1]
     slot = next(q for q in range(capacity) if plan.query(0, q).expert == bad)
     plan.debug_set_device_gen(0, slot, plan.query(0, slot).generation + 1000)
@@ -259,11 +262,12 @@ def test_stale_generation_tile_path():
     _stale_tile_cell(synth.layer_inputs(wl), capacity=32, persistent=False)
 
 
-def test_stale_generation_persistent_down():
-    """Prefill-shaped layer whose down launch exceeds one tile per CU, so the
-    persistent down kernel runs (T = 2048, d = 2048, E = 16, K = 4)."""
+def test_stale_generation_persistent_tiles():
+    """Prefill-shaped layer whose gate/up and down launches exceed one tile
+    per CU, so both persistent tile kernels run (T = 4096, d = 2048, E = 16,
+    K = 4)."""
     log("cell stale_generation_persistent")
-    wl = synth.Workload("cells_persistent_bf16", 20, synth.LayerShape(2048, 2048, 16, 4, 512, "bf16"),
+    wl = synth.Workload("cells_persistent_bf16", 20, synth.LayerShape(4096, 2048, 16, 4, 512, "bf16"),
                         prior="dirichlet", prior_param=2.0, tau=0.2)
     _stale_tile_cell(synth.layer_inputs(wl), capacity=16, persistent=True)
 
