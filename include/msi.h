@@ -132,7 +132,7 @@ typedef struct {
     uint32_t wdtype;             /* msi_wdtype                                */
     uint32_t slots_per_layer;    /* C >= 0; 0 selects zero-cache              */
     uint32_t transient_slots;    /* zero-cache staging slots (0 -> 8), >= 2   */
-    uint32_t reserved0;
+    uint32_t policy;             /* msi_policy: replacement among demand slots */
     void *slot_pool;             /* device, caller-owned                      */
     uint64_t slot_pool_bytes;
     uint64_t slot_stride;        /* >= object bytes, multiple of 256          */
@@ -149,7 +149,23 @@ typedef struct {
      * copied to its slot (states Free -> Reading -> HostReady -> Copying ->
      * Free), so the source holds at most n_windows * window_bytes. */
     const msi_source_desc *source;
+    /* Two-bank prefetch: the last prefetch_slots slots of each layer's pool
+     * form its prefetch bank, filled only by msi_prefetch; demand misses of a
+     * forward go to the other slots (the demand bank), so a wrong prefetch
+     * never evicts a cached object.  0 (no bank) or < slots_per_layer; 0 for
+     * zero-cache plans. */
+    uint32_t prefetch_slots;
+    uint32_t reserved1;
 } msi_plan_desc;
+
+/* Replacement policies (kept apart from the slot lifecycle: "A Shared
+ * Cross-Adapter Plan Core").  LRU: the least recently used slot without
+ * consumers.  PROTECTED_LRU: a segmented LRU -- a hit moves the object into
+ * a protected segment of at most half the demand bank (its least recently
+ * used member drops back when it overflows); victims are the least recently
+ * used unprotected slots first, protected ones only when no other is
+ * left. */
+typedef enum { MSI_POLICY_LRU = 0, MSI_POLICY_PROTECTED_LRU = 1 } msi_policy;
 
 /* Ticket of a fill ("Separate Window and GPU-Slot Lifecycles": tickets carry object, generation, epoch and
  * resource identity). */
@@ -232,6 +248,8 @@ typedef struct {
     uint64_t consumers_live;
     uint32_t epoch;
     uint32_t reserved;
+    uint64_t prefetch_fills;     /* fills issued by msi_prefetch                         */
+    uint64_t prefetch_used;      /* prefetched objects a forward then used               */
 } msi_stats;
 
 /* Kernel kinds of the per-kind timing telemetry. */
@@ -312,6 +330,19 @@ msi_status msi_workspace_size(const msi_plan *plan, uint32_t n_tokens, uint64_t 
  * slot has live consumers, or every slot does), MSI_E_DEVICE. */
 msi_status msi_slot_fill(msi_plan *plan, uint32_t layer, uint32_t expert, int32_t slot,
                          void *side_stream, msi_ticket *ticket);
+
+/* Next-layer prefetch into the layer's prefetch bank (two-bank prefetch,
+ * the mechanism the paper's Qwen natural-utility experiment runs beside its
+ * protected LRU): for each of the n listed experts (host array) that is not
+ * already resident or loading, fill it into the least recently used
+ * prefetch-bank slot without consumers, asynchronously on side_stream (or
+ * through the source), at most prefetch_slots fills per call; *issued (may
+ * be NULL) receives the number of fills.  A later forward finds prefetched
+ * objects as hits.  Errors: MSI_E_INVALID_ARG (no prefetch bank, layer out
+ * of range), MSI_E_WRONG_OBJECT (an expert outside the layer's manifest),
+ * MSI_E_DEVICE. */
+msi_status msi_prefetch(msi_plan *plan, uint32_t layer, const int32_t *experts, uint32_t n, void *side_stream,
+                        uint32_t *issued);
 
 /* Observe completed fills and consumer releases without blocking. */
 msi_status msi_plan_poll(msi_plan *plan);

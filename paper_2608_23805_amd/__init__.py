@@ -32,6 +32,7 @@ STATUS_NAMES = {0: "MSI_OK", -1: "MSI_E_INVALID_ARG", -2: "MSI_E_SHORT", -3: "MS
                 -8: "MSI_E_STATE", -9: "MSI_E_IO"}
 MSI_SOURCE_BUFFERED_OK = 1
 FAULTS = {"short": 1, "eio": 2, "hold": 3}
+POLICIES = {"lru": 0, "protected_lru": 1}
 
 MSI_W_F32, MSI_W_BF16, MSI_W_Q4B32 = 0, 1, 2
 MSI_NOALLOC_SCRATCH_BYTES = 64 << 20
@@ -68,10 +69,11 @@ class msi_source_stats(ctypes.Structure):
 class msi_plan_desc(ctypes.Structure):
     _fields_ = [("abi_version", _u32), ("n_layers", _u32), ("n_experts", _u32), ("d_model", _u32),
                 ("d_ff", _u32), ("top_k", _u32), ("wdtype", _u32), ("slots_per_layer", _u32),
-                ("transient_slots", _u32), ("reserved0", _u32), ("slot_pool", _vp),
+                ("transient_slots", _u32), ("policy", _u32), ("slot_pool", _vp),
                 ("slot_pool_bytes", _u64), ("slot_stride", _u64), ("windows", ctypes.POINTER(_vp)),
                 ("n_windows", _u32), ("n_objects", _u32), ("window_bytes", _u64),
-                ("objects", ctypes.POINTER(msi_object_desc)), ("source", ctypes.POINTER(msi_source_desc))]
+                ("objects", ctypes.POINTER(msi_object_desc)), ("source", ctypes.POINTER(msi_source_desc)),
+                ("prefetch_slots", _u32), ("reserved1", _u32)]
 
 
 class msi_ticket(ctypes.Structure):
@@ -103,7 +105,8 @@ class msi_stats(ctypes.Structure):
     _fields_ = [(n, _u64) for n in ("forwards", "rounds", "fills", "fills_published", "fills_discarded",
                                     "hits", "misses", "evictions", "h2d_bytes", "rejections",
                                     "stale_detected", "fills_in_flight", "windows_busy",
-                                    "consumers_live")] + [("epoch", _u32), ("reserved", _u32)]
+                                    "consumers_live")] + [("epoch", _u32), ("reserved", _u32),
+                                                          ("prefetch_fills", _u64), ("prefetch_used", _u64)]
 
 
 KERNEL_KINDS = ["router_logits", "topk", "permute", "gateup_tile", "gateup_stream", "down_tile",
@@ -121,7 +124,7 @@ EXPORTS = ["msi_residual_init", "msi_residual_add", "msi_plan_set_timing", "msi_
            "msi_moe_forward_noalloc",
            "msi_slot_hold", "msi_slot_unhold", "msi_slot_query", "msi_plan_stats",
            "msi_debug_set_device_gen", "msi_stream_threshold", "msi_source_stats_get",
-           "msi_debug_source_fault", "msi_debug_source_release"]
+           "msi_debug_source_fault", "msi_debug_source_release", "msi_prefetch"]
 
 
 class MsiError(RuntimeError):
@@ -154,6 +157,7 @@ def _load():
     L.msi_source_stats_get.argtypes = [_vp, P(msi_source_stats)]
     L.msi_debug_source_fault.argtypes = [_vp, _u32, _u32, _u32, _u32]
     L.msi_debug_source_release.argtypes = [_vp]
+    L.msi_prefetch.argtypes = [_vp, _u32, P(_i32), _u32, _vp, P(_u32)]
     L.msi_plan_set_timing.argtypes = [_vp, ctypes.c_int]
     L.msi_plan_set_timing_period.argtypes = [_vp, _u32]
     L.msi_residual_init.argtypes = [_vp, _vp, _vp, _u32, _u32, _vp]
@@ -265,7 +269,8 @@ class Plan:
     def __init__(self, *, n_layers: int, n_experts: int, d_model: int, d_ff: int, top_k: int,
                  wdtype: str, slots_per_layer: int, windows: Sequence, objects: Sequence[Tuple],
                  transient_slots: int = 0, slot_stride: Optional[int] = None, device="cuda",
-                 slot_pool=None, source: Optional["Source"] = None):
+                 slot_pool=None, source: Optional["Source"] = None, policy: str = "lru",
+                 prefetch_slots: int = 0):
         import torch
         self.wdtype = wdtype
         self.n_layers, self.n_experts, self.d, self.I, self.K = n_layers, n_experts, d_model, d_ff, top_k
@@ -290,14 +295,15 @@ class Plan:
         desc = msi_plan_desc(
             abi_version=MSI_ABI_VERSION, n_layers=n_layers, n_experts=n_experts, d_model=d_model,
             d_ff=d_ff, top_k=top_k, wdtype=WDTYPE[wdtype], slots_per_layer=slots_per_layer,
-            transient_slots=transient_slots, reserved0=0, slot_pool=self.slot_pool_ptr,
+            transient_slots=transient_slots, policy=POLICIES[policy], slot_pool=self.slot_pool_ptr,
             slot_pool_bytes=self.slot_pool_bytes, slot_stride=self.slot_stride,
             windows=ctypes.cast(self._win_ptrs, ctypes.POINTER(_vp)), n_windows=len(self.windows),
             n_objects=len(objects),
             window_bytes=(source.window_bytes if source is not None else
                           (self.windows[0].numel() if self.windows else 0)),
             objects=ctypes.cast(self._objs, ctypes.POINTER(msi_object_desc)),
-            source=ctypes.pointer(source.c()) if source is not None else None)
+            source=ctypes.pointer(source.c()) if source is not None else None,
+            prefetch_slots=prefetch_slots, reserved1=0)
         h = _vp()
         _check(lib.msi_plan_create(ctypes.byref(desc), ctypes.byref(h)))
         self.h = h
@@ -407,6 +413,14 @@ class Plan:
 
     def debug_set_device_gen(self, layer: int, slot: int, gen: int):
         _check(lib.msi_debug_set_device_gen(self.h, layer, slot, gen))
+
+    def prefetch(self, layer: int, experts, side_stream=None) -> int:
+        """msi_prefetch: fill the listed experts into the layer's prefetch bank; returns the fills issued."""
+        ids = [int(e) for e in experts]
+        arr = (_i32 * max(1, len(ids)))(*ids)
+        n = _u32()
+        _check(lib.msi_prefetch(self.h, layer, arr, len(ids), _stream(side_stream), ctypes.byref(n)))
+        return n.value
 
     def source_stats(self) -> dict:
         s = msi_source_stats()

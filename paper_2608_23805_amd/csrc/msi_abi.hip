@@ -857,6 +857,57 @@ msi_status msi_slot_fill(msi_plan *p, uint32_t layer, uint32_t expert, int32_t s
     return MSI_OK;
 }
 
+msi_status msi_prefetch(msi_plan *p, uint32_t layer, const int32_t *experts, uint32_t n, void *side_stream,
+                        uint32_t *issued)
+{
+    if (issued)
+        *issued = 0;
+    if (!p || (n && !experts))
+        return fail(MSI_E_INVALID_ARG, "null argument");
+    HIP_OK(hipSetDevice(p->device));
+    poll_fills(p);
+    std::vector<int64_t> ids;
+    const msi_status st = p->core->request_prefetch(layer, std::vector<int32_t>(experts, experts + n), &ids);
+    if (st != MSI_OK)
+        return fail(st, p->core->error());
+    hipStream_t side = static_cast<hipStream_t>(side_stream);
+    if (p->src) {
+        for (int64_t id : ids) {
+            msi_plan::SrcFill f;
+            f.rec = *p->core->fill(id);
+            f.side = side;
+            f.round = -1;
+            p->sfills.push_back(f);
+        }
+        const msi_status pst = source_progress(p, 0);
+        if (pst != MSI_OK && pst != MSI_E_SHORT && pst != MSI_E_IO && pst != MSI_E_STALE)
+            return pst;
+    } else if (!ids.empty()) {
+        std::vector<FillRecord> fills;
+        for (int64_t id : ids)
+            fills.push_back(*p->core->fill(id));
+        const msi_status est = enqueue_fills(p, layer, fills, side);
+        if (est != MSI_OK)
+            return est;
+        // one owned event per filled slot, recorded after the whole batch
+        for (const FillRecord &fr : fills) {
+            const uint32_t gs = p->core->global_slot(layer, fr.slot);
+            hipEvent_t ev = p->get_event();
+            if (!ev)
+                return fail(MSI_E_DEVICE, "event creation failed");
+            HIP_OK(hipEventRecord(ev, side));
+            if (p->fill_ev[gs] && !p->fill_ev_shared[gs])
+                p->free_events.push_back(p->fill_ev[gs]);
+            p->fill_ev[gs] = ev;
+            p->fill_ev_id[gs] = fr.id;
+            p->fill_ev_shared[gs] = 0;
+        }
+    }
+    if (issued)
+        *issued = uint32_t(ids.size());
+    return MSI_OK;
+}
+
 msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
 {
     if (!p || !a)

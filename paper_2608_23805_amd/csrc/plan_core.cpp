@@ -41,6 +41,12 @@ PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes, const std::vec
     pool_slots_ = zero_cache_ ? (d.transient_slots ? d.transient_slots : 8u) : d.slots_per_layer;
     if (zero_cache_ && pool_slots_ < 2)
         { fail(MSI_E_INVALID_ARG, "transient_slots must be >= 2"); return; }
+    if (d.policy > MSI_POLICY_PROTECTED_LRU)
+        { fail(MSI_E_INVALID_ARG, "unknown replacement policy"); return; }
+    policy_ = d.policy;
+    if (d.prefetch_slots && (zero_cache_ || d.prefetch_slots >= pool_slots_))
+        { fail(MSI_E_INVALID_ARG, "prefetch_slots must be below slots_per_layer (and 0 for zero-cache)"); return; }
+    prefetch_slots_ = d.prefetch_slots;
     if (d.slot_stride < object_bytes || d.slot_stride % 256 != 0)
         { fail(MSI_E_INVALID_ARG, "slot_stride must be >= the object size and a multiple of 256"); return; }
     if (!d.slot_pool || reinterpret_cast<uintptr_t>(d.slot_pool) % 256 != 0)
@@ -170,7 +176,7 @@ void PlanCore::note_direct_hits(uint32_t layer, const std::vector<int32_t> &dema
     for (int32_t e : demanded) {
         const int32_t s = resident_slot(layer, uint32_t(e));
         if (s >= 0)
-            slot(layer, uint32_t(s)).last_use = ++tick_;
+            touch(layer, uint32_t(s));
         stats_.hits++;
     }
     stats_.rounds++;
@@ -265,21 +271,87 @@ int32_t PlanCore::resident_slot(uint32_t layer, uint32_t expert) const
     return res_index_[size_t(layer) * n_experts_ + expert];
 }
 
-int32_t PlanCore::choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude) const
+int32_t PlanCore::choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude, bool prefetch) const
 {
     int32_t best = -1;
     uint64_t best_key = std::numeric_limits<uint64_t>::max();
-    for (uint32_t s = 0; s < pool_slots_; ++s) {
+    const uint32_t s0 = prefetch ? demand_slots() : 0, s1 = prefetch ? pool_slots_ : demand_slots();
+    for (uint32_t s = s0; s < s1; ++s) {
         const Slot &sl = slot(layer, s);
         if (sl.holds > 0 || (!exclude.empty() && exclude[s]))
             continue;
-        const uint64_t key = sl.state == SlotState::Vacant ? 0 : sl.last_use + 1;
+        uint64_t key = sl.state == SlotState::Vacant ? 0 : sl.last_use + 1;
+        if (!prefetch && policy_ == MSI_POLICY_PROTECTED_LRU && sl.prot && sl.state != SlotState::Vacant)
+            key += uint64_t(1) << 62;          // protected: only when no unprotected slot is left
         if (key < best_key) {
             best_key = key;
             best = int32_t(s);
         }
     }
     return best;
+}
+
+void PlanCore::touch(uint32_t layer, uint32_t s)
+{
+    Slot &sl = slot(layer, s);
+    sl.last_use = ++tick_;
+    if (sl.prefetched) {
+        sl.prefetched = false;
+        stats_.prefetch_used++;
+    }
+    if (policy_ != MSI_POLICY_PROTECTED_LRU || in_prefetch_bank(s) || sl.prot)
+        return;
+    sl.prot = true;
+    // the protected segment holds at most half of the demand bank: its least
+    // recently used member returns to the unprotected one
+    uint32_t n = 0;
+    int32_t lru = -1;
+    for (uint32_t q = 0; q < demand_slots(); ++q) {
+        const Slot &o = slot(layer, q);
+        if (!o.prot)
+            continue;
+        ++n;
+        if (lru < 0 || o.last_use < slot(layer, uint32_t(lru)).last_use)
+            lru = int32_t(q);
+    }
+    if (n > std::max(1u, demand_slots() / 2))
+        slot(layer, uint32_t(lru)).prot = false;
+}
+
+msi_status PlanCore::request_prefetch(uint32_t layer, const std::vector<int32_t> &experts, std::vector<int64_t> *ids)
+{
+    ids->clear();
+    if (layer >= n_layers_ || prefetch_slots_ == 0) {
+        set_error(MSI_E_INVALID_ARG, "layer out of range or the plan has no prefetch bank");
+        return MSI_E_INVALID_ARG;
+    }
+    for (int32_t e : experts)
+        if (e < 0 || !object(layer, uint32_t(e))) {
+            stats_.rejections++;
+            set_error(MSI_E_WRONG_OBJECT, "prefetch of an expert outside the layer's manifest");
+            return MSI_E_WRONG_OBJECT;
+        }
+    std::vector<uint8_t> exclude(pool_slots_, 0);
+    for (int32_t e : experts) {                 // listed objects already in the bank stay
+        const int32_t r = resident_slot(layer, uint32_t(e));
+        if (r >= 0)
+            exclude[r] = 1;
+    }
+    for (int32_t e : experts) {
+        if (ids->size() >= prefetch_slots_)
+            break;
+        if (resident_slot(layer, uint32_t(e)) >= 0)
+            continue;                        // resident or already loading: nothing to do
+        const int32_t v = choose_victim(layer, exclude, true);
+        if (v < 0 || slot(layer, uint32_t(v)).consumers > 0)
+            break;
+        exclude[v] = 1;
+        const int64_t id = new_fill(layer, uint32_t(v), uint32_t(e));
+        slot(layer, uint32_t(v)).prefetched = true;
+        stats_.prefetch_fills++;
+        ids->push_back(id);
+    }
+    return MSI_OK;
 }
 
 int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
@@ -317,6 +389,8 @@ int64_t PlanCore::new_fill(uint32_t layer, uint32_t s, uint32_t expert)
     sl.epoch = epoch_;
     sl.state = SlotState::Loading;
     sl.fill_id = r.id;
+    sl.prot = false;
+    sl.prefetched = false;
     layer_version_[layer]++;
     sl.last_use = ++tick_;
     if (o.window != SOURCE_WINDOW)
@@ -350,7 +424,7 @@ msi_status PlanCore::request_fill(uint32_t layer, uint32_t expert, int32_t force
     const int32_t r = resident_slot(layer, expert);
     if (r >= 0 && (forced_slot < 0 || forced_slot == r)) {
         Slot &sl = slot(layer, uint32_t(r));
-        sl.last_use = ++tick_;
+        touch(layer, uint32_t(r));
         stats_.hits++;
         *t = msi_ticket{layer, expert, r, sl.gen, sl.epoch, 1u};
         return MSI_OK;
@@ -430,17 +504,22 @@ msi_status PlanCore::schedule_forward(uint32_t layer, const std::vector<int32_t>
         }
         (resident_slot(layer, uint32_t(e)) >= 0 ? hits : misses).push_back(e);
     }
+    // rounds are sized by the demand bank: misses fill only there, hits in the
+    // prefetch bank take no demand slot
+    const uint32_t A = demand_slots();
     uint32_t eligible = 0;
-    for (uint32_t s = 0; s < pool_slots_; ++s)
+    for (uint32_t s = 0; s < A; ++s)
         eligible += slot(layer, s).holds == 0;
     if (!misses.empty() && eligible == 0) {
         stats_.rejections++;
         set_error(MSI_E_BUSY, "no slot of the layer can be freed (all held)");
         return MSI_E_BUSY;
     }
-    const size_t n = hits.size() + misses.size();
-    uint32_t R = n <= pool_slots_ ? pool_slots_ : std::max(1u, pool_slots_ / 2);
-    R = std::max(1u, std::min(R, eligible ? eligible : pool_slots_));
+    size_t n = misses.size();
+    for (int32_t e : hits)
+        n += !in_prefetch_bank(uint32_t(resident_slot(layer, uint32_t(e))));
+    uint32_t R = n <= A ? A : std::max(1u, A / 2);
+    R = std::max(1u, std::min(R, eligible ? eligible : A));
 
     size_t hi = 0, mi = 0;
     while (hi < hits.size() || mi < misses.size()) {
@@ -449,7 +528,7 @@ msi_status PlanCore::schedule_forward(uint32_t layer, const std::vector<int32_t>
         uint32_t taken = 0;      // eligible slots this round occupies
         while (hi < hits.size()) {
             const int32_t s = resident_slot(layer, uint32_t(hits[hi]));
-            const bool el = slot(layer, uint32_t(s)).holds == 0;
+            const bool el = slot(layer, uint32_t(s)).holds == 0 && !in_prefetch_bank(uint32_t(s));
             if (el && taken + 1 > R)
                 break;
             exclude[s] = 1;
@@ -479,7 +558,12 @@ msi_status PlanCore::schedule_forward(uint32_t layer, const std::vector<int32_t>
         for (const SchedItem &it : round.items) {
             Slot &sl = slot(layer, uint32_t(it.slot));
             sl.consumers++;
-            sl.last_use = ++tick_;
+            const bool filled = std::any_of(round.fills.begin(), round.fills.end(),
+                                            [&](const FillRecord &f) { return int32_t(f.slot) == it.slot; });
+            if (filled)
+                sl.last_use = ++tick_;
+            else
+                touch(layer, uint32_t(it.slot));     // a hit
             if (sl.state != SlotState::Loading)
                 sl.state = SlotState::InUse;
         }

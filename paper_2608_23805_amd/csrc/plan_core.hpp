@@ -39,6 +39,8 @@ struct Slot {
     uint32_t holds = 0;        // consumers held through the API
     uint64_t last_use = 0;     // LRU tick
     int64_t fill_id = -1;      // unobserved fill targeting this slot, -1 if none
+    bool prot = false;         // protected segment (protected LRU)
+    bool prefetched = false;   // filled by a prefetch and not used yet
 };
 
 struct FillRecord {
@@ -116,9 +118,17 @@ public:
     // usable as a hit; -1 if none.  Zero-cache plans never report hits.
     int32_t resident_slot(uint32_t layer, uint32_t expert) const;
 
-    // Least recently used slot of `layer` that has no holds and is not in
-    // `exclude` (one flag per pool slot); -1 if none.
-    int32_t choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude) const;
+    // Victim among the demand bank's slots of `layer` (all slots without a
+    // prefetch bank) that have no holds and are not in `exclude` (one flag
+    // per pool slot), by the plan's policy; -1 if none.  prefetch: choose in
+    // the prefetch bank instead (least recently used).
+    int32_t choose_victim(uint32_t layer, const std::vector<uint8_t> &exclude, bool prefetch = false) const;
+    uint32_t demand_slots() const { return pool_slots_ - prefetch_slots_; }
+    bool in_prefetch_bank(uint32_t s) const { return s >= pool_slots_ - prefetch_slots_; }
+
+    // Prefetch (msi_prefetch): fills for the listed experts not resident or
+    // loading, into the prefetch bank, at most its size.  Fill ids in *ids.
+    msi_status request_prefetch(uint32_t layer, const std::vector<int32_t> &experts, std::vector<int64_t> *ids);
 
     // Explicit fill (msi_slot_fill).  On MSI_OK *t is the ticket and, unless
     // t->hit, *fill_id the new fill to submit.
@@ -171,10 +181,12 @@ public:
 private:
     int64_t new_fill(uint32_t layer, uint32_t s, uint32_t expert);
     void publish_state(Slot &sl);
+    void touch(uint32_t layer, uint32_t s);    // a use: LRU tick, protection, prefetch accounting
 
     msi_status status_ = MSI_OK;
     std::string err_;
-    uint32_t n_layers_ = 0, n_experts_ = 0, pool_slots_ = 0;
+    uint32_t n_layers_ = 0, n_experts_ = 0, pool_slots_ = 0, prefetch_slots_ = 0;
+    uint32_t policy_ = MSI_POLICY_LRU;
     bool zero_cache_ = false;
     uint32_t epoch_ = 0;
     uint64_t tick_ = 0;

@@ -17,7 +17,7 @@ from _gpu_helpers import to_device
 
 class Stack:
     def __init__(self, wl: synth.Workload, capacity: int, n_layers: int = None, per_window: int = 8,
-                 pool: synth.LayerInputs = None):
+                 pool: synth.LayerInputs = None, policy: str = "lru", prefetch_slots: int = 0):
         import torch
         import paper_2608_23805_amd as msi
         s = wl.shape
@@ -34,7 +34,10 @@ class Stack:
             entries += [(l, e, *loc[int(m[e])]) for e in range(s.E)]
         self.plan = msi.Plan(n_layers=self.L, n_experts=s.E, d_model=s.d, d_ff=s.I, top_k=s.K,
                              wdtype=s.wdtype, slots_per_layer=capacity,
-                             transient_slots=8 if capacity == 0 else 0, windows=wins, objects=entries)
+                             transient_slots=8 if capacity == 0 else 0, windows=wins, objects=entries,
+                             policy=policy, prefetch_slots=prefetch_slots)
+        self.prefetch_slots = prefetch_slots
+        self.r_next = msi.Routing.alloc(s.T, s.K, s.E) if prefetch_slots else None
         self.wr, self.bias, self.shared = [], [], []
         for l in range(self.L):
             self.wr.append(to_device(synth.router_weight(wl, l), s.xdtype))
@@ -47,16 +50,32 @@ class Stack:
         self.h = torch.empty((s.T, s.d), dtype=torch.float32, device="cuda")
         self.x = torch.empty_like(self.x0)
 
-    def run(self, compute=None, side=None, capture=()):
+    def predict_next(self, l: int, compute):
+        """Next-layer prediction for two-bank prefetch: layer l + 1's router on
+        layer l's input; its demanded experts, most tokens first (ties by
+        id), at most the prefetch bank's size, are prefetched into layer
+        l + 1's bank while layer l runs."""
+        import numpy as np
+        self.plan.route(self.x, self.wr[l + 1], self.bias[l + 1], self.r_next, self.ws, compute)
+        counts = self.r_next.counts.cpu().numpy()
+        dem = np.nonzero(counts)[0]
+        order = dem[np.lexsort((dem, -counts[dem]))]
+        return [int(e) for e in order[:self.prefetch_slots]]
+
+    def run(self, compute=None, side=None, capture=(), x0=None):
         """One pass over every layer; returns {layer: (x_l bf16, out_l, h_l,
-        x_{l+1} bf16)} for the captured layers (host copies)."""
+        x_{l+1} bf16)} for the captured layers (host copies).  With a
+        prefetch bank, each layer first prefetches the next layer's predicted
+        experts.  x0: the stack's input (default: the workload's)."""
         import torch
         import paper_2608_23805_amd as msi
         compute = compute or torch.cuda.current_stream()
         side = side or torch.cuda.Stream()
-        msi.residual_init(self.x0, self.h, self.x, compute)
+        msi.residual_init(self.x0 if x0 is None else x0, self.h, self.x, compute)
         caps = {}
         for l in range(self.L):
+            if self.prefetch_slots and l + 1 < self.L:
+                self.plan.prefetch(l + 1, self.predict_next(l, compute), side)
             self.plan.route(self.x, self.wr[l], self.bias[l], self.r, self.ws, compute)
             self.plan.forward(l, self.x, self.r, self.shared[l], self.out, self.ws, compute, side)
             if l in capture:

@@ -242,9 +242,103 @@ static void test_batch_limits()
     CHECK(!batch_limit_error(d, 1u << 22).empty());        // exactly 2^31 bytes
 }
 
+static void fill_and_complete(PlanCore &c, uint32_t e)
+{
+    msi_ticket t{};
+    int64_t id = -1;
+    CHECK(c.request_fill(0, e, -1, &t, &id) == MSI_OK);
+    if (id >= 0)
+        c.complete_fill(id);
+}
+
+static int32_t slot_of(const PlanCore &c, uint32_t e)
+{
+    for (uint32_t s = 0; s < c.pool_slots(); ++s)
+        if (c.slot(0, s).expert == int32_t(e))
+            return int32_t(s);
+    return -1;
+}
+
+// Protected LRU resists a scan: an object hit once stays while a run of
+// single-use objects passes through; plain LRU evicts it.
+static void test_protected_lru()
+{
+    for (uint32_t policy : {uint32_t(MSI_POLICY_LRU), uint32_t(MSI_POLICY_PROTECTED_LRU)}) {
+        Fixture f(1, 8, 4);
+        f.d.policy = policy;
+        PlanCore c(f.d, OB);
+        CHECK(c.status() == MSI_OK);
+        for (uint32_t e = 0; e < 4; ++e)
+            fill_and_complete(c, e);
+        fill_and_complete(c, 0);                 // a hit: protected under PROTECTED_LRU
+        CHECK(c.stats().hits == 1);
+        for (uint32_t e = 4; e < 8; ++e)
+            fill_and_complete(c, e);             // a scan of single-use objects
+        const bool kept = slot_of(c, 0) >= 0;
+        CHECK(kept == (policy == MSI_POLICY_PROTECTED_LRU));
+    }
+    // the protected segment is at most half the pool
+    Fixture f(1, 8, 4);
+    f.d.policy = MSI_POLICY_PROTECTED_LRU;
+    PlanCore c(f.d, OB);
+    for (uint32_t e = 0; e < 4; ++e)
+        fill_and_complete(c, e);
+    for (uint32_t e = 0; e < 4; ++e)
+        fill_and_complete(c, e);                 // all hit once
+    uint32_t prot = 0;
+    for (uint32_t s = 0; s < 4; ++s)
+        prot += c.slot(0, s).prot;
+    CHECK(prot == 2);
+    Fixture bad(1, 8, 4);
+    bad.d.policy = 7;
+    CHECK(PlanCore(bad.d, OB).status() == MSI_E_INVALID_ARG);
+}
+
+// Two-bank prefetch: prefetches fill only the prefetch bank (at most its
+// size per call), a forward finds them as hits, and demand misses never
+// take a prefetch-bank slot.
+static void test_prefetch_bank()
+{
+    Fixture f(1, 16, 6);
+    f.d.prefetch_slots = 2;
+    PlanCore c(f.d, OB);
+    CHECK(c.status() == MSI_OK && c.demand_slots() == 4);
+    std::vector<int64_t> ids;
+    CHECK(c.request_prefetch(0, {10, 11, 12}, &ids) == MSI_OK);
+    CHECK(ids.size() == 2);
+    for (int64_t id : ids) {
+        CHECK(c.fill(id)->slot >= 4);
+        c.complete_fill(id);
+    }
+    CHECK(slot_of(c, 10) >= 4 && slot_of(c, 11) >= 4 && slot_of(c, 12) < 0);
+    Schedule s;
+    CHECK(c.schedule_forward(0, {1, 2, 3, 4, 10}, &s) == MSI_OK);
+    for (const SchedRound &r : s.rounds)
+        for (const FillRecord &fr : r.fills)
+            CHECK(fr.slot < 4);
+    for (const SchedRound &r : s.rounds)
+        for (const FillRecord &fr : r.fills)
+            c.complete_fill(fr.id);
+    c.end_forward(0, s);
+    CHECK(c.stats().prefetch_fills == 2 && c.stats().prefetch_used == 1);
+    // a listed object already in the bank stays; the other takes the bank's LRU slot
+    CHECK(c.request_prefetch(0, {11, 13}, &ids) == MSI_OK);
+    CHECK(ids.size() == 1 && c.fill(ids[0])->expert == 13);
+    c.complete_fill(ids[0]);
+    CHECK(slot_of(c, 11) >= 4 && slot_of(c, 13) >= 4 && slot_of(c, 10) < 0);
+    // no bank: refused; bank as large as the pool: refused at creation
+    Fixture g(1, 16, 6);
+    PlanCore nb(g.d, OB);
+    CHECK(nb.request_prefetch(0, {1}, &ids) == MSI_E_INVALID_ARG);
+    g.d.prefetch_slots = 6;
+    CHECK(PlanCore(g.d, OB).status() == MSI_E_INVALID_ARG);
+}
+
 int main()
 {
     test_manifest();
+    test_protected_lru();
+    test_prefetch_bank();
     test_batch_limits();
     test_fill_hit_lru();
     test_holds();

@@ -41,7 +41,7 @@ def _desc(msi, **over):
     objs = over.pop("objects", [(0, e, 0, e * ob, ob) for e in range(E)])
     arr = (msi.msi_object_desc * len(objs))(*[msi.msi_object_desc(l, e, w, 0, o, n) for l, e, w, o, n in objs])
     kw = dict(abi_version=msi.MSI_ABI_VERSION, n_layers=1, n_experts=E, d_model=d, d_ff=I, top_k=2,
-              wdtype=msi.MSI_W_BF16, slots_per_layer=2, transient_slots=0, reserved0=0,
+              wdtype=msi.MSI_W_BF16, slots_per_layer=2, transient_slots=0, policy=0,
               slot_pool=1 << 20, slot_pool_bytes=2 * ob + 4096, slot_stride=(ob + 255) // 256 * 256,
               windows=ctypes.cast(wins, ctypes.POINTER(ctypes.c_void_p)), n_windows=1, n_objects=len(objs),
               window_bytes=4 * ob, objects=ctypes.cast(arr, ctypes.POINTER(msi.msi_object_desc)))
@@ -123,7 +123,7 @@ def _source_create(msi, tmp_path, ext_over=None, over=None, src_over=None, win_b
     src = msi.msi_source_desc(**skw)
     objs = (msi.msi_object_desc * 1)(msi.msi_object_desc(0, 0, 0, 0, 0, ob))
     kw = dict(abi_version=msi.MSI_ABI_VERSION, n_layers=1, n_experts=E, d_model=d, d_ff=I, top_k=2,
-              wdtype=msi.MSI_W_BF16, slots_per_layer=2, transient_slots=0, reserved0=0,
+              wdtype=msi.MSI_W_BF16, slots_per_layer=2, transient_slots=0, policy=0,
               slot_pool=1 << 20, slot_pool_bytes=2 * ob + 4096, slot_stride=(ob + 255) // 256 * 256,
               windows=ctypes.cast(wins, ctypes.POINTER(ctypes.c_void_p)), n_windows=1, n_objects=0,
               window_bytes=wb, objects=ctypes.cast(objs, ctypes.POINTER(msi.msi_object_desc)),
