@@ -263,6 +263,23 @@ __device__ __forceinline__ void block_scan_1024(int32_t *part)
     }
 }
 
+// Work counts of a launch whose work list was built on the device: the grid
+// is an upper bound and each workgroup reads the list's length.
+struct DevCount {
+    int32_t n_items;
+    int32_t n_tiles;
+};
+
+// Tile of workgroup b when n tiles exist and the grid may be larger: XCD x
+// (b % 8) walks tiles [x per, (x + 1) per), per = ceil(n / 8), so the real
+// tiles spread over every XCD however large the grid; -1 past the end.
+__device__ __forceinline__ int xcd_tile(int b, int n)
+{
+    const int per = (n + 7) >> 3;
+    const int q = b >> 3, t = (b & 7) * per + q;
+    return (q < per && t < n) ? t : -1;
+}
+
 // Logical tile index with consecutive tiles kept on one XCD: hardware hands
 // workgroup b to XCD b % 8, so XCD x walks tiles [x*per, (x+1)*per).
 __device__ __forceinline__ int xcd_swizzle(int b, int n)

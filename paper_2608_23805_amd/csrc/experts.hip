@@ -62,9 +62,10 @@ __device__ __forceinline__ StreamTile stream_tile(const ExpertLaunch &L, int per
         st.valid = st.it.nrows > 0;       // nrows 0: unpublished expert, no work
         return st;
     }
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
+    int n_items, n_tiles;
+    const int t = launch_tile(L, n_items, n_tiles);
     const int i = t / per_item;
-    if (i >= L.n_items)
+    if (t < 0 || i >= n_items)
         return st;
     st.it = L.items[i];
     st.local = t - i * per_item;

@@ -68,8 +68,11 @@ __device__ __forceinline__ bool q4_tile(const ExpertLaunch &L, int per_item, int
         t = i * per_item + local;
         return direct_item(L.direct, i, per_item, L.status, it);
     }
-    t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    it = L.items[find_item(L.items, L.n_items, t)];
+    int n_items, n_tiles;
+    t = launch_tile(L, n_items, n_tiles);
+    if (t < 0)
+        return false;
+    it = L.items[find_item(L.items, n_items, t)];
     return true;
 }
 
@@ -321,6 +324,18 @@ int tiles_down_q4_tile(int nrows, int d, int I)
     return ((nrows + q4t::BM - 1) / q4t::BM) * (d / q4t::BN);
 }
 
+TileGeom geom_gateup_q4_tile(int d, int I)
+{
+    (void)d;
+    return TileGeom{q4t::BM, I / 64};
+}
+
+TileGeom geom_down_q4_tile(int d, int I)
+{
+    (void)I;
+    return TileGeom{q4t::BM, d / q4t::BN};
+}
+
 // GATEUP: tile columns 0..63 are gate rows nt*64 .. nt*64+63, columns 64..127 the
 // matching up rows; wavefront (wm, wn) owns rows wm*64.., gate columns
 // wn*32.. and the matching up columns, so SiLU * up forms in registers.
@@ -329,8 +344,11 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
 {
     using namespace q4t;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds8[];
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = L.items[find_item(L.items, L.n_items, t)];
+    int n_items, n_tiles;
+    const int t = launch_tile(L, n_items, n_tiles);
+    if (t < 0)
+        return;                                   // past the device-built list's tiles
+    const WorkItem it = L.items[find_item(L.items, n_items, t)];
     if (!slot_current(it, L.gen_dev, L.status))
         return;
     const bool sh = it.slot < 0;

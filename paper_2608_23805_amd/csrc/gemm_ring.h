@@ -228,8 +228,11 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_kernel(ExpertLaunc
     constexpr bool RT = MODE == RingMode::Router;     // router logits: one item of T token rows, E router rows
     __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * STAGE];
 
-    const int t = xcd_swizzle(int(blockIdx.x), int(gridDim.x));
-    const WorkItem it = RT ? WorkItem{-1, -1, 0u, 0, L.T, 0} : L.items[find_item(L.items, L.n_items, t)];
+    int n_items = 1, n_tiles = 0;
+    const int t = RT ? xcd_swizzle(int(blockIdx.x), int(gridDim.x)) : launch_tile(L, n_items, n_tiles);
+    if (t < 0)
+        return;                                   // past the device-built list's tiles
+    const WorkItem it = RT ? WorkItem{-1, -1, 0u, 0, L.T, 0} : L.items[find_item(L.items, n_items, t)];
     if (!RT && !slot_current(it, L.gen_dev, L.status))
         return;
     const int d = L.d, I = L.I;
@@ -418,10 +421,10 @@ __device__ __forceinline__ const MSI_SCALAR_AS T *scalar_view(const T *p)
 }
 
 template <RingMode MODE>
-__device__ __forceinline__ RingTile ring_tile_at(const ExpertLaunch &L, int t, int ii)
+__device__ __forceinline__ RingTile ring_tile_at(const ExpertLaunch &L, int t, int ii, int n_items)
 {
     const auto *items = scalar_view(L.items);
-    while (ii + 1 < L.n_items && items[ii + 1].tile0 <= t)   // items are sorted by tile0
+    while (ii + 1 < n_items && items[ii + 1].tile0 <= t)   // items are sorted by tile0
         ++ii;
     const WorkItem w = items[ii];
     constexpr bool GU = MODE == RingMode::GateUp;
@@ -459,7 +462,8 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
     const int d = L.d, I = L.I;
     const int K = GU ? d : I;
     const int nstage = K / SK;
-    const int n = L.n_tiles;
+    const int n = L.dev_n ? __builtin_amdgcn_readfirstlane(L.dev_n->n_tiles) : L.n_tiles;
+    const int n_items = L.dev_n ? __builtin_amdgcn_readfirstlane(L.dev_n->n_items) : L.n_items;
     const int nwg = int(gridDim.x), b = int(blockIdx.x);
     int t, tend, tstep;
     if (nwg % 8 == 0) {
@@ -554,7 +558,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
     using W_STEADY = std::integral_constant<int, LP * (NBUF - 3)>;   // stage s+1 landed, s+2 in flight
 
     // ---- first tile (blocking)
-    RingTile cur = ring_tile_at<MODE>(L, t, find_item(L.items, L.n_items, t));
+    RingTile cur = ring_tile_at<MODE>(L, t, find_item(L.items, n_items, t), n_items);
     bool cur_ok = cur.sh || scalar_view(L.gen_dev)[cur.slot] == cur.gen;
     uint32_t aoff[LA];
     a_offsets(cur, aoff, false);
@@ -621,7 +625,7 @@ __global__ void __launch_bounds__(ring::THREADS, 1) ring_gemm_persistent(ExpertL
         // the next tile's item (scalar loads; first used by step 2's extra copy)
         const int tn = t + tstep;
         const bool has_next = tn < tend;
-        const RingTile nxt = has_next ? ring_tile_at<MODE>(L, tn, cur.ii) : cur;
+        const RingTile nxt = has_next ? ring_tile_at<MODE>(L, tn, cur.ii, n_items) : cur;
         const bool nxt_ok = nxt.sh || !has_next || scalar_view(L.gen_dev)[nxt.slot] == nxt.gen;
 
         using S0 = std::integral_constant<int, 0>;

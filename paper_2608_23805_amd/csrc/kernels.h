@@ -108,12 +108,58 @@ struct ExpertLaunch {
     // the grid (n_tiles) is then an upper bound and workgroups past the last
     // item exit.  direct.demand null: `items` is the list.
     DirectList direct;
+    // device-built work list: when set, the list's length (items, tiles) is
+    // read from here and the grid (n_tiles on the host) is an upper bound
+    const DevCount *dev_n;
     // router logits launches (ring tiles in router mode) only: x [T, d] tokens,
     // wbase the router weight [E, d], logits[t, e] = x[t] . Wr[e] + bias[e]
     const float *bias;
     float *logits;
     int T, E;
 };
+
+// Tile of this workgroup and the launch's work counts: from the device-built
+// list (L.dev_n; the grid is an upper bound, tiles spread over the XCDs by
+// the real count) or the host list (the grid is the tile count); -1 if this
+// workgroup has no tile.  (Scalar loads: the counts are uniform.)
+__device__ __forceinline__ int launch_tile(const ExpertLaunch &L, int &n_items, int &n_tiles)
+{
+    if (L.dev_n) {
+        n_items = __builtin_amdgcn_readfirstlane(L.dev_n->n_items);
+        n_tiles = __builtin_amdgcn_readfirstlane(L.dev_n->n_tiles);
+        return xcd_tile(int(blockIdx.x), n_tiles);
+    }
+    n_items = L.n_items;
+    n_tiles = L.n_tiles;
+    return xcd_swizzle(int(blockIdx.x), int(gridDim.x));
+}
+
+// Row and weight-slice geometry of a tile-path launch kind: an item of n
+// rows has ceil(n / rows) * slices tiles.
+struct TileGeom {
+    int rows, slices;
+};
+TileGeom geom_gateup_tile(int d, int I);
+TileGeom geom_down_tile(int d, int I);
+TileGeom geom_gateup_q4_tile(int d, int I);
+TileGeom geom_down_q4_tile(int d, int I);
+
+// Device-built work list of a forward whose demanded experts are all
+// published (build_worklist_kernel): the four launch lists (tile and stream
+// path, gate/up and down), each ascending by expert, the shared expert first
+// in the tile lists, with their counts.
+struct WorklistArgs {
+    const int32_t *counts, *offsets;     // routing
+    const int32_t *slot_of;              // [E] published global slot, -1 if none
+    const uint32_t *gen_of;              // [E] published generation
+    uint32_t *status;                    // STATUS_MISS if a demanded expert is unpublished
+    WorkItem *items[4];                  // gate/up tile, down tile, gate/up stream, down stream; E + 1 each
+    DevCount *counts_out;                // [4]
+    int E, T, thr, has_shared;
+    TileGeom gu, dn;                     // tile-path geometry
+    int per_gu_stream, per_dn_stream;    // tiles per stream item
+};
+hipError_t launch_build_worklist(const WorklistArgs &A, hipStream_t s);
 
 // tiles per item of each launch kind
 int tiles_gateup_tile(int nrows, int d, int I);

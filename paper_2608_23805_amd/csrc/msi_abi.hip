@@ -171,6 +171,8 @@ struct msi_plan {
     uint32_t *res_gen_dev = nullptr;    // [n_layers][E]
     int32_t *res_host = nullptr;        // pinned staging [2 * E]
     uint32_t *arrive_dev = nullptr;     // arrival counters (zero between launches): [ARRIVE_ROUTE], [ARRIVE_COMBINE]
+    WorkItem *dlist_dev = nullptr;      // device-built work lists: 4 x (E + 1) items
+    DevCount *dcount_dev = nullptr;     // their counts [4]
     bool status_clean = true;           // status_dev is zero (the last forward's combine cleared it)
     uint32_t *tail_host = nullptr;      // pinned [2 + E]: status | DONE, demanded count, ids (written by the combine)
     uint32_t *tail_hdev = nullptr;      // device-visible address of tail_host
@@ -705,6 +707,8 @@ msi_status msi_plan_create(const msi_plan_desc *desc, msi_plan **out)
         hipMalloc(&p->res_slot_dev, sizeof(int32_t) * E * NL) != hipSuccess ||
         hipMalloc(&p->res_gen_dev, sizeof(uint32_t) * E * NL) != hipSuccess ||
         hipMalloc(&p->arrive_dev, 256) != hipSuccess ||
+        hipMalloc(&p->dlist_dev, 4 * (E + 1) * sizeof(WorkItem)) != hipSuccess ||
+        hipMalloc(&p->dcount_dev, 4 * sizeof(DevCount)) != hipSuccess ||
         hipMalloc(&p->table_dev, p->table_cap * sizeof(WorkItem)) != hipSuccess)
         return cleanup(MSI_E_DEVICE, "device allocation failed");
     if (hipHostMalloc(&p->table_host, p->table_cap * sizeof(WorkItem), hipHostMallocDefault) != hipSuccess ||
@@ -761,6 +765,10 @@ msi_status msi_plan_destroy(msi_plan *p)
         (void)hipFree(p->res_gen_dev);
     if (p->arrive_dev)
         (void)hipFree(p->arrive_dev);
+    if (p->dlist_dev)
+        (void)hipFree(p->dlist_dev);
+    if (p->dcount_dev)
+        (void)hipFree(p->dcount_dev);
     if (p->res_host)
         (void)hipHostFree(p->res_host);
     if (p->tail_host)
@@ -1057,6 +1065,120 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
             return MSI_OK;
         }
         p->direct_ok[L0] = 0;       // a demanded expert was not resident: schedule it
+    }
+
+    // ---- layer entry, device-built work lists (T above the stream threshold):
+    // when the layer's last forward needed no fill, a one-workgroup kernel
+    // builds the four launch lists from the counts and the published
+    // residency table and the expert kernels read their lengths on the
+    // device (grids sized for the largest possible lists), so nothing waits
+    // for the host between the routing and the combine.  A demanded expert
+    // without a published slot makes the attempt publish nothing
+    // (STATUS_MISS) and the forward continues on the scheduled path.
+    if (!core.zero_cache() && !f32w && uint32_t(T) > g_stream_threshold && p->direct_ok[a->layer]) {
+        const uint32_t L0 = a->layer;
+        if (p->res_version[L0] != core.layer_version(L0)) {
+            core.published_map(L0, p->res_host, reinterpret_cast<uint32_t *>(p->res_host + E));
+            HIP_OK(hipMemcpyAsync(p->res_slot_dev + size_t(L0) * E, p->res_host, sizeof(int32_t) * E,
+                                  hipMemcpyHostToDevice, cs));
+            HIP_OK(hipMemcpyAsync(p->res_gen_dev + size_t(L0) * E, p->res_host + E, sizeof(uint32_t) * E,
+                                  hipMemcpyHostToDevice, cs));
+            p->res_version[L0] = core.layer_version(L0);
+        }
+        const bool q4w = d.wdtype == MSI_W_Q4B32;
+        const int thr = int(g_stream_threshold);
+        const int has_sh = a->shared_object ? 1 : 0;
+        WorklistArgs W{};
+        W.counts = a->r.counts;
+        W.offsets = a->r.offsets;
+        W.slot_of = p->res_slot_dev + size_t(L0) * E;
+        W.gen_of = p->res_gen_dev + size_t(L0) * E;
+        W.status = p->status_dev;
+        for (int k = 0; k < 4; ++k)
+            W.items[k] = p->dlist_dev + size_t(k) * (E + 1);
+        W.counts_out = p->dcount_dev;
+        W.E = E;
+        W.T = T;
+        W.thr = thr;
+        W.has_shared = has_sh;
+        W.gu = q4w ? geom_gateup_q4_tile(D, I) : geom_gateup_tile(D, I);
+        W.dn = q4w ? geom_down_q4_tile(D, I) : geom_down_tile(D, I);
+        W.per_gu_stream = q4w ? tiles_gateup_q4_stream(1, D, I) : tiles_gateup_stream(1, D, I);
+        W.per_dn_stream = q4w ? tiles_down_q4_stream(1, D, I) : tiles_down_stream(1, D, I);
+        if (!p->status_clean)
+            HIP_OK(launch_clear_word(p->status_dev, cs));
+        p->status_clean = false;
+        __atomic_store_n(&p->tail_host[0], 0u, __ATOMIC_RELAXED);
+        HIP_OK(p->timed_launch(MSI_K_PERMUTE, cs, [&] { return launch_build_worklist(W, cs); }));
+        // grids for the largest lists this routing could give
+        const int64_t rows = int64_t(T) * K;
+        const int64_t n_tile_max = std::min<int64_t>(E, rows / (thr + 1));
+        // (whole multiples of 8: each XCD's share of the real tiles must fit its workgroups)
+        auto round8 = [](int64_t v) { return int((v + 7) / 8 * 8); };
+        auto tile_ub = [&](TileGeom g) {
+            return round8(((rows + g.rows - 1) / g.rows + n_tile_max + (has_sh ? (T + g.rows - 1) / g.rows : 0)) *
+                          g.slices);
+        };
+        const int n_stream_max = int(std::min<int64_t>(E, rows));
+        ExpertLaunch X{};
+        X.x = a->x;
+        X.perm = a->r.perm;
+        X.wbase = static_cast<const uint8_t *>(d.slot_pool);
+        X.wstride = d.slot_stride;
+        X.gen_dev = p->gen_dev;
+        X.status = p->status_dev;
+        X.act = B.act;
+        X.y = B.y;
+        X.row_weight = a->r.row_weight;
+        X.shared_w = static_cast<const uint8_t *>(a->shared_object);
+        X.act_s = B.act_s;
+        X.ys = B.ys;
+        X.d = D;
+        X.I = I;
+        ExpertLaunch GT = X, DT = X, GS = X, DS = X;
+        GT.items = W.items[0];
+        GT.dev_n = p->dcount_dev + 0;
+        GT.n_tiles = tile_ub(W.gu);
+        DT.items = W.items[1];
+        DT.dev_n = p->dcount_dev + 1;
+        DT.n_tiles = tile_ub(W.dn);
+        GS.items = W.items[2];
+        GS.dev_n = p->dcount_dev + 2;
+        GS.n_tiles = round8(int64_t(n_stream_max) * W.per_gu_stream);
+        DS.items = W.items[3];
+        DS.dev_n = p->dcount_dev + 3;
+        DS.n_tiles = round8(int64_t(n_stream_max) * W.per_dn_stream);
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_TILE, cs,
+                               [&] { return q4w ? launch_gateup_q4_tile(GT, cs) : launch_gateup_tile(GT, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs, [&] {
+            return q4w ? launch_gateup_q4_stream(GS, cs) : launch_gateup_stream(GS, cs);
+        }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_TILE, cs,
+                               [&] { return q4w ? launch_down_q4_tile(DT, cs) : launch_down_tile(DT, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
+                               [&] { return q4w ? launch_down_q4_stream(DS, cs) : launch_down_stream(DS, cs); }));
+        // large grid: no arrival counter (the next forward clears the status word)
+        const CombinePublish pub{p->status_dev, nullptr, p->tail_hdev, a->r.demand};
+        HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
+            return launch_combine(B.y, has_sh ? B.ys : nullptr, false, a->r.inv, a->out, pub, T, K, D, cs);
+        }));
+        HIP_OK(wait_published(&p->tail_host[0], cs));
+        const uint32_t st = __atomic_load_n(&p->tail_host[0], __ATOMIC_ACQUIRE);
+        if (!(st & STATUS_MISS)) {
+            const uint32_t n = std::min<uint32_t>(p->tail_host[1], uint32_t(E));
+            std::vector<int32_t> dem(p->tail_host + 2, p->tail_host + 2 + n);
+            if (st & STATUS_STALE) {
+                core.stats().stale_detected++;
+                core.stats().forwards++;
+                core.invalidate_experts(L0, dem);
+                p->direct_ok[L0] = 0;
+                return fail(MSI_E_STALE, "a kernel saw a slot generation it did not expect; output not published");
+            }
+            core.note_direct_hits(L0, dem);
+            return MSI_OK;
+        }
+        p->direct_ok[L0] = 0;       // a demanded expert was not resident: schedule it
+        HIP_OK(hipStreamSynchronize(cs));
     }
 
     // ---- layer entry: the demanded set (one device-to-host read of the counts)

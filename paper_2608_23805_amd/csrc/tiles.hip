@@ -19,6 +19,18 @@ int tiles_down_tile(int nrows, int d, int I)
     return ring_tiles_down(nrows, d);
 }
 
+TileGeom geom_gateup_tile(int d, int I)
+{
+    (void)d;
+    return TileGeom{ring::TM, I / 128};
+}
+
+TileGeom geom_down_tile(int d, int I)
+{
+    (void)I;
+    return TileGeom{ring::TM, d / ring::TN};
+}
+
 // workgroups of a persistent launch: one per compute unit
 static int g_persistent_wgs = 256;
 

@@ -10,6 +10,8 @@
   on the host and still matches the oracle; the next two forwards of the
   same batch (all resident: host-built list, then the device path again) are
   byte-identical to it, so the status word was left clean.
+* The same above the stream threshold (T > 16), where the four launch lists
+  are built on the device.
 """
 import dataclasses
 
@@ -91,4 +93,46 @@ def test_device_work_list_miss_reschedules(o):
         again = run_layer(plan, db, T=8)
         assert plan.stats()["fills"] == fills + len(new)
         assert again["out"].cpu().numpy().tobytes() == rb["out"].cpu().numpy().tobytes()
+    plan.close()
+
+
+# 96 tokens over 64 experts, skewed: popular experts take the tile path (more
+# than 16 rows), rare ones the stream path
+MISS_PRE = synth.Workload("miss_prefill_bf16", 24, synth.LayerShape(96, 256, 64, 4, 128, "bf16"),
+                          prior="dirichlet", prior_param=0.3, tau=1.0)
+
+
+def test_device_built_lists_above_stream_threshold(o):
+    """T > 16: the work lists built on the device (after a forward that
+    needed no fill) give byte-identical outputs to the host schedule, over
+    both paths; a demanded expert without a published slot makes the
+    attempt publish nothing and the forward is rescheduled on the host."""
+    li = synth.layer_inputs(MISS_PRE)
+    la = dataclasses.replace(li, x=li.x[:48])
+    lb = dataclasses.replace(li, x=li.x[48:96])
+    da, db = device_layer(la), device_layer(lb)
+    plan = make_plan(li, capacity=MISS_PRE.shape.E)
+    plan.set_timing(True, kinds=["permute"])       # the work-list kernel is the only launch of this kind
+    log("case device lists: batch a fills, runs with no fill, then on the device lists")
+    ra = run_layer(plan, da, T=48)
+    c = ra["counts"]
+    log(f"device lists: tile experts {(c > 16).sum()}, stream experts {((c > 0) & (c <= 16)).sum()}")
+    assert (c > 16).any() and ((c > 0) & (c <= 16)).any()
+    run_layer(plan, da, T=48)
+    assert plan.timings()["permute"][0] == 0
+    again = run_layer(plan, da, T=48)
+    assert plan.timings()["permute"][0] == 1
+    assert again["out"].cpu().numpy().tobytes() == ra["out"].cpu().numpy().tobytes()
+    fills = plan.stats()["fills"]
+    log("case device lists: batch b meets unpublished experts")
+    rb = run_layer(plan, db, T=48)
+    assert plan.timings()["permute"][0] == 2
+    new = set(np.nonzero(rb["counts"])[0]) - set(np.nonzero(ra["counts"])[0])
+    assert new and plan.stats()["fills"] == fills + len(new)
+    oracle_compare(o, lb, rb, list(range(48)), TOL_BF16)
+    _check_routing(o, rb, MISS_PRE.shape.E)
+    for _ in range(2):
+        again = run_layer(plan, db, T=48)
+        assert again["out"].cpu().numpy().tobytes() == rb["out"].cpu().numpy().tobytes()
+    assert plan.timings()["permute"][0] == 3
     plan.close()

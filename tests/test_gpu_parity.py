@@ -122,7 +122,7 @@ def test_small_bf16_capacity_bit_identity(small):
     for cap in (0, 5, 32):
         log(f"case small_bf16 capacity={cap}")
         plan = make_plan(small, capacity=cap, transient=6)
-        for _ in range(2):
+        for _ in range(3):               # at capacity 32 the third forward runs on device-built lists
             out = run_layer(plan, dl)["out"].cpu().numpy()
             if ref is None:
                 ref = out
@@ -224,6 +224,9 @@ def test_prefill_full_sampled(o):
     err, near, ora = oracle_compare(o, li, res, toks, TOL_BF16)
     log(f"prefill sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
     _check_weights(res, ora, toks)
+    # all resident: the host schedule, then the device-built work lists, byte-identical
+    for _ in range(2):
+        assert run_layer(plan, dl)["out"].cpu().numpy().tobytes() == res["out"].cpu().numpy().tobytes()
     plan.close()
 
 
@@ -245,6 +248,8 @@ def test_small_q4_layer_and_capacities(o, small_q4):
         log(f"case small_q4 capacity={cap}")
         plan = make_plan(small_q4, capacity=cap, transient=4)
         res = run_layer(plan, dl)
+        for _ in range(2):               # at capacity 24 the last runs on device-built lists
+            assert run_layer(plan, dl)["out"].cpu().numpy().tobytes() == res["out"].cpu().numpy().tobytes()
         if ref is None:
             counts = res["counts"]
             log(f"small_q4 counts min={counts.min()} max={counts.max()} "
@@ -296,4 +301,6 @@ def test_prefill_q4_full_sampled(o):
                       + sets["moved_tokens"]))
     err, near, _ = oracle_compare(o, li, res, toks, TOL_BF16)
     log(f"prefill_q4 sampled {len(toks)} tokens err={err:.3e} near_ties={len(near)}")
+    for _ in range(2):               # host schedule, then device-built work lists
+        assert run_layer(plan, dl)["out"].cpu().numpy().tobytes() == res["out"].cpu().numpy().tobytes()
     plan.close()
