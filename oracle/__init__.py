@@ -23,7 +23,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "moe_oracle.c")
 LIB_PATH = os.path.join(_HERE, "libmsi_oracle.so")
 
-DTYPE_CODE = {"f32": 0, "bf16": 1, "q4b32": 2}
+DTYPE_CODE = {"f32": 0, "bf16": 1, "q4b32": 2, "kq": 3, "k4": 3, "k6": 4}
 MAX_K = 64
 
 _lib = None
@@ -112,9 +112,10 @@ class Oracle:
         """(Wg [I,d], Wu [I,d], Wd [d,I]) of an expert object, as fp64."""
         nb = self.matrix_nbytes(dtype, I, d)
         obj = np.ascontiguousarray(obj, dtype=np.uint8)
+        dd = "k6" if dtype == "kq" else dtype
         return (self.dequant(dtype, I, d, obj[:nb]),
                 self.dequant(dtype, I, d, obj[nb:2 * nb]),
-                self.dequant(dtype, d, I, obj[2 * nb:]))
+                self.dequant(dd, d, I, obj[2 * nb:]))
 
     # -- method steps -----------------------------------------------------------
     def router_logits(self, x: np.ndarray, wr: np.ndarray, bias: Optional[np.ndarray],

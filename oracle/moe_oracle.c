@@ -34,7 +34,10 @@
  * Inputs are read in their stored formats and upcast exactly to double:
  *   dtype 0 f32, 1 bf16 (uint16 = top half of binary32), 2 q4b32 (nibbles
  *   [rows, cols/2], low nibble = even column, 4-bit two's complement, then
- *   fp16 scales [rows, cols/32]; value = scale * q).
+ *   fp16 scales [rows, cols/32]; value = scale * q), 3 k4 and 4 k6 (the
+ *   256-element super-block formats of 4.5 and 6.5625 bits per weight,
+ *   decoded in wmat_at below); an expert object of dtype 3 (kq) holds Wg and
+ *   Wu in k4 and Wd in k6.
  * An expert object is [Wg (I x d) | Wu (I x d) | Wd (d x I)], row-major.
  */
 #include <math.h>
@@ -50,7 +53,9 @@
 #define MSIO_MUTANT 0 /* tests plant single mistakes with -DMSIO_MUTANT=n */
 #endif
 
-enum { MSIO_F32 = 0, MSIO_BF16 = 1, MSIO_Q4B32 = 2 };
+/* matrix formats; an expert object of format KQ holds Wg, Wu in K4 and Wd in K6 */
+enum { MSIO_F32 = 0, MSIO_BF16 = 1, MSIO_Q4B32 = 2, MSIO_K4 = 3, MSIO_K6 = 4 };
+#define MSIO_KQ MSIO_K4
 
 /* ---- exact upcasts of the stored formats ------------------------------- */
 
@@ -112,8 +117,26 @@ size_t msio_matrix_nbytes(int dtype, int64_t rows, int64_t cols)
     switch (dtype) {
     case MSIO_F32: return (size_t)(rows * cols * 4);
     case MSIO_BF16: return (size_t)(rows * cols * 2);
+    case MSIO_K4: return (size_t)(rows * cols / 2 + rows * (cols / 256) * 16);
+    case MSIO_K6: return (size_t)(rows * cols / 2 + rows * cols / 4 + rows * cols / 16 + rows * (cols / 256) * 2);
     default: return (size_t)(rows * cols / 2 + rows * (cols / 32) * 2);
     }
+}
+
+static double fp16_at(const uint8_t *p)
+{
+    uint16_t h;
+    memcpy(&h, p, 2);
+    return msio_fp16_to_f64(h);
+}
+
+/* 6-bit field j of a 48-bit little-endian group of 6 bytes */
+static int six_bits(const uint8_t *p, int j)
+{
+    uint64_t w = 0;
+    for (int b = 5; b >= 0; --b)
+        w = (w << 8) | p[b];
+    return (int)((w >> (6 * j)) & 63);
 }
 
 typedef struct {
@@ -134,6 +157,36 @@ static inline double wmat_at(const wmat *m, int64_t r, int64_t c)
         uint16_t b;
         memcpy(&b, m->base + 2 * (r * m->cols + c), 2);
         return msio_bf16_to_f64(b);
+    }
+    case MSIO_K4: {
+        /* nibbles [rows, cols/2], then a 16-byte header per (row, 256-element super-block):
+         * fp16 d, fp16 dmin, eight 6-bit scales, eight 6-bit mins; value = d sc_j q - dmin m_j */
+        const uint8_t byte = m->base[r * (m->cols / 2) + c / 2];
+        const int q = (c & 1) ? (byte >> 4) : (byte & 0x0F);
+        const uint8_t *h = m->base + (size_t)(m->rows * m->cols / 2) + 16 * (size_t)(r * (m->cols / 256) + c / 256);
+        const int j = (int)((c % 256) / 32);
+        const double d = fp16_at(h), dmin = fp16_at(h + 2);
+#if MSIO_MUTANT == 13
+        return d * six_bits(h + 4, j) * q + dmin * six_bits(h + 10, j);     /* min added */
+#else
+        return d * six_bits(h + 4, j) * q - dmin * six_bits(h + 10, j);
+#endif
+    }
+    case MSIO_K6: {
+        /* low nibbles [rows, cols/2], high 2-bit parts [rows, cols/4], int8 scales [rows, cols/16],
+         * fp16 d [rows, cols/256]; q = low | high << 4, value = d sc_j (q - 32) */
+        const int64_t R = m->rows, C = m->cols;
+        const uint8_t byte = m->base[r * (C / 2) + c / 2];
+        const int lo = (c & 1) ? (byte >> 4) : (byte & 0x0F);
+        const int hi = (m->base[R * C / 2 + r * (C / 4) + c / 4] >> (2 * (c % 4))) & 3;
+#if MSIO_MUTANT == 14
+        const int q = lo | (hi << 2);                                        /* high bits misplaced */
+#else
+        const int q = lo | (hi << 4);
+#endif
+        const int8_t sc = (int8_t)m->base[R * C / 2 + R * C / 4 + r * (C / 16) + c / 16];
+        const double d = fp16_at(m->base + R * C / 2 + R * C / 4 + R * C / 16 + 2 * (r * (C / 256) + c / 256));
+        return d * sc * (q - 32);
     }
     default: {
         uint8_t byte = m->base[r * (m->cols / 2) + c / 2];
@@ -337,7 +390,7 @@ void msio_expert_ffn(int64_t d, int64_t I, int wdtype, const void *obj, const do
     size_t nb = msio_matrix_nbytes(wdtype, I, d);
     wmat Wg = {wdtype, b, I, d};
     wmat Wu = {wdtype, b + nb, I, d};
-    wmat Wd = {wdtype, b + 2 * nb, d, I};
+    wmat Wd = {wdtype == MSIO_KQ ? MSIO_K6 : wdtype, b + 2 * nb, d, I};
 #if MSIO_MUTANT == 5
     Wg.base = Wu.base;                                /* gate reads the up matrix */
 #endif

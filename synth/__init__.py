@@ -18,6 +18,19 @@ Byte formats (little endian):
   quantizer below only builds test data: scale = fp16(amax / 7),
   q = clamp(rint(w / scale), -8, 7), amax == 0 gives scale 0 and q 0.
 
+* ``kq``    -- a mix of two super-block formats with 256-element super-blocks
+  along each row (cols % 256 == 0), stored planar:
+  ``k4`` (4.5 bits per weight, for Wg and Wu): nibbles [rows, cols/2] (element
+  2j in the low nibble of byte j, unsigned 0..15), then one 16-byte header per
+  row and super-block: fp16 d, fp16 dmin, eight 6-bit sub-block scales (48
+  bits, little endian, scale j at bits 6j..6j+5), eight 6-bit sub-block mins
+  likewise; value = d * sc_j * q - dmin * m_j for the j-th 32-element
+  sub-block.  ``k6`` (6.5625 bits per weight, for Wd): low nibbles
+  [rows, cols/2] (as above), high 2-bit parts [rows, cols/4] (element 4j + t
+  at bits 2t..2t+1 of byte j), int8 scales [rows, cols/16] (one per 16
+  elements), fp16 d [rows, cols/256]; q = low | high << 4 in 0..63 and value
+  = d * sc_j * (q - 32).  The quantizers below only build test data.
+
 An expert object is the concatenation [Wg | Wu | Wd] with Wg, Wu of shape
 [I, d] (row-major, the reduction axis d contiguous) and Wd of shape [d, I]
 (reduction axis I contiguous).  The router weight is stored [E, d].
@@ -45,7 +58,7 @@ KIND_EXPERT = 3
 KIND_SHARED = 4
 KIND_PERM = 5
 
-WDTYPES = ("f32", "bf16", "q4b32")
+WDTYPES = ("f32", "bf16", "q4b32", "kq")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -148,11 +161,98 @@ def q4b32_matrix_nbytes(rows: int, cols: int) -> int:
     return rows * cols // 2 + rows * (cols // 32) * 2
 
 
+def k4_matrix_nbytes(rows: int, cols: int) -> int:
+    return rows * cols // 2 + rows * (cols // 256) * 16
+
+
+def k6_matrix_nbytes(rows: int, cols: int) -> int:
+    return rows * cols // 2 + rows * cols // 4 + rows * cols // 16 + rows * (cols // 256) * 2
+
+
+def _pack6(v):
+    """Eight 6-bit values per row of v [n, 8] -> [n, 6] bytes, value j at bits 6j.. (little endian)."""
+    import numpy as np
+    v = np.asarray(v, dtype=np.uint64)
+    word = np.zeros(v.shape[0], dtype=np.uint64)
+    for j in range(8):
+        word |= (v[:, j] & np.uint64(63)) << np.uint64(6 * j)
+    return np.stack([((word >> np.uint64(8 * b)) & np.uint64(255)).astype(np.uint8) for b in range(6)], axis=1)
+
+
+def _fp16_at_least(v: np.ndarray) -> np.ndarray:
+    """The fp16 nearest to v, moved up one step where it fell below v."""
+    h = np.asarray(v, dtype=np.float64).astype(np.float16)
+    low = h.astype(np.float64) < v
+    h[low] = np.nextafter(h[low], np.float16(np.inf))
+    return h
+
+
+def quantize_k4(w: np.ndarray) -> bytes:
+    """w [rows, cols] (cols % 256 == 0) -> the k4 layout.  Per 32-element
+    sub-block: lo = min(0, min w), hi = max(0, max w), a = (hi - lo) / 15,
+    b = -lo; per super-block d = max a / 63 and dmin = max b / 63 in fp16
+    (rounded up), sc = ceil(a / d), m = ceil(b / dmin) in 0..63 (so the step
+    d sc covers a and the offset dmin m covers b), q = clamp(rint((w + dmin m)
+    / (d sc)), 0, 15) (0 where d sc = 0)."""
+    w = np.asarray(w, dtype=np.float32)
+    rows, cols = w.shape
+    assert cols % 256 == 0
+    nsb = cols // 256
+    sub = w.reshape(rows, nsb, 8, 32).astype(np.float64)
+    lo = np.minimum(sub.min(axis=3), 0.0)
+    hi = np.maximum(sub.max(axis=3), 0.0)
+    a, b = (hi - lo) / 15.0, -lo
+    d16 = _fp16_at_least(a.max(axis=2) / 63.0)
+    m16 = _fp16_at_least(b.max(axis=2) / 63.0)
+    d, dm = d16.astype(np.float64), m16.astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        sc = np.where(d[..., None] > 0, np.ceil(a / d[..., None]), 0.0).clip(0, 63)
+        mn = np.where(dm[..., None] > 0, np.ceil(b / dm[..., None]), 0.0).clip(0, 63)
+        step = d[..., None] * sc
+        q = np.where(step[..., None] > 0, np.rint((sub + (dm[..., None] * mn)[..., None]) / step[..., None]), 0.0)
+    q = q.clip(0, 15).astype(np.uint8).reshape(rows, cols)
+    nib = (q[:, 0::2] | (q[:, 1::2] << np.uint8(4))).astype(np.uint8)
+    hdr = np.zeros((rows, nsb, 16), dtype=np.uint8)
+    hdr[:, :, 0:2] = d16.view(np.uint8).reshape(rows, nsb, 2)
+    hdr[:, :, 2:4] = m16.view(np.uint8).reshape(rows, nsb, 2)
+    hdr[:, :, 4:10] = _pack6(sc.reshape(-1, 8).astype(np.int64)).reshape(rows, nsb, 6)
+    hdr[:, :, 10:16] = _pack6(mn.reshape(-1, 8).astype(np.int64)).reshape(rows, nsb, 6)
+    return nib.tobytes() + hdr.tobytes()
+
+
+def quantize_k6(w: np.ndarray) -> bytes:
+    """w [rows, cols] (cols % 256 == 0) -> the k6 layout.  Per 16-element
+    sub-block s = amax / 31; per super-block d = max s / 127 in fp16 (rounded
+    up), sc = ceil(s / d) in 0..127 (the step d sc covers s), q =
+    clamp(rint(w / (d sc)) + 32, 0, 63) (32 where d sc = 0)."""
+    w = np.asarray(w, dtype=np.float32)
+    rows, cols = w.shape
+    assert cols % 256 == 0
+    nsb = cols // 256
+    sub = w.reshape(rows, nsb, 16, 16).astype(np.float64)
+    s = np.abs(sub).max(axis=3) / 31.0
+    d16 = _fp16_at_least(s.max(axis=2) / 127.0)
+    d = d16.astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        sc = np.where(d[..., None] > 0, np.ceil(s / d[..., None]), 0.0).clip(-128, 127)
+        step = d[..., None] * sc
+        q = np.where(step[..., None] != 0, np.rint(sub / step[..., None]) + 32, 32.0)
+    q = q.clip(0, 63).astype(np.uint8).reshape(rows, cols)
+    low = q & np.uint8(15)
+    ql = (low[:, 0::2] | (low[:, 1::2] << np.uint8(4))).astype(np.uint8)
+    hi2 = (q >> np.uint8(4)) & np.uint8(3)
+    qh = (hi2[:, 0::4] | (hi2[:, 1::4] << np.uint8(2)) | (hi2[:, 2::4] << np.uint8(4)) |
+          (hi2[:, 3::4] << np.uint8(6))).astype(np.uint8)
+    return ql.tobytes() + qh.tobytes() + sc.astype(np.int8).tobytes() + d16.tobytes()
+
+
 def object_nbytes(d: int, I: int, wdtype: str) -> int:
     if wdtype == "f32":
         return 3 * I * d * 4
     if wdtype == "bf16":
         return 3 * I * d * 2
+    if wdtype == "kq":
+        return 2 * k4_matrix_nbytes(I, d) + k6_matrix_nbytes(d, I)
     return 2 * q4b32_matrix_nbytes(I, d) + q4b32_matrix_nbytes(d, I)
 
 
@@ -161,6 +261,8 @@ def encode_matrix(w: np.ndarray, wdtype: str) -> bytes:
         return np.ascontiguousarray(w, dtype=np.float32).tobytes()
     if wdtype == "bf16":
         return f32_to_bf16_bits(w).tobytes()
+    if wdtype in ("k4", "k6"):
+        return quantize_k4(w) if wdtype == "k4" else quantize_k6(w)
     return quantize_q4b32(w)
 
 
@@ -183,7 +285,10 @@ def expert_object(wl: Workload, layer: int, expert: int, shared: bool = False) -
     wg = g.standard_normal((s.I, s.d), dtype=np.float32) * np.float32(0.02)
     wu = g.standard_normal((s.I, s.d), dtype=np.float32) * np.float32(0.02)
     wd = g.standard_normal((s.d, s.I), dtype=np.float32) * np.float32(0.02)
-    b = encode_matrix(wg, s.wdtype) + encode_matrix(wu, s.wdtype) + encode_matrix(wd, s.wdtype)
+    if s.wdtype == "kq":       # gate / up in the 4.5-bit format, down in the 6.5625-bit one
+        b = encode_matrix(wg, "k4") + encode_matrix(wu, "k4") + encode_matrix(wd, "k6")
+    else:
+        b = encode_matrix(wg, s.wdtype) + encode_matrix(wu, s.wdtype) + encode_matrix(wd, s.wdtype)
     out = np.frombuffer(b, dtype=np.uint8).copy()
     assert out.nbytes == s.object_bytes()
     return out
@@ -293,6 +398,9 @@ def layer_inputs(wl: Workload, layer: int = 0, step: int = 0, T: Optional[int] =
 
 def component_sizes(shape: LayerShape):
     """Byte sizes of an expert object's components [Wg, Wu, Wd]."""
+    if shape.wdtype == "kq":
+        return [k4_matrix_nbytes(shape.I, shape.d), k4_matrix_nbytes(shape.I, shape.d),
+                k6_matrix_nbytes(shape.d, shape.I)]
     if shape.wdtype == "f32":
         m = lambda r, c: r * c * 4  # noqa: E731
     elif shape.wdtype == "bf16":

@@ -31,6 +31,7 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 TINY = synth.WORKLOADS["tiny_f32"]          # T=64 d=256 E=16 K=2 I=128 fp32
 SMALL_BF16 = synth.LayerShape(12, 64, 8, 3, 32, "bf16")
 SMALL_Q4 = synth.LayerShape(6, 64, 6, 2, 64, "q4b32")
+SMALL_KQ = synth.LayerShape(5, 256, 6, 2, 256, "kq")
 
 
 def _tiny_inputs(shape=None, wl=TINY, bias=False):
@@ -103,6 +104,66 @@ def pin_q4_quantizer_bound(o):
     bound = np.repeat(s * 0.5 + blk * 2.0 ** -10, 32, axis=1)
     assert np.all(np.abs(deq - w) <= bound + 1e-12)
     assert np.all(deq[3, 32:64] == 0.0)
+
+
+def _k4_block_bytes():
+    """The k4 super-block of the golden fixture, packed from the format
+    definition with plain integer arithmetic."""
+    nib = bytes((((2 * i) % 16) | (((2 * i + 1) % 16) << 4)) for i in range(128))
+    sc = sum((j + 1) << (6 * j) for j in range(8))
+    mn = sum(j << (6 * j) for j in range(8))
+    hdr = (0x3800).to_bytes(2, "little") + (0x3400).to_bytes(2, "little") + sc.to_bytes(6, "little") + \
+        mn.to_bytes(6, "little")
+    return nib + hdr
+
+
+def _k6_block_bytes():
+    q = [(5 * k) % 64 for k in range(256)]
+    ql = bytes(((q[2 * i] & 15) | ((q[2 * i + 1] & 15) << 4)) for i in range(128))
+    qh = bytes(sum(((q[4 * i + t] >> 4) & 3) << (2 * t) for t in range(4)) for i in range(64))
+    sc = bytes(((j - 8) & 0xFF) for j in range(16))
+    return ql + qh + sc + (0x3000).to_bytes(2, "little")
+
+
+def pin_kquant_blocks(o):
+    """Hand-derived elements of one super-block of each quantized-expert format."""
+    want = {"k4": {}, "k6": {}}
+    with open(os.path.join(GOLDEN, "kquant_blocks.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                fmt, k, v = line.split()
+                want[fmt][int(k)] = float(v)
+    for fmt, raw in (("k4", _k4_block_bytes()), ("k6", _k6_block_bytes())):
+        assert len(raw) == o.matrix_nbytes(fmt, 1, 256)
+        got = o.dequant(fmt, 1, 256, np.frombuffer(raw, dtype=np.uint8))[0]
+        for k, v in want[fmt].items():
+            assert got[k] == v, (fmt, k, got[k], v)
+
+
+def pin_kquant_quantizer_bound(o):
+    """The test-data quantizers' outputs decode within the formats' error
+    bounds: k4 within half a step (the step d*sc is below a + d) plus the
+    offset's excess (below dmin); k6 within half a step (below (s + d) / 2,
+    s = amax / 31); an all-zero super-block decodes to zeros."""
+    g = np.random.default_rng(12)
+    w = (g.standard_normal((6, 512)) * 0.02).astype(np.float32)
+    w[2, 256:] = 0.0                                   # an all-zero super-block
+    dq = o.dequant("k4", 6, 512, np.frombuffer(synth.quantize_k4(w), dtype=np.uint8))
+    sub = w.astype(np.float64).reshape(6, 2, 8, 32)
+    a = (np.maximum(sub.max(axis=3), 0) - np.minimum(sub.min(axis=3), 0)) / 15.0
+    d = a.max(axis=2, keepdims=True) / 63.0
+    b = -np.minimum(sub.min(axis=3), 0)
+    dm = b.max(axis=2, keepdims=True) / 63.0
+    bound = (0.5 * (a + d) + dm) * (1 + 2.0 ** -9) + 1e-9
+    assert np.all(np.abs(dq - w).reshape(6, 2, 8, 32) <= bound[..., None])
+    assert np.all(dq[2, 256:] == 0.0)
+    dq6 = o.dequant("k6", 6, 512, np.frombuffer(synth.quantize_k6(w), dtype=np.uint8))
+    sub6 = w.astype(np.float64).reshape(6, 2, 16, 16)
+    s6 = np.abs(sub6).max(axis=3) / 31.0
+    d6 = s6.max(axis=2, keepdims=True) / 127.0
+    bound6 = (0.5 * (s6 + d6)) * (1 + 2.0 ** -9) + 1e-9
+    assert np.all(np.abs(dq6 - w).reshape(6, 2, 16, 16) <= bound6[..., None])
+    assert np.all(dq6[2, 256:] == 0.0)
 
 
 # ---------------------------------------------------------------- router
@@ -217,7 +278,7 @@ def pin_expert_ffn_special(o):
 def pin_expert_ffn_matmul(o):
     """Cross-check of the gated-SiLU FFN against numpy matrix products with
     scipy's expit, in all three storage formats."""
-    for shape, wl in ((TINY.shape, TINY), (SMALL_BF16, TINY), (SMALL_Q4, TINY)):
+    for shape, wl in ((TINY.shape, TINY), (SMALL_BF16, TINY), (SMALL_Q4, TINY), (SMALL_KQ, TINY)):
         li = _tiny_inputs(shape)
         s = shape
         x = _dense(o, li.x, s.xdtype, s.T, s.d)
@@ -253,7 +314,7 @@ def _dense_layer(o, li, shape):
 
 
 def pin_layer_dense(o):
-    for shape, bias in ((TINY.shape, True), (SMALL_BF16, False), (SMALL_Q4, True)):
+    for shape, bias in ((TINY.shape, True), (SMALL_BF16, False), (SMALL_Q4, True), (SMALL_KQ, True)):
         li = _tiny_inputs(shape, bias=bias)
         s = shape
         ref, idx, w = _dense_layer(o, li, s)
@@ -372,4 +433,5 @@ ALL_PINS = [
     pin_router_matches_matmul, pin_topk_bruteforce, pin_topk_zero_router, pin_gate_weights,
     pin_permutation, pin_expert_ffn_special, pin_expert_ffn_matmul, pin_layer_dense,
     pin_layer_invariants, pin_residual_rows, pin_residual_invariants, pin_stack_chain,
+    pin_kquant_blocks, pin_kquant_quantizer_bound,
 ]

@@ -22,6 +22,8 @@ MUTANTS = {
     10: "stack normalisation without its epsilon",
     11: "stack normalisation by the sum of squares instead of the mean",
     12: "stack residual add dropped",
+    13: "4.5-bit format: sub-block min added instead of subtracted",
+    14: "6.5625-bit format: high bits placed at bit 2 instead of bit 4",
 }
 
 
