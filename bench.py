@@ -198,7 +198,7 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
     flops_gu = 2.0 * rows_tile * s.d * 2 * s.I
     # algorithmic bytes of that launch: each tile expert's Wg and Wu (and the shared one's) once, every
     # token's x row once, act written once
-    wbytes = 2 * s.I * s.d * 2 if s.wdtype != "q4b32" else 2 * s.I * (s.d // 2 + s.d // 32 * 2)
+    wbytes = gateup_weight_bytes(s)
     bytes_gu = (int((c > 16).sum()) + 1) * wbytes + s.T * s.d * 2 + rows_tile * s.I * 2
     layer_flops = 2.0 * s.T * (s.K * 3 * s.d * s.I + 3 * s.d * s.I + s.d * s.E)
     achieved = flops_gu / (avg_gu * 1e-3) / 1e12
@@ -211,36 +211,73 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                T=s.T, layer_tflops=round(layer_flops / (ms * 1e-3) / 1e12, 1),
                layer_mfma_frac=round(layer_flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
                roofline={"bound": "mfma",
-                         "kernel": "tile_q4_kernel<GateUp>" if s.wdtype == "q4b32" else "ring_gemm_kernel<GateUp>",
+                         "kernel": {"q4b32": "tile_q4_kernel<GateUp>", "kq": "tile_kq_kernel<GateUp>"}.get(
+                             s.wdtype, "ring_gemm_kernel<GateUp>"),
                          "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-                         "traffic": None if s.wdtype == "q4b32" else recorded_traffic(PREFILL_TRAFFIC_FILE,
-                                                                                      PREFILL_KERNEL_SOURCES),
+                         "traffic": None if s.wdtype != "bf16" else recorded_traffic(PREFILL_TRAFFIC_FILE,
+                                                                                     PREFILL_KERNEL_SOURCES),
                          "flops_per_launch": flops_gu, "algorithmic_bytes_per_launch": bytes_gu,
                          "avg_launch_us": round(avg_gu * 1e3, 1),
-                         "note": "int4 weights unpacked to bf16 MFMA operands" if s.wdtype == "q4b32" else ""},
+                         "note": {"q4b32": "int4 weights unpacked to bf16 MFMA operands",
+                                  "kq": "4.5-bit weights unpacked to exact bf16 MFMA operands, per-sub-block "
+                                        "scale and min applied in fp32"}.get(s.wdtype, "")},
                kernels=kernels, _routed_idx=routed_idx)
     log(f"[bench] prefill: {ms:.3f} ms/step, {res['value']:.0f} tok/s, layer {res['layer_tflops']} TFLOP/s, "
         f"gate/up {avg_gu * 1e3:.0f} us = {achieved:.0f} TFLOP/s")
     return res
 
 
-def bench_decode_q4(args, cs, side):
-    """T = 1 decode with 4-bit experts: ~21 MB of weights per step, launch-bound."""
+def gateup_weight_bytes(s):
+    """Bytes of one expert's Wg and Wu in the layer's storage format."""
+    if s.wdtype == "q4b32":
+        return 2 * s.I * (s.d // 2 + s.d // 32 * 2)
+    if s.wdtype == "kq":
+        return 2 * s.I * (s.d // 2 + s.d // 256 * 16)
+    return 2 * s.I * s.d * 2
+
+
+def bench_decode_quant(args, cs, side, name):
+    """Decode with quantized experts, all demanded experts resident:
+    decode_q4 (T = 1, ~21 MB of weights per step, launch-bound) and
+    decode_kq (T = 16).  A second, untimed pass with events on every launch
+    gives the gate/up stream kernel's duration and its algorithmic bandwidth
+    (the demanded experts' and the shared expert's Wg and Wu once, each routed
+    row's x read and act written once)."""
     import synth
-    wl = synth.WORKLOADS["decode_q4"]
+    wl = synth.WORKLOADS[name]
+    s = wl.shape
     li, plan, xs, dev, r, ws, out = _setup(wl, capacity=512, n_batches=16)
     _run(plan, xs, dev, r, ws, out, 0, max(args.warmup, len(xs)), cs, side)
     before = plan.stats()
     ms = _run(plan, xs, dev, r, ws, out, args.steps, 0, cs, side)
     fills_timed = plan.stats()["fills"] - before["fills"]
-    plan.close()
     if fills_timed:
-        raise RuntimeError(f"decode_q4: {fills_timed} fills inside the timed region of an all-resident run")
-    res = dict(workload="decode_q4", ms=round(ms, 4), tokens_per_s=round(wl.shape.T / (ms * 1e-3), 1),
-               fills_in_timed_region=fills_timed)
-    log(f"[bench] decode_q4: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s")
+        plan.close()
+        raise RuntimeError(f"{name}: {fills_timed} fills inside the timed region of an all-resident run")
+    plan.set_timing(args.telemetry == "on")
+    _run(plan, xs, dev, r, ws, out, 32, 0, cs, side)
+    t = plan.timings()
+    plan.set_timing(False)
+    gu_bytes = []
+    for b in range(len(xs)):
+        plan.route(xs[b], dev["wr"], dev["bias"], r, ws, cs)
+        c = r.counts.cpu().numpy()
+        dem = c[c > 0]
+        gu_bytes.append((len(dem) + 1) * gateup_weight_bytes(s) + (int(dem.sum()) + s.T) * (s.d * 2 + s.I * 2))
+    plan.close()
+    n_gu, ms_gu = t.get("gateup_stream", (0, 0.0))
+    avg_gu = ms_gu / max(n_gu, 1)
+    bytes_gu = sum(gu_bytes[i % len(xs)] for i in range(32)) / 32
+    kernels = {k: {"launches": n, "avg_us": round(v * 1e3 / max(n, 1), 2)} for k, (n, v) in t.items() if n}
+    res = dict(workload=name, T=s.T, ms=round(ms, 4), tokens_per_s=round(s.T / (ms * 1e-3), 1),
+               fills_in_timed_region=fills_timed, kernels=kernels,
+               gateup_stream={"avg_launch_us": round(avg_gu * 1e3, 2), "bytes_per_launch": int(bytes_gu),
+                              "achieved_GBs": round(bytes_gu / (avg_gu * 1e-3) / 1e9, 1) if avg_gu > 0 else None,
+                              "frac_of_hbm_peak": round(bytes_gu / (avg_gu * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+                              if avg_gu > 0 else None})
+    log(f"[bench] {name}: {ms * 1e3:.1f} us/step, {res['tokens_per_s']:.0f} tok/s, gate/up {avg_gu * 1e3:.1f} us")
     return res
 
 
@@ -497,7 +534,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--telemetry", default="on", choices=["on", "off"],
                     help="HIP-event timing around each launch inside the decode timed region")
-    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4,stack,source")
+    ap.add_argument("--skip", default="", help="comma list of: prefill,lru,cpu,decode,q4,kq,stack,source")
     ap.add_argument("--df-layers", type=int, default=2, help="source D/F experiment: layers")
     ap.add_argument("--df-steps", type=int, default=6, help="source D/F experiment: decode steps")
     ap.add_argument("--df-pairs", type=int, default=2, help="source D/F experiment: pairs (1 or 2)")
@@ -526,9 +563,11 @@ def main():
         if "prefill" not in skip:
             res["prefill"] = bench_prefill(args, cs, side)
             res["prefill"].pop("_routed_idx")
-        if "q4" not in skip:
-            res["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
-            res["prefill_q4"].pop("_routed_idx")
+        for fmt in ("q4", "kq"):
+            if fmt not in skip:
+                key = "prefill_q4" if fmt == "q4" else "prefill_kq"
+                res[key] = bench_prefill(args, cs, side, key)
+                res[key].pop("_routed_idx")
         print(json.dumps(res), flush=True)
         return
     dec, li = bench_decode(args, cs, side)
@@ -539,14 +578,18 @@ def main():
         extra["prefill"] = bench_prefill(args, cs, side)
     if "q4" not in skip:
         extra["prefill_q4"] = bench_prefill(args, cs, side, "prefill_q4")
-        extra["decode_q4"] = bench_decode_q4(args, cs, side)
+        extra["decode_q4"] = bench_decode_quant(args, cs, side, "decode_q4")
+    if "kq" not in skip:
+        extra["prefill_kq"] = bench_prefill(args, cs, side, "prefill_kq")
+        extra["decode_kq"] = bench_decode_quant(args, cs, side, "decode_kq")
     if "stack" not in skip:
         extra["stack"] = bench_stack(args, cs, side)
     if "source" not in skip:
         extra["source_df"] = bench_source_df(args, cs, side)
     pidx = extra["prefill"].pop("_routed_idx") if "prefill" in extra else None
-    if "prefill_q4" in extra:
-        extra["prefill_q4"].pop("_routed_idx")
+    for key in ("prefill_q4", "prefill_kq"):
+        if key in extra:
+            extra[key].pop("_routed_idx")
     cpu = None if "cpu" in skip else cpu_baseline(li, args.cpu_seconds, pidx)
 
     s = li.wl.shape

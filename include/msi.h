@@ -43,8 +43,19 @@
  *    half of binary32); MSI_W_Q4B32 4-bit blocks: a [rows, cols] matrix is
  *    nibbles [rows, cols/2] (element 2j in the low nibble of byte j, 4-bit
  *    two's complement) followed by fp16 scales [rows, cols/32], value =
- *    scale * q.  Hidden states and the router weight are f32 for MSI_W_F32
- *    and bf16 otherwise.
+ *    scale * q.  MSI_W_KQ, the mixed super-block format of the quantized
+ *    experts (the paper's 4.5 / 6.5625 bits-per-weight representation,
+ *    Implementation section): Wg and Wu in k4 -- nibbles [rows, cols/2]
+ *    (unsigned, element 2j in the low nibble of byte j) followed by a 16-byte
+ *    header per (row, 256-element super-block): fp16 d, fp16 dmin, eight
+ *    6-bit sub-block scales sc_j, eight 6-bit mins m_j (each group of eight a
+ *    48-bit little-endian field, j-th at bits 6j); value = d sc_j q - dmin m_j
+ *    for the j-th 32-element sub-block -- and Wd in k6: low nibbles
+ *    [rows, cols/2], high 2-bit parts [rows, cols/4] (element 4j + t at bits
+ *    2t of byte j), int8 scales [rows, cols/16], fp16 d [rows, cols/256];
+ *    q = low | high << 4, value = d sc_j (q - 32) for the j-th 16-element
+ *    sub-block.  KQ needs d_ff % 256 == 0.  Hidden states and the router
+ *    weight are f32 for MSI_W_F32 and bf16 otherwise.
  *  - An expert object is [Wg | Wu | Wd]: Wg, Wu are [d_ff, d_model] and Wd is
  *    [d_model, d_ff], each row-major with the reduction axis contiguous.
  *    The router weight is [n_experts, d_model] row-major.
@@ -74,7 +85,7 @@ typedef int32_t msi_status;
 #define MSI_E_STATE (-8)        /* lifecycle transition not allowed in this state     */
 #define MSI_E_IO (-9)           /* a source read completed with a negative status (EIO...) */
 
-typedef enum { MSI_W_F32 = 0, MSI_W_BF16 = 1, MSI_W_Q4B32 = 2 } msi_wdtype;
+typedef enum { MSI_W_F32 = 0, MSI_W_BF16 = 1, MSI_W_Q4B32 = 2, MSI_W_KQ = 3 } msi_wdtype;
 
 typedef struct msi_plan msi_plan;
 

@@ -34,9 +34,9 @@ MSI_SOURCE_BUFFERED_OK = 1
 FAULTS = {"short": 1, "eio": 2, "hold": 3}
 POLICIES = {"lru": 0, "protected_lru": 1}
 
-MSI_W_F32, MSI_W_BF16, MSI_W_Q4B32 = 0, 1, 2
+MSI_W_F32, MSI_W_BF16, MSI_W_Q4B32, MSI_W_KQ = 0, 1, 2, 3
 MSI_NOALLOC_SCRATCH_BYTES = 64 << 20
-WDTYPE = {"f32": MSI_W_F32, "bf16": MSI_W_BF16, "q4b32": MSI_W_Q4B32}
+WDTYPE = {"f32": MSI_W_F32, "bf16": MSI_W_BF16, "q4b32": MSI_W_Q4B32, "kq": MSI_W_KQ}
 SLOT_STATES = {0: "Vacant", 1: "Loading", 2: "DeviceReady", 3: "InUse", 4: "Recyclable"}
 
 _u32, _i32, _u64, _vp = ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64, ctypes.c_void_p
@@ -218,6 +218,10 @@ def object_nbytes(d: int, I: int, wdtype: str) -> int:
         return 3 * I * d * 4
     if wdtype == "bf16":
         return 3 * I * d * 2
+    if wdtype == "kq":        # Wg, Wu in the 4.5-bit format, Wd in the 6.5625-bit format
+        k4 = lambda r, c: r * c // 2 + r * (c // 256) * 16  # noqa: E731
+        k6 = lambda r, c: r * c // 2 + r * c // 4 + r * c // 16 + r * (c // 256) * 2  # noqa: E731
+        return 2 * k4(I, d) + k6(d, I)
     m = lambda r, c: r * c // 2 + r * (c // 32) * 2  # noqa: E731
     return 2 * m(I, d) + m(d, I)
 

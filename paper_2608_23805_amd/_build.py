@@ -16,7 +16,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmsi.so")
 ARCH = "gfx950"
 
-SOURCES = ["plan_core.cpp", "source.cpp", "route.hip", "experts.hip", "tiles.hip", "experts_q4.hip", "combine.hip", "worklist.hip", "msi_abi.hip"]
+SOURCES = ["plan_core.cpp", "source.cpp", "route.hip", "experts.hip", "tiles.hip", "experts_q4.hip", "experts_kq.hip", "combine.hip", "worklist.hip", "msi_abi.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",

@@ -484,6 +484,8 @@ hipError_t init_kernel_attributes()
         e = init_route_attributes();
     if (e == hipSuccess)
         e = init_q4_attributes();
+    if (e == hipSuccess)
+        e = init_kq_attributes();
     return e;
 }
 

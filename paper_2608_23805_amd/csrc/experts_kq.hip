@@ -1,0 +1,669 @@
+// experts_kq.hip -- expert projections of the quantized-expert mix (the
+// paper's 4.5 / 6.5625 bits-per-weight representation, "Implementation" and
+// "Output-Exact Execution Beyond the Full-Residency Envelope"), gfx950.
+//
+// Formats (per matrix [rows, cols], 256-element super-blocks along a row):
+//  * k4 (Wg, Wu): nibbles [rows, cols/2] (unsigned 0..15, element 2j in the
+//    low nibble of byte j), then a 16-byte header per (row, super-block):
+//    fp16 d, fp16 dmin, eight 6-bit sub-block scales, eight 6-bit sub-block
+//    mins (48-bit little-endian fields); value = d sc_j q - dmin m_j for the
+//    j-th 32-element sub-block.
+//  * k6 (Wd): low nibbles [rows, cols/2], high 2-bit parts [rows, cols/4]
+//    (element 4j + t at bits 2t of byte j), int8 scales [rows, cols/16], fp16
+//    d [rows, cols/256]; q = low | high << 4 and value = d sc_j (q - 32) for
+//    the j-th 16-element sub-block.
+//
+// The integers q and q - 32 are exact in bf16, so every MFMA partial over a
+// sub-block is an exact-product fp32 sum; the sub-block's scale (and the k4
+// min times the tokens' sum over the sub-block, from one more MFMA against a
+// fragment of ones) is then applied in fp32.  A 16x16x32 MFMA spans one k4
+// sub-block, or two k6 sub-blocks: those are split by zeroing the operand
+// lanes of the other half (lanes 0..31 carry elements 0..15 of the 32).
+//
+//  * stream path (<= 16 tokens per expert): weights as the A operand read
+//    straight from memory, tokens as the B operand from LDS, the layout of the
+//    4-bit stream kernels;
+//  * tile path: 128 tokens x 128 weight rows per workgroup, packed weights,
+//    headers and scales staged in LDS, unpacked while the fragments are built.
+#include "common.h"
+#include "kernels.h"
+
+namespace msi {
+
+namespace {
+
+constexpr uint32_t BF16_ONE2 = 0x3F803F80u;        // two bf16 1.0
+
+__device__ __forceinline__ float h2f(uint16_t h) { return float(__builtin_bit_cast(_Float16, h)); }
+
+// 8 unsigned nibbles (element e at bits 4e) -> 8 exact bf16 values
+__device__ __forceinline__ bf16x8 unpack_u4(uint32_t q)
+{
+    u32x4 r;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        const uint32_t lo = (q >> (8 * h)) & 15u, hi = (q >> (8 * h + 4)) & 15u;
+        r[h] = (__float_as_uint(float(lo)) >> 16) | (__float_as_uint(float(hi)) & 0xFFFF0000u);
+    }
+    return __builtin_bit_cast(bf16x8, r);
+}
+
+// 8 k6 elements: low nibbles (element e at bits 4e of lo) and 2-bit high
+// parts (element e at bits 2e of hi) -> 8 exact bf16 values q - 32
+__device__ __forceinline__ bf16x8 unpack_k6(uint32_t lo, uint32_t hi)
+{
+    u32x4 r;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        const int e0 = int(((lo >> (8 * h)) & 15u) | (((hi >> (4 * h)) & 3u) << 4)) - 32;
+        const int e1 = int(((lo >> (8 * h + 4)) & 15u) | (((hi >> (4 * h + 2)) & 3u) << 4)) - 32;
+        r[h] = (__float_as_uint(float(e0)) >> 16) | (__float_as_uint(float(e1)) & 0xFFFF0000u);
+    }
+    return __builtin_bit_cast(bf16x8, r);
+}
+
+// k4 header (16 bytes as four words): sub-block j's scale d sc_j and offset dmin m_j
+__device__ __forceinline__ void k4_coef(const u32x4 &h, int j, float &a, float &b)
+{
+    const uint64_t sc = uint64_t(h[1]) | (uint64_t(h[2] & 0xFFFFu) << 32);
+    const uint64_t mn = uint64_t(h[2] >> 16) | (uint64_t(h[3]) << 16);
+    a = h2f(uint16_t(h[0])) * float(uint32_t(sc >> (6 * j)) & 63u);
+    b = h2f(uint16_t(h[0] >> 16)) * float(uint32_t(mn >> (6 * j)) & 63u);
+}
+
+__host__ __device__ __forceinline__ uint32_t k4_bytes(uint32_t rows, uint32_t cols)
+{
+    return rows * (cols / 2) + rows * (cols / 256) * 16u;
+}
+
+// k6 planes of a [rows, cols] matrix at m: low nibbles, high parts, scales, d
+struct K6Planes {
+    const uint8_t *ql, *qh;
+    const int8_t *sc;
+    const uint16_t *d;
+};
+__device__ __forceinline__ K6Planes k6_planes(const uint8_t *m, uint32_t rows, uint32_t cols)
+{
+    K6Planes p;
+    p.ql = m;
+    p.qh = m + rows * (cols / 2);
+    p.sc = reinterpret_cast<const int8_t *>(p.qh + rows * (cols / 4));
+    p.d = reinterpret_cast<const uint16_t *>(reinterpret_cast<const uint8_t *>(p.sc) + rows * (cols / 16));
+    return p;
+}
+
+// Tile of a launch and its item (device-built decode list, device-built
+// prefill list, or host list), as the 4-bit kernels find theirs.
+__device__ __forceinline__ bool kq_tile(const ExpertLaunch &L, int per_item, int &t, WorkItem &it)
+{
+    if (L.direct.demand) {
+        int i, local;
+        direct_tile(int(blockIdx.x), per_item, i, local);
+        t = i * per_item + local;
+        return direct_item(L.direct, i, per_item, L.status, it);
+    }
+    int n_items, n_tiles;
+    t = launch_tile(L, n_items, n_tiles);
+    if (t < 0)
+        return false;
+    it = L.items[find_item(L.items, n_items, t)];
+    return true;
+}
+
+}  // namespace
+
+// ============================================================== stream path
+
+namespace kqs {
+constexpr int WAVES = 4, ROWS = 16;
+}
+
+int tiles_gateup_kq_stream(int nrows, int d, int I)
+{
+    (void)nrows;
+    (void)d;
+    return I / kqs::ROWS;
+}
+
+int tiles_down_kq_stream(int nrows, int d, int I)
+{
+    (void)nrows;
+    (void)I;
+    return d / (kqs::WAVES * kqs::ROWS);
+}
+
+// Gate/up, k4 stream path: a workgroup owns 16 rows of Wg and of Wu; its four
+// wavefronts take the quarters of d and add their partial sums in wavefront
+// order.  Within a quarter, 32-element blocks go in chunks of CH (CH divides
+// 8, so a chunk stays inside one super-block and needs one header per row):
+// every nibble word and the four output rows' headers of a chunk are issued
+// before its first MFMA.  Lane (row r = lane % 16, group g = lane / 16) holds
+// elements 8g .. 8g + 7 of each block of row r; the output lane (rows 4g ..
+// 4g + 3, token lane % 16) applies those rows' sub-block scales and mins.
+template <int CH>
+__global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L)
+{
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    __shared__ f32x4 red[3][2][64];
+    int t;
+    WorkItem it;
+    if (!kq_tile(L, L.I / kqs::ROWS, t, it) || it.nrows == 0 ||
+        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
+        return;
+    const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8, nsb = d / 256, nq = d / 32 / kqs::WAVES;
+    const bool sh = it.slot < 0;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i0 = (t - it.tile0) * kqs::ROWS;
+    const int r = lane & 15, g = lane >> 4;
+    const int bq = wave * nq;                          // this wavefront's first block
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
+    const uint32_t mb = k4_bytes(I, d);
+    const uint32_t *qp[2];
+    const u32x4 *hp[2];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+        const uint8_t *mat = base + m * mb;
+        qp[m] = reinterpret_cast<const uint32_t *>(mat + int64_t(i0 + r) * (d / 2)) + 4 * bq + g;
+        hp[m] = reinterpret_cast<const u32x4 *>(mat + uint32_t(I) * uint32_t(d / 2)) + int64_t(i0 + 4 * g) * nsb;
+    }
+    uint32_t q[2][CH];
+    u32x4 hd[2][4];
+    auto issue = [&](int c0) {
+        const int sb = (bq + c0) >> 3;
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+#pragma unroll
+            for (int u = 0; u < CH; ++u)
+                q[m][u] = __builtin_nontemporal_load(qp[m] + 4 * (c0 + u));
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                hd[m][rr] = hp[m][rr * nsb + sb];
+        }
+    };
+    issue(0);                                          // the first chunk goes out before the token rows
+    {
+        const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
+        const int32_t *xperm = sh ? nullptr : L.perm;
+        StageRows<4> sr;                               // one pass for d <= 2048
+        sr.load(xsrc, xperm, it.row0, n, d, 0);
+        sr.store(xs, n, d, 0);
+        sr.rest(xsrc, xperm, it.row0, n, d, xs);
+    }
+    __syncthreads();
+    const uint16_t *xrow = xs + r * ldk + 8 * g + 32 * bq;   // rows past n hold stale data: not stored
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{BF16_ONE2, BF16_ONE2, BF16_ONE2, BF16_ONE2});
+    f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nq; c0 += CH) {
+        if (c0 > 0)
+            issue(c0);
+#pragma unroll
+        for (int u = 0; u < CH; ++u) {
+            const int j = (bq + c0 + u) & 7;           // sub-block within the super-block
+            const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4 *>(xrow + 32 * (c0 + u)));
+            const f32x4 pg = mfma16(unpack_u4(q[0][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 pu = mfma16(unpack_u4(q[1][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 sx = mfma16(ones, xb, f32x4{0.f, 0.f, 0.f, 0.f});    // the token's sum over the block
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                float a, b;
+                k4_coef(hd[0][rr], j, a, b);
+                ag[rr] = fmaf(a, pg[rr], ag[rr]);
+                ag[rr] = fmaf(-b, sx[rr], ag[rr]);
+                k4_coef(hd[1][rr], j, a, b);
+                au[rr] = fmaf(a, pu[rr], au[rr]);
+                au[rr] = fmaf(-b, sx[rr], au[rr]);
+            }
+        }
+    }
+    // quarters of d added in wavefront order
+    if (wave > 0) {
+        red[wave - 1][0][lane] = ag;
+        red[wave - 1][1][lane] = au;
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+        ag[rr] = ((ag[rr] + red[0][0][lane][rr]) + red[1][0][lane][rr]) + red[2][0][lane][rr];
+        au[rr] = ((au[rr] + red[0][1][lane][rr]) + red[1][1][lane][rr]) + red[2][1][lane][rr];
+    }
+    const int j = lane & 15;
+    if (j < n) {
+        uint2 v;
+        v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
+        v.y = pack_bf16x2(silu(ag[2]) * au[2], silu(ag[3]) * au[3]);
+        uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0 + j) * I + i0 + 4 * g;
+        *reinterpret_cast<uint2 *>(act) = v;
+    }
+}
+
+// Down, k6 stream path: a workgroup owns 64 output columns (16 per wavefront)
+// over all of I, in groups of G super-blocks; the first group's low-nibble
+// words, high-part half-words, sub-block scales and super-block scales are
+// issued before the act rows are staged.  Each 32-element block holds two
+// 16-element sub-blocks: two MFMAs with the other half's weight lanes zeroed
+// (lanes with g < 2 carry elements 0 .. 15), each partial scaled by its own
+// d * sc.
+template <int G>
+__global__ void __launch_bounds__(256, 2) stream_down_kq_kernel(ExpertLaunch L)
+{
+    extern __shared__ __attribute__((aligned(16))) uint16_t as[];
+    int t;
+    WorkItem it;
+    if (!kq_tile(L, L.d / (kqs::WAVES * kqs::ROWS), t, it) || it.nrows == 0 ||
+        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
+        return;
+    constexpr int NB = 8 * G;                          // 32-element blocks per group
+    const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8, nsb = I / 256;
+    const bool sh = it.slot < 0;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int c0 = ((t - it.tile0) * kqs::WAVES + wave) * kqs::ROWS;
+    const int r = lane & 15, g = lane >> 4;
+    const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
+    const K6Planes P = k6_planes(base + 2 * k4_bytes(I, d), d, I);
+    const uint32_t *qlp = reinterpret_cast<const uint32_t *>(P.ql + int64_t(c0 + r) * (I / 2)) + g;
+    const uint16_t *qhp = reinterpret_cast<const uint16_t *>(P.qh + int64_t(c0 + r) * (I / 4)) + g;
+    uint32_t ql[NB], qh[NB];
+    u32x4 sc[4][G];
+    float dd[4][G];
+    auto issue = [&](int s0) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            ql[u] = __builtin_nontemporal_load(qlp + 4 * (8 * s0 + u));
+            qh[u] = qhp[4 * (8 * s0 + u)];
+        }
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            const int64_t row = c0 + 4 * g + rr;
+            const u32x4 *sp = reinterpret_cast<const u32x4 *>(P.sc + row * (I / 16)) + s0;
+#pragma unroll
+            for (int s = 0; s < G; ++s) {
+                sc[rr][s] = sp[s];
+                dd[rr][s] = h2f(P.d[row * nsb + s0 + s]);
+            }
+        }
+    };
+    issue(0);
+    {
+        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
+        StageRows<1> sr;                               // one pass for I <= 512
+        sr.load(asrc, nullptr, it.row0, n, I, 0);
+        sr.store(as, n, I, 0);
+        sr.rest(asrc, nullptr, it.row0, n, I, as);
+    }
+    __syncthreads();
+    const uint16_t *arow = as + r * ldk + 8 * g;       // rows past n hold stale data: not stored
+    const bool first_half = g < 2;
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsb; s0 += G) {
+        if (s0 > 0)
+            issue(s0);
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const bf16x8 ab = as_bf16x8(*reinterpret_cast<const u32x4 *>(arow + 32 * (8 * s0 + u)));
+            const bf16x8 w = unpack_k6(ql[u], qh[u]);
+            const f32x4 p0 = mfma16(first_half ? w : zero, ab, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 p1 = mfma16(first_half ? zero : w, ab, f32x4{0.f, 0.f, 0.f, 0.f});
+            const int s = u >> 3, lb = u & 7;          // super-block of the group, block within it
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                // scales 2 lb and 2 lb + 1 of the super-block: bytes 2 (lb & 1) and + 1 of word lb / 2
+                const uint32_t word = sc[rr][s][lb >> 1] >> (16 * (lb & 1));
+                acc[rr] = fmaf(dd[rr][s] * float(int(int8_t(word & 0xFFu))), p0[rr], acc[rr]);
+                acc[rr] = fmaf(dd[rr][s] * float(int(int8_t((word >> 8) & 0xFFu))), p1[rr], acc[rr]);
+            }
+        }
+    }
+    const int j = lane & 15;
+    if (j < n) {
+        const int64_t row = it.row0 + j;
+        const float w = sh ? 1.0f : L.row_weight[row];
+        uint2 v;
+        v.x = pack_bf16x2(acc[0] * w, acc[1] * w);
+        v.y = pack_bf16x2(acc[2] * w, acc[3] * w);
+        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * g) = v;
+    }
+}
+
+hipError_t launch_gateup_kq_stream(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    if (L.d % 256 != 0)
+        return hipErrorInvalidValue;
+    // chunk: 8, 4 or 2 blocks, dividing a quarter of d's blocks (d / 128)
+    const int nq = L.d / 128;
+    const size_t lds = size_t(16) * (L.d + 8) * 2;
+    if (nq % 8 == 0)
+        launch_k(stream_gateup_kq_kernel<8>, L.n_tiles, 256, lds, s, L);
+    else if (nq % 4 == 0)
+        launch_k(stream_gateup_kq_kernel<4>, L.n_tiles, 256, lds, s, L);
+    else
+        launch_k(stream_gateup_kq_kernel<2>, L.n_tiles, 256, lds, s, L);
+    return hipGetLastError();
+}
+
+hipError_t launch_down_kq_stream(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    if (L.I % 256 != 0 || L.d % 64 != 0)
+        return hipErrorInvalidValue;
+    const size_t lds = size_t(16) * (L.I + 8) * 2;
+    if ((L.I / 256) % 2 == 0)
+        launch_k(stream_down_kq_kernel<2>, L.n_tiles, 256, lds, s, L);
+    else
+        launch_k(stream_down_kq_kernel<1>, L.n_tiles, 256, lds, s, L);
+    return hipGetLastError();
+}
+
+// ============================================================== tile path
+
+namespace kqt {
+constexpr int BM = 128, BN = 128, BK = 64, THREADS = 256;
+constexpr int LDA = BK + 8;                 // bf16 elements per staged A row
+constexpr int LDQ = BK / 2 + 4;             // bytes per staged low-nibble row (36: conflict-spread)
+constexpr int LDH = BK / 4 + 4;             // bytes per staged high-part row (k6)
+constexpr int A_BYTES = BM * LDA * 2;
+constexpr int Q_BYTES = BN * LDQ;
+constexpr int H_BYTES = BN * LDH;
+constexpr int S_BYTES = BN * 16;            // four fp32 coefficients per weight row
+constexpr int STAGE = A_BYTES + Q_BYTES + H_BYTES + S_BYTES;
+constexpr size_t LDS_BYTES = size_t(2) * STAGE;
+}  // namespace kqt
+
+int tiles_gateup_kq_tile(int nrows, int d, int I)
+{
+    (void)d;
+    return ((nrows + kqt::BM - 1) / kqt::BM) * (I / 64);
+}
+
+int tiles_down_kq_tile(int nrows, int d, int I)
+{
+    (void)I;
+    return ((nrows + kqt::BM - 1) / kqt::BM) * (d / kqt::BN);
+}
+
+TileGeom geom_gateup_kq_tile(int d, int I)
+{
+    (void)d;
+    return TileGeom{kqt::BM, I / 64};
+}
+
+TileGeom geom_down_kq_tile(int d, int I)
+{
+    (void)I;
+    return TileGeom{kqt::BM, d / kqt::BN};
+}
+
+// 128 tokens x 128 weight rows per workgroup, K in stages of 64 (two
+// 32-element blocks; a stage never crosses a 256-element super-block).
+// GATEUP: tile columns 0..63 are gate rows nt*64 .. nt*64+63, columns 64..127
+// the matching up rows (k4); wavefront (wm, wn) owns rows wm*64.., gate
+// columns wn*32.. and the matching up columns, so SiLU * up forms in
+// registers.  Per stage each weight row's coefficients are decoded once into
+// LDS as fp32: gate/up {a0, a1, b0, b1} (scale d sc_j and offset dmin m_j of
+// the stage's two blocks), down {s0 .. s3} (d sc_j of its four 16-element
+// sub-blocks).  The k4 offset multiplies the tokens' sums over the block,
+// from one MFMA against ones per token block; the k6 sub-blocks are two
+// MFMAs with the other half's weight lanes zeroed.
+template <bool GATEUP>
+__global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L)
+{
+    using namespace kqt;
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds8[];
+    int n_items, n_tiles;
+    const int t = launch_tile(L, n_items, n_tiles);
+    if (t < 0)
+        return;                                   // past the device-built list's tiles
+    const WorkItem it = L.items[find_item(L.items, n_items, t)];
+    if (!slot_current(it, L.gen_dev, L.status))
+        return;
+    const bool sh = it.slot < 0;
+    const int d = L.d, I = L.I;
+    const int K = GATEUP ? d : I;
+    const int ntn = GATEUP ? I / 64 : d / BN;
+    const int local = t - it.tile0;
+    const int m0 = (local / ntn) * BM;
+    const int nt = local % ntn;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    const uint16_t *abase = reinterpret_cast<const uint16_t *>(GATEUP ? L.x : (sh ? L.act_s : L.act));
+    const int32_t *perm = (GATEUP && !sh) ? L.perm : nullptr;
+    const uint8_t *obj = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
+    const uint32_t mbytes = k4_bytes(I, d);
+
+    // A: 128 rows x 64 bf16 per stage = 8 chunks of 16 B per row; 4 per thread
+    uint32_t aoff[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = (tid >> 3) + 32 * i;
+        int64_t src = 0;
+        if (m0 + r < it.nrows)
+            src = perm ? int64_t(perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
+        aoff[i] = uint32_t(src * K) + (tid & 7) * 8;
+    }
+    auto weight_row = [&](int c) -> int {          // tile column -> row of its matrix
+        if (GATEUP)
+            return nt * 64 + (c & 63);
+        return nt * BN + c;
+    };
+    auto matrix_of = [&](int c) -> const uint8_t * {
+        if (GATEUP)
+            return obj + (c < 64 ? 0u : mbytes);
+        return obj + 2 * mbytes;
+    };
+    // low nibbles: 128 rows x 32 B per stage, 2 chunks of 16 B per row, 1 per thread
+    const int brow_l = tid >> 1, bchunk = tid & 1;
+    const uint8_t *qrow = matrix_of(brow_l) + int64_t(weight_row(brow_l)) * (K / 2) + bchunk * 16;
+    // coefficients (and the k6 high parts): thread tid < 128 takes tile column tid
+    const int cc = tid & 127;
+    const uint8_t *cmat = matrix_of(cc);
+    const int64_t crow = weight_row(cc);
+    const int rows_m = GATEUP ? I : d;
+    const u32x4 *hdr = reinterpret_cast<const u32x4 *>(cmat + uint32_t(rows_m) * uint32_t(K / 2)) + crow * (K / 256);
+    const K6Planes P = k6_planes(cmat, rows_m, K);
+
+    u32x4 ra[4], rq, rh, rc;
+    uint32_t rsc = 0;
+    uint16_t rd = 0;
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            ra[i] = *reinterpret_cast<const u32x4 *>(abase + (aoff[i] + uint32_t(k0)));
+        rq = *reinterpret_cast<const u32x4 *>(qrow + k0 / 2);
+        if (tid < 128) {
+            if (GATEUP) {
+                rc = hdr[k0 / 256];
+            } else {
+                rh = *reinterpret_cast<const u32x4 *>(P.qh + crow * (K / 4) + k0 / 4);
+                rsc = *reinterpret_cast<const uint32_t *>(P.sc + crow * (K / 16) + k0 / 16);
+                rd = P.d[crow * (K / 256) + k0 / 256];
+            }
+        }
+    };
+    auto store = [&](int buf, int k0) {
+        uint8_t *st = lds8 + buf * STAGE;
+        uint16_t *a = reinterpret_cast<uint16_t *>(st);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            *reinterpret_cast<u32x4 *>(a + ((tid >> 3) + 32 * i) * LDA + (tid & 7) * 8) = ra[i];
+        uint32_t *q = reinterpret_cast<uint32_t *>(st + A_BYTES + brow_l * LDQ + bchunk * 16);
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+            q[w] = rq[w];
+        if (tid < 128) {
+            f32x4 cf;
+            if (GATEUP) {
+                const int j0 = (k0 & 255) >> 5;
+                float a0, b0, a1, b1;
+                k4_coef(rc, j0, a0, b0);
+                k4_coef(rc, j0 + 1, a1, b1);
+                cf = f32x4{a0, a1, b0, b1};
+            } else {
+                uint32_t *h = reinterpret_cast<uint32_t *>(st + A_BYTES + Q_BYTES + cc * LDH);
+#pragma unroll
+                for (int w = 0; w < 4; ++w)
+                    h[w] = rh[w];
+                const float dv = h2f(rd);
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    cf[s] = dv * float(int(int8_t((rsc >> (8 * s)) & 0xFFu)));
+            }
+            *reinterpret_cast<f32x4 *>(st + A_BYTES + Q_BYTES + H_BYTES + cc * 16) = cf;
+        }
+    };
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int r16 = lane & 15, g = lane >> 4;
+    auto col_of = [&](int nb) -> int {              // tile column block of this wavefront
+        if (GATEUP)
+            return nb < 2 ? wn * 32 + nb * 16 : 64 + wn * 32 + (nb - 2) * 16;
+        return wn * 64 + nb * 16;
+    };
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{BF16_ONE2, BF16_ONE2, BF16_ONE2, BF16_ONE2});
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    const bool first_half = g < 2;                  // B lanes of elements 0 .. 15 of a block
+    auto compute = [&](int buf) {
+        const uint8_t *st = lds8 + buf * STAGE;
+        const uint16_t *a = reinterpret_cast<const uint16_t *>(st);
+        const uint8_t *q = st + A_BYTES;
+        const uint8_t *h = st + A_BYTES + Q_BYTES;
+        const float *cf = reinterpret_cast<const float *>(st + A_BYTES + Q_BYTES + H_BYTES);
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb) {
+            bf16x8 af[4];
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb)
+                af[mb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(a + (wm * 64 + mb * 16 + r16) * LDA + kb * 32 + g * 8));
+            if (GATEUP) {
+                f32x4 sx[4];                        // tokens' sums over the block
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+                    sx[mb] = mfma16(af[mb], ones, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb) {
+                    const int c = col_of(nb) + r16;                // B fragment: weight row c
+                    const bf16x8 bq = unpack_u4(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4));
+                    const float sa = cf[c * 4 + kb], sb = cf[c * 4 + 2 + kb];   // output column = c
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb) {
+                        const f32x4 part = mfma16(af[mb], bq, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            acc[mb][nb][rr] = fmaf(sa, part[rr], acc[mb][nb][rr]);
+                            acc[mb][nb][rr] = fmaf(-sb, sx[mb][rr], acc[mb][nb][rr]);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);   // bounds the partial sums in flight
+                }
+            } else {
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb) {
+                    const int c = col_of(nb) + r16;
+                    const bf16x8 w = unpack_k6(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4),
+                                               *reinterpret_cast<const uint16_t *>(h + c * LDH + kb * 8 + g * 2));
+                    const bf16x8 w0 = first_half ? w : zero, w1 = first_half ? zero : w;
+                    const float s0 = cf[c * 4 + 2 * kb], s1 = cf[c * 4 + 2 * kb + 1];
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb) {
+                        const f32x4 p0 = mfma16(af[mb], w0, f32x4{0.f, 0.f, 0.f, 0.f});
+                        const f32x4 p1 = mfma16(af[mb], w1, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            acc[mb][nb][rr] = fmaf(s0, p0[rr], acc[mb][nb][rr]);
+                            acc[mb][nb][rr] = fmaf(s1, p1[rr], acc[mb][nb][rr]);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);   // bounds the partial sums in flight
+                }
+            }
+        }
+    };
+
+    const int nk = K / BK;
+    load(0);
+    store(0, 0);
+    if (nk > 1)
+        load(BK);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        compute(kt & 1);
+        if (kt + 1 < nk)
+            store((kt + 1) & 1, (kt + 1) * BK);
+        if (kt + 2 < nk)
+            load((kt + 2) * BK);
+        __syncthreads();
+    }
+
+    // lane holds rows 4g + rr of each 16x16 block, column r16
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            const int row = wm * 64 + mb * 16 + 4 * g + rr;
+            if (m0 + row >= it.nrows)
+                continue;
+            const int64_t orow = int64_t(it.row0) + m0 + row;
+            if (GATEUP) {
+                uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + orow * I;
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+                    act[nt * 64 + wn * 32 + nb * 16 + r16] =
+                        f32_to_bf16(silu(acc[mb][nb][rr]) * acc[mb][nb + 2][rr]);
+            } else {
+                uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + orow * d;
+                const float w = sh ? 1.0f : L.row_weight[orow];
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb)
+                    y[nt * BN + wn * 64 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * w);
+            }
+        }
+}
+
+hipError_t launch_gateup_kq_tile(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    if (L.d % 256 != 0 || L.I % 64 != 0)
+        return hipErrorInvalidValue;
+    launch_k(tile_kq_kernel<true>, L.n_tiles, kqt::THREADS, kqt::LDS_BYTES, s, L);
+    return hipGetLastError();
+}
+
+hipError_t launch_down_kq_tile(const ExpertLaunch &L, hipStream_t s)
+{
+    if (L.n_tiles == 0)
+        return hipSuccess;
+    if (L.I % 256 != 0 || L.d % kqt::BN != 0)
+        return hipErrorInvalidValue;
+    launch_k(tile_kq_kernel<false>, L.n_tiles, kqt::THREADS, kqt::LDS_BYTES, s, L);
+    return hipGetLastError();
+}
+
+hipError_t init_kq_attributes()
+{
+    const void *ks[] = {reinterpret_cast<const void *>(&stream_gateup_kq_kernel<8>),
+                        reinterpret_cast<const void *>(&stream_gateup_kq_kernel<4>),
+                        reinterpret_cast<const void *>(&stream_gateup_kq_kernel<2>),
+                        reinterpret_cast<const void *>(&stream_down_kq_kernel<2>),
+                        reinterpret_cast<const void *>(&stream_down_kq_kernel<1>),
+                        reinterpret_cast<const void *>(&tile_kq_kernel<true>),
+                        reinterpret_cast<const void *>(&tile_kq_kernel<false>)};
+    for (const void *k : ks) {
+        const hipError_t e = allow_large_lds(k);
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace msi

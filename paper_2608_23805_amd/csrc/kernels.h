@@ -187,6 +187,32 @@ hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s);
 hipError_t init_q4_attributes();
 
+// quantized-expert mix, Wg / Wu in k4 and Wd in k6 (experts_kq.hip)
+int tiles_gateup_kq_stream(int nrows, int d, int I);
+int tiles_down_kq_stream(int nrows, int d, int I);
+int tiles_gateup_kq_tile(int nrows, int d, int I);
+int tiles_down_kq_tile(int nrows, int d, int I);
+TileGeom geom_gateup_kq_tile(int d, int I);
+TileGeom geom_down_kq_tile(int d, int I);
+hipError_t launch_gateup_kq_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_kq_stream(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_gateup_kq_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t launch_down_kq_tile(const ExpertLaunch &L, hipStream_t s);
+hipError_t init_kq_attributes();
+
+// The expert kernels of one storage format: the tile path (rows above the
+// stream threshold, and every row of an f32 layer) and the stream path, for
+// gate/up and down, with their tiles per item and tile geometry.  f32 layers
+// have no stream path and no device-built lists (null entries).
+struct KernelSet {
+    using Tiles = int (*)(int nrows, int d, int I);
+    using Geom = TileGeom (*)(int d, int I);
+    using Launch = hipError_t (*)(const ExpertLaunch &L, hipStream_t s);
+    Tiles tiles_gu_tile, tiles_gu_stream, tiles_dn_tile, tiles_dn_stream;
+    Geom geom_gu, geom_dn;
+    Launch gu_tile, gu_stream, dn_tile, dn_stream;
+};
+
 // ---- combine / publication and slot generation words (combine.hip)
 // Status word of a forward and where the combine publishes it.
 struct CombinePublish {

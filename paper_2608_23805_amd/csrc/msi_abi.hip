@@ -46,18 +46,48 @@ msi_status fail(msi_status st, const std::string &m)
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-uint64_t matrix_bytes(uint32_t wdtype, uint64_t rows, uint64_t cols)
+// bytes of a [rows, cols] matrix; for MSI_W_KQ, `down` selects Wd's k6
+// format (Wg and Wu are k4)
+uint64_t matrix_bytes(uint32_t wdtype, uint64_t rows, uint64_t cols, bool down)
 {
     switch (wdtype) {
     case MSI_W_F32: return rows * cols * 4;
     case MSI_W_BF16: return rows * cols * 2;
+    case MSI_W_KQ:
+        if (down)
+            return rows * cols / 2 + rows * cols / 4 + rows * cols / 16 + rows * (cols / 256) * 2;
+        return rows * cols / 2 + rows * (cols / 256) * 16;
     default: return rows * cols / 2 + rows * (cols / 32) * 2;
+    }
+}
+
+// expert kernels of each storage format
+const KernelSet &kernel_set(uint32_t wdtype)
+{
+    static const KernelSet f32{tiles_gateup_f32, nullptr, tiles_down_f32, nullptr, nullptr, nullptr,
+                               launch_gateup_f32, nullptr, launch_down_f32, nullptr};
+    static const KernelSet bf16{tiles_gateup_tile, tiles_gateup_stream, tiles_down_tile, tiles_down_stream,
+                                geom_gateup_tile, geom_down_tile,
+                                launch_gateup_tile, launch_gateup_stream, launch_down_tile, launch_down_stream};
+    static const KernelSet q4{tiles_gateup_q4_tile, tiles_gateup_q4_stream, tiles_down_q4_tile,
+                              tiles_down_q4_stream, geom_gateup_q4_tile, geom_down_q4_tile,
+                              launch_gateup_q4_tile, launch_gateup_q4_stream, launch_down_q4_tile,
+                              launch_down_q4_stream};
+    static const KernelSet kq{tiles_gateup_kq_tile, tiles_gateup_kq_stream, tiles_down_kq_tile,
+                              tiles_down_kq_stream, geom_gateup_kq_tile, geom_down_kq_tile,
+                              launch_gateup_kq_tile, launch_gateup_kq_stream, launch_down_kq_tile,
+                              launch_down_kq_stream};
+    switch (wdtype) {
+    case MSI_W_F32: return f32;
+    case MSI_W_Q4B32: return q4;
+    case MSI_W_KQ: return kq;
+    default: return bf16;
     }
 }
 
 uint64_t object_bytes_of(const msi_plan_desc &d)
 {
-    return 2 * matrix_bytes(d.wdtype, d.d_ff, d.d_model) + matrix_bytes(d.wdtype, d.d_model, d.d_ff);
+    return 2 * matrix_bytes(d.wdtype, d.d_ff, d.d_model, false) + matrix_bytes(d.wdtype, d.d_model, d.d_ff, true);
 }
 
 // Workspace layout for T tokens (offsets in bytes, each region 256-aligned).
@@ -1007,9 +1037,9 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
                                   hipMemcpyHostToDevice, cs));
             p->res_version[L0] = core.layer_version(L0);
         }
-        const bool q4w = d.wdtype == MSI_W_Q4B32;
-        const int tpg = q4w ? tiles_gateup_q4_stream(1, D, I) : tiles_gateup_stream(1, D, I);
-        const int tpd = q4w ? tiles_down_q4_stream(1, D, I) : tiles_down_stream(1, D, I);
+        const KernelSet &ks = kernel_set(d.wdtype);
+        const int tpg = ks.tiles_gu_stream(1, D, I);
+        const int tpd = ks.tiles_dn_stream(1, D, I);
         const int has_sh = a->shared_object ? 1 : 0;
         const int max_items = (std::min(E, T * K) + has_sh + 7) / 8 * 8;   // whole rounds of 8 items (XCDs)
         if (!p->status_clean)
@@ -1036,10 +1066,8 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         ExpertLaunch G = X, Dn = X;
         G.n_tiles = max_items * tpg;
         Dn.n_tiles = max_items * tpd;
-        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs,
-                               [&] { return q4w ? launch_gateup_q4_stream(G, cs) : launch_gateup_stream(G, cs); }));
-        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
-                               [&] { return q4w ? launch_down_q4_stream(Dn, cs) : launch_down_stream(Dn, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs, [&] { return ks.gu_stream(G, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs, [&] { return ks.dn_stream(Dn, cs); }));
         const CombinePublish pub{p->status_dev, p->arrive_dev + ARRIVE_COMBINE, p->tail_hdev, a->r.demand};
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
             return launch_combine(B.y, has_sh ? B.ys : nullptr, false, a->r.inv, a->out, pub, T, K,
@@ -1085,7 +1113,7 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
                                   hipMemcpyHostToDevice, cs));
             p->res_version[L0] = core.layer_version(L0);
         }
-        const bool q4w = d.wdtype == MSI_W_Q4B32;
+        const KernelSet &ks = kernel_set(d.wdtype);
         const int thr = int(g_stream_threshold);
         const int has_sh = a->shared_object ? 1 : 0;
         WorklistArgs W{};
@@ -1101,10 +1129,10 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         W.T = T;
         W.thr = thr;
         W.has_shared = has_sh;
-        W.gu = q4w ? geom_gateup_q4_tile(D, I) : geom_gateup_tile(D, I);
-        W.dn = q4w ? geom_down_q4_tile(D, I) : geom_down_tile(D, I);
-        W.per_gu_stream = q4w ? tiles_gateup_q4_stream(1, D, I) : tiles_gateup_stream(1, D, I);
-        W.per_dn_stream = q4w ? tiles_down_q4_stream(1, D, I) : tiles_down_stream(1, D, I);
+        W.gu = ks.geom_gu(D, I);
+        W.dn = ks.geom_dn(D, I);
+        W.per_gu_stream = ks.tiles_gu_stream(1, D, I);
+        W.per_dn_stream = ks.tiles_dn_stream(1, D, I);
         if (!p->status_clean)
             HIP_OK(launch_clear_word(p->status_dev, cs));
         p->status_clean = false;
@@ -1148,15 +1176,10 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         DS.items = W.items[3];
         DS.dev_n = p->dcount_dev + 3;
         DS.n_tiles = round8(int64_t(n_stream_max) * W.per_dn_stream);
-        HIP_OK(p->timed_launch(MSI_K_GATEUP_TILE, cs,
-                               [&] { return q4w ? launch_gateup_q4_tile(GT, cs) : launch_gateup_tile(GT, cs); }));
-        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs, [&] {
-            return q4w ? launch_gateup_q4_stream(GS, cs) : launch_gateup_stream(GS, cs);
-        }));
-        HIP_OK(p->timed_launch(MSI_K_DOWN_TILE, cs,
-                               [&] { return q4w ? launch_down_q4_tile(DT, cs) : launch_down_tile(DT, cs); }));
-        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs,
-                               [&] { return q4w ? launch_down_q4_stream(DS, cs) : launch_down_stream(DS, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_TILE, cs, [&] { return ks.gu_tile(GT, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_GATEUP_STREAM, cs, [&] { return ks.gu_stream(GS, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_TILE, cs, [&] { return ks.dn_tile(DT, cs); }));
+        HIP_OK(p->timed_launch(MSI_K_DOWN_STREAM, cs, [&] { return ks.dn_stream(DS, cs); }));
         // large grid: no arrival counter (the next forward clears the status word)
         const CombinePublish pub{p->status_dev, nullptr, p->tail_hdev, a->r.demand};
         HIP_OK(p->timed_launch(MSI_K_COMBINE, cs, [&] {
@@ -1203,7 +1226,7 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         return fail(sst, core.error());
 
     // ---- work tables: per round, gate/up and down launches of each path
-    enum Kind { GU_TILE, GU_STREAM, GU_F32, DN_TILE, DN_STREAM, DN_F32, GU_Q4T, GU_Q4S, DN_Q4T, DN_Q4S, NKIND };
+    enum Kind { GU_TILE, GU_STREAM, DN_TILE, DN_STREAM, NKIND };
     struct Launch {
         int kind;
         size_t off;
@@ -1213,7 +1236,7 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
     std::vector<std::vector<Launch>> launches(sched.rounds.size());
     std::vector<WorkItem> table;
     const bool f32 = d.wdtype == MSI_W_F32;
-    const bool q4 = d.wdtype == MSI_W_Q4B32;
+    const KernelSet &ks = kernel_set(d.wdtype);
     auto add_launch = [&](size_t r, int kind, const std::vector<WorkItem> &items) {
         if (items.empty())
             return;
@@ -1222,16 +1245,10 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         for (WorkItem w : items) {
             int n;
             switch (kind) {
-            case GU_TILE: n = tiles_gateup_tile(w.nrows, D, I); break;
-            case GU_STREAM: n = tiles_gateup_stream(w.nrows, D, I); break;
-            case GU_F32: n = tiles_gateup_f32(w.nrows, D, I); break;
-            case DN_TILE: n = tiles_down_tile(w.nrows, D, I); break;
-            case DN_STREAM: n = tiles_down_stream(w.nrows, D, I); break;
-            case DN_F32: n = tiles_down_f32(w.nrows, D, I); break;
-            case GU_Q4T: n = tiles_gateup_q4_tile(w.nrows, D, I); break;
-            case GU_Q4S: n = tiles_gateup_q4_stream(w.nrows, D, I); break;
-            case DN_Q4T: n = tiles_down_q4_tile(w.nrows, D, I); break;
-            default: n = tiles_down_q4_stream(w.nrows, D, I); break;
+            case GU_TILE: n = ks.tiles_gu_tile(w.nrows, D, I); break;
+            case GU_STREAM: n = ks.tiles_gu_stream(w.nrows, D, I); break;
+            case DN_TILE: n = ks.tiles_dn_tile(w.nrows, D, I); break;
+            default: n = ks.tiles_dn_stream(w.nrows, D, I); break;
             }
             w.tile0 = tiles;
             tiles += n;
@@ -1254,10 +1271,10 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
                        counts[si.expert], 0};
             (f32 || uint32_t(w.nrows) > thr ? tile_items : stream_items).push_back(w);
         }
-        add_launch(r, f32 ? GU_F32 : q4 ? GU_Q4T : GU_TILE, tile_items);
-        add_launch(r, q4 ? GU_Q4S : GU_STREAM, stream_items);
-        add_launch(r, f32 ? DN_F32 : q4 ? DN_Q4T : DN_TILE, tile_items);
-        add_launch(r, q4 ? DN_Q4S : DN_STREAM, stream_items);
+        add_launch(r, GU_TILE, tile_items);
+        add_launch(r, GU_STREAM, stream_items);      // (empty for f32 layers)
+        add_launch(r, DN_TILE, tile_items);
+        add_launch(r, DN_STREAM, stream_items);
     }
     if (table.size() > p->table_cap)
         return fail(MSI_E_INVALID_ARG, "internal: schedule table overflow");
@@ -1371,22 +1388,14 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
             L.shared_w = static_cast<const uint8_t *>(a->shared_object);
             L.act_s = B.act_s;
             L.ys = B.ys;
-            static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_EXPERT_F32,
-                                             MSI_K_DOWN_TILE,   MSI_K_DOWN_STREAM,   MSI_K_EXPERT_F32,
-                                             MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_DOWN_TILE,
+            static const int tkind[NKIND] = {MSI_K_GATEUP_TILE, MSI_K_GATEUP_STREAM, MSI_K_DOWN_TILE,
                                              MSI_K_DOWN_STREAM};
-            const hipError_t e = p->timed_launch(tkind[l.kind], cs, [&] {
+            const hipError_t e = p->timed_launch(f32 ? MSI_K_EXPERT_F32 : tkind[l.kind], cs, [&] {
                 switch (l.kind) {
-                case GU_TILE: return launch_gateup_tile(L, cs);
-                case GU_STREAM: return launch_gateup_stream(L, cs);
-                case GU_F32: return launch_gateup_f32(L, cs);
-                case DN_TILE: return launch_down_tile(L, cs);
-                case DN_STREAM: return launch_down_stream(L, cs);
-                case DN_F32: return launch_down_f32(L, cs);
-                case GU_Q4T: return launch_gateup_q4_tile(L, cs);
-                case GU_Q4S: return launch_gateup_q4_stream(L, cs);
-                case DN_Q4T: return launch_down_q4_tile(L, cs);
-                default: return launch_down_q4_stream(L, cs);
+                case GU_TILE: return ks.gu_tile(L, cs);
+                case GU_STREAM: return ks.gu_stream(L, cs);
+                case DN_TILE: return ks.dn_tile(L, cs);
+                default: return ks.dn_stream(L, cs);
                 }
             });
             if (e != hipSuccess) {

@@ -35,8 +35,10 @@ PlanCore::PlanCore(const msi_plan_desc &d, uint64_t object_bytes, const std::vec
         { fail(MSI_E_INVALID_ARG, "d_ff must be a positive multiple of 128"); return; }
     if (d.top_k == 0 || d.top_k > d.n_experts || d.top_k > 16)
         { fail(MSI_E_INVALID_ARG, "top_k must be in [1, min(n_experts, 16)]"); return; }
-    if (d.wdtype > MSI_W_Q4B32)
+    if (d.wdtype > MSI_W_KQ)
         { fail(MSI_E_INVALID_ARG, "unknown wdtype"); return; }
+    if (d.wdtype == MSI_W_KQ && d.d_ff % 256 != 0)
+        { fail(MSI_E_INVALID_ARG, "the KQ format needs d_ff to be a multiple of 256"); return; }
     zero_cache_ = d.slots_per_layer == 0;
     pool_slots_ = zero_cache_ ? (d.transient_slots ? d.transient_slots : 8u) : d.slots_per_layer;
     if (zero_cache_ && pool_slots_ < 2)

@@ -115,6 +115,11 @@ WORKLOADS = {
                            prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
     "decode_q4": Workload("decode_q4", 5, LayerShape(1, 2048, 512, 10, 512, "q4b32"),
                           prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
+    # the quantized-expert mix (Wg, Wu 4.5 bits per weight, Wd 6.5625)
+    "prefill_kq": Workload("prefill_kq", 6, LayerShape(32768, 2048, 512, 10, 512, "kq"),
+                           prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
+    "decode_kq": Workload("decode_kq", 6, LayerShape(16, 2048, 512, 10, 512, "kq"),
+                          prior="zipf", prior_param=1.5, tau=0.3, capacity=512),
 }
 
 

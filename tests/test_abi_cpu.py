@@ -65,6 +65,8 @@ def _create(msi, **over):
     ("bad_stride", -1, "slot_stride"),
     ("bad_version", -1, "abi_version"),
     ("window_index", -1, "out of range"),
+    ("bad_wdtype", -1, "unknown wdtype"),
+    ("kq_d_ff", -1, "multiple of 256"),
 ])
 def test_manifest_rejections(case, status, fragment):
     import paper_2608_23805_amd as msi
@@ -78,9 +80,24 @@ def test_manifest_rejections(case, status, fragment):
         "bad_stride": dict(slot_stride=1000),
         "bad_version": dict(abi_version=99),
         "window_index": dict(objects=[(0, 0, 3, 0, ob)]),
+        "bad_wdtype": dict(wdtype=4),
+        "kq_d_ff": dict(wdtype=msi.MSI_W_KQ),        # d_ff = 128: not whole 256-element super-blocks
     }[case]
     st, err = _create(msi, **over)
     assert st == status and fragment in err, (st, err)
+
+
+def test_object_sizes_agree():
+    """The binding's object sizes are the generators' for every format
+    (the quantized mix: two k4 matrices and one k6 matrix)."""
+    import paper_2608_23805_amd as msi
+    import synth
+    for wd in ("f32", "bf16", "q4b32", "kq"):
+        for d, I in ((256, 256), (2048, 512), (512, 768)):
+            assert msi.object_nbytes(d, I, wd) == synth.object_nbytes(d, I, wd), (wd, d, I)
+    # 4.5 bits per weight for Wg / Wu, 6.5625 for Wd
+    assert synth.k4_matrix_nbytes(512, 2048) * 8 == 4.5 * 512 * 2048
+    assert synth.k6_matrix_nbytes(2048, 512) * 8 == 6.5625 * 512 * 2048
 
 
 def test_null_arguments():
