@@ -13,18 +13,21 @@
 //    d [rows, cols/256]; q = low | high << 4 and value = d sc_j (q - 32) for
 //    the j-th 16-element sub-block.
 //
-// The integers q and q - 32 are exact in bf16, so every MFMA partial over a
-// sub-block is an exact-product fp32 sum; the sub-block's scale (and the k4
-// min times the tokens' sum over the sub-block, from one more MFMA against a
-// fragment of ones) is then applied in fp32.  A 16x16x32 MFMA spans one k4
-// sub-block, or two k6 sub-blocks: those are split by zeroing the operand
-// lanes of the other half (lanes 0..31 carry elements 0..15 of the 32).
+// The k6 integers q - 32 and the k4 integers 128 + q are exact in bf16, so
+// every MFMA partial over a sub-block is a sum of exact products in fp32; the
+// sub-block's scale is then applied in fp32.  The k4 min term takes the
+// tokens' sums over the sub-block (one more MFMA, against a fragment of ones)
+// times dmin m_j + 128 d sc_j, which also removes the 128 of the operands.  A
+// 16x16x32 MFMA spans one k4 sub-block, or two k6 sub-blocks: those are split
+// by zeroing the weight lanes of the other half (lanes 0..31 carry elements
+// 0..15 of the 32).
 //
-//  * stream path (<= 16 tokens per expert): weights as the A operand read
-//    straight from memory, tokens as the B operand from LDS, the layout of the
-//    4-bit stream kernels;
+//  * stream path (<= 16 tokens per expert): tokens as the A operand and
+//    weights as the B operand, both read straight from memory, so each output
+//    lane holds one weight row (and that row's coefficients) for four tokens;
 //  * tile path: 128 tokens x 128 weight rows per workgroup, packed weights,
-//    headers and scales staged in LDS, unpacked while the fragments are built.
+//    headers and scales staged in LDS (the coefficients decoded once per
+//    stage into fp32), unpacked while the fragments are built.
 #include "common.h"
 #include "kernels.h"
 
@@ -36,15 +39,19 @@ constexpr uint32_t BF16_ONE2 = 0x3F803F80u;        // two bf16 1.0
 
 __device__ __forceinline__ float h2f(uint16_t h) { return float(__builtin_bit_cast(_Float16, h)); }
 
-// 8 unsigned nibbles (element e at bits 4e) -> 8 exact bf16 values
-__device__ __forceinline__ bf16x8 unpack_u4(uint32_t q)
+// 8 unsigned nibbles (element e at bits 4e) -> 8 bf16 values 128 + q, exact
+// (bf16 numbers in [128, 256) are the integers: bits 0x4300 | q).  A partial
+// sum over these is the partial over q plus 128 times the sum of the other
+// operand, which the callers subtract with the sub-block's min term.
+__device__ __forceinline__ bf16x8 unpack_u4_128(uint32_t q)
 {
+    const uint32_t ev = q & 0x0F0F0F0Fu;               // elements 0, 2, 4, 6 in bytes 0..3
+    const uint32_t od = (q >> 4) & 0x0F0F0F0Fu;        // elements 1, 3, 5, 7
     u32x4 r;
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        const uint32_t lo = (q >> (8 * h)) & 15u, hi = (q >> (8 * h + 4)) & 15u;
-        r[h] = (__float_as_uint(float(lo)) >> 16) | (__float_as_uint(float(hi)) & 0xFFFF0000u);
-    }
+    r[0] = (ev & 0xFFu) | ((od & 0xFFu) << 16) | 0x43004300u;
+    r[1] = ((ev >> 8) & 0xFFu) | ((od << 8) & 0xFF0000u) | 0x43004300u;
+    r[2] = ((ev >> 16) & 0xFFu) | (od & 0xFF0000u) | 0x43004300u;
+    r[3] = (ev >> 24) | ((od >> 8) & 0xFF0000u) | 0x43004300u;
     return __builtin_bit_cast(bf16x8, r);
 }
 
@@ -69,6 +76,14 @@ __device__ __forceinline__ void k4_coef(const u32x4 &h, int j, float &a, float &
     const uint64_t mn = uint64_t(h[2] >> 16) | (uint64_t(h[3]) << 16);
     a = h2f(uint16_t(h[0])) * float(uint32_t(sc >> (6 * j)) & 63u);
     b = h2f(uint16_t(h[0] >> 16)) * float(uint32_t(mn >> (6 * j)) & 63u);
+}
+
+// the same with the min coefficient taken against partials over 128 + q:
+// a (P + 128 S) - (b + 128 a) S = a P - b S
+__device__ __forceinline__ void k4_coef128(const u32x4 &h, int j, float &a, float &b)
+{
+    k4_coef(h, j, a, b);
+    b = fmaf(128.0f, a, b);
 }
 
 __host__ __device__ __forceinline__ uint32_t k4_bytes(uint32_t rows, uint32_t cols)
@@ -132,25 +147,66 @@ int tiles_down_kq_stream(int nrows, int d, int I)
     return d / (kqs::WAVES * kqs::ROWS);
 }
 
+// Stream-path weight staging.  A wavefront's weights are 16 rows of W bytes
+// each (its share of one row); per-lane 4-byte loads of the MFMA layout would
+// touch 16 rows per load instruction, so the wavefront instead reads them with
+// 16-byte loads that run along the rows (each instruction covers 64 / (W / 16)
+// rows), writes them to its own LDS region, and reads the MFMA words back.
+// Rows are padded by 16 bytes there, which puts the 64 lanes' word reads on
+// distinct banks.  The region is the wavefront's alone: it needs no barrier
+// (a wavefront's LDS operations complete in order).
+template <int W>
+struct WaveRows {
+    static constexpr int RS = W + 16;                  // LDS bytes per row
+    static constexpr int CPR = W / 16;                 // 16-byte chunks per row
+    static constexpr int NL = (16 * CPR + 63) / 64;    // load instructions
+    u32x4 v[NL];
+
+    // rows row0 .. row0 + 15 of stride `stride` bytes, W bytes from `src` on
+    __device__ __forceinline__ void load(const uint8_t *src, int64_t stride, int lane)
+    {
+#pragma unroll
+        for (int k = 0; k < NL; ++k) {
+            const int ci = 64 * k + lane, row = ci / CPR, ch = ci % CPR;
+            if (row < 16)
+                v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + row * stride + 16 * ch));
+        }
+    }
+    __device__ __forceinline__ void store(uint8_t *lds, int lane) const
+    {
+#pragma unroll
+        for (int k = 0; k < NL; ++k) {
+            const int ci = 64 * k + lane, row = ci / CPR, ch = ci % CPR;
+            if (row < 16)
+                *reinterpret_cast<u32x4 *>(lds + row * RS + 16 * ch) = v[k];
+        }
+    }
+};
+
 // Gate/up, k4 stream path: a workgroup owns 16 rows of Wg and of Wu; its four
 // wavefronts take the quarters of d and add their partial sums in wavefront
-// order.  Within a quarter, 32-element blocks go in chunks of CH (CH divides
-// 8, so a chunk stays inside one super-block and needs one header per row):
-// every nibble word and the four output rows' headers of a chunk are issued
-// before its first MFMA.  Lane (row r = lane % 16, group g = lane / 16) holds
-// elements 8g .. 8g + 7 of each block of row r; the output lane (rows 4g ..
-// 4g + 3, token lane % 16) applies those rows' sub-block scales and mins.
+// order.  Tokens are the A operand and weights the B operand, so lane
+// (r = lane % 16, g = lane / 16) holds elements 8g .. 8g + 7 of each block of
+// token r and of weight row i0 + r, and its outputs are tokens 4g .. 4g + 3
+// of weight row i0 + r: one row's sub-block coefficients per lane.  Token
+// fragments come straight from global memory (the few rows of a decode step
+// stay in cache; lanes past the item's rows repeat its last row and are not
+// stored); weights go through WaveRows.  Blocks go in chunks of CH (CH
+// divides 8, or is 16: whole super-blocks), each chunk's loads issued before
+// its first MFMA.
 template <int CH>
 __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    using Rows = WaveRows<16 * CH>;
+    __shared__ __attribute__((aligned(16))) uint8_t wst[kqs::WAVES][2][16 * Rows::RS];
     __shared__ f32x4 red[3][2][64];
     int t;
     WorkItem it;
     if (!kq_tile(L, L.I / kqs::ROWS, t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8, nsb = d / 256, nq = d / 32 / kqs::WAVES;
+    constexpr int HS = CH > 8 ? CH / 8 : 1;            // super-blocks per chunk
+    const int n = it.nrows, d = L.d, I = L.I, nsb = d / 256, nq = d / 32 / kqs::WAVES;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int i0 = (t - it.tile0) * kqs::ROWS;
@@ -158,60 +214,58 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
     const int bq = wave * nq;                          // this wavefront's first block
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mb = k4_bytes(I, d);
-    const uint32_t *qp[2];
+    const uint8_t *qrows[2];
     const u32x4 *hp[2];
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
         const uint8_t *mat = base + m * mb;
-        qp[m] = reinterpret_cast<const uint32_t *>(mat + int64_t(i0 + r) * (d / 2)) + 4 * bq + g;
-        hp[m] = reinterpret_cast<const u32x4 *>(mat + uint32_t(I) * uint32_t(d / 2)) + int64_t(i0 + 4 * g) * nsb;
+        qrows[m] = mat + int64_t(i0) * (d / 2) + 16 * bq;
+        hp[m] = reinterpret_cast<const u32x4 *>(mat + uint32_t(I) * uint32_t(d / 2)) + int64_t(i0 + r) * nsb;
     }
-    uint32_t q[2][CH];
-    u32x4 hd[2][4];
+    const int tr = min(r, n - 1);
+    const int64_t xrow = sh ? int64_t(it.row0 + tr) : int64_t(L.perm[it.row0 + tr]);
+    const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + 8 * g + 32 * bq;
+    Rows wr[2];
+    u32x4 xv[CH], hd[2][HS];
     auto issue = [&](int c0) {
-        const int sb = (bq + c0) >> 3;
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int m = 0; m < 2; ++m)
+            wr[m].load(qrows[m] + 16 * c0, d / 2, lane);
 #pragma unroll
-            for (int u = 0; u < CH; ++u)
-                q[m][u] = __builtin_nontemporal_load(qp[m] + 4 * (c0 + u));
+        for (int u = 0; u < CH; ++u)
+            xv[u] = *reinterpret_cast<const u32x4 *>(xp + 32 * (c0 + u));
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                hd[m][rr] = hp[m][rr * nsb + sb];
-        }
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int h = 0; h < HS; ++h)
+                hd[m][h] = hp[m][((bq + c0) >> 3) + h];
     };
-    issue(0);                                          // the first chunk goes out before the token rows
-    {
-        const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
-        const int32_t *xperm = sh ? nullptr : L.perm;
-        StageRows<4> sr;                               // one pass for d <= 2048
-        sr.load(xsrc, xperm, it.row0, n, d, 0);
-        sr.store(xs, n, d, 0);
-        sr.rest(xsrc, xperm, it.row0, n, d, xs);
-    }
-    __syncthreads();
-    const uint16_t *xrow = xs + r * ldk + 8 * g + 32 * bq;   // rows past n hold stale data: not stored
     const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{BF16_ONE2, BF16_ONE2, BF16_ONE2, BF16_ONE2});
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
     for (int c0 = 0; c0 < nq; c0 += CH) {
-        if (c0 > 0)
-            issue(c0);
+        issue(c0);
+        wr[0].store(wst[wave][0], lane);
+        wr[1].store(wst[wave][1], lane);
+        const uint8_t *q0 = wst[wave][0] + r * Rows::RS + 4 * g, *q1 = wst[wave][1] + r * Rows::RS + 4 * g;
 #pragma unroll
         for (int u = 0; u < CH; ++u) {
             const int j = (bq + c0 + u) & 7;           // sub-block within the super-block
-            const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4 *>(xrow + 32 * (c0 + u)));
-            const f32x4 pg = mfma16(unpack_u4(q[0][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
-            const f32x4 pu = mfma16(unpack_u4(q[1][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
-            const f32x4 sx = mfma16(ones, xb, f32x4{0.f, 0.f, 0.f, 0.f});    // the token's sum over the block
+            const int h = CH > 8 ? u >> 3 : 0;
+            const bf16x8 xb = as_bf16x8(xv[u]);
+            const f32x4 pg = mfma16(xb, unpack_u4_128(*reinterpret_cast<const uint32_t *>(q0 + 16 * u)),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 pu = mfma16(xb, unpack_u4_128(*reinterpret_cast<const uint32_t *>(q1 + 16 * u)),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 sx = mfma16(xb, ones, f32x4{0.f, 0.f, 0.f, 0.f});    // the tokens' sums over the block
+            float a_g, b_g, a_u, b_u;
+            k4_coef128(hd[0][h], j, a_g, b_g);
+            k4_coef128(hd[1][h], j, a_u, b_u);
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                float a, b;
-                k4_coef(hd[0][rr], j, a, b);
-                ag[rr] = fmaf(a, pg[rr], ag[rr]);
-                ag[rr] = fmaf(-b, sx[rr], ag[rr]);
-                k4_coef(hd[1][rr], j, a, b);
-                au[rr] = fmaf(a, pu[rr], au[rr]);
-                au[rr] = fmaf(-b, sx[rr], au[rr]);
+            for (int i = 0; i < 4; ++i) {
+                ag[i] = fmaf(a_g, pg[i], ag[i]);
+                ag[i] = fmaf(-b_g, sx[i], ag[i]);
+                au[i] = fmaf(a_u, pu[i], au[i]);
+                au[i] = fmaf(-b_u, sx[i], au[i]);
             }
         }
     }
@@ -223,107 +277,103 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
     __syncthreads();
     if (wave != 0)
         return;
+    uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0) * I + i0 + r;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-        ag[rr] = ((ag[rr] + red[0][0][lane][rr]) + red[1][0][lane][rr]) + red[2][0][lane][rr];
-        au[rr] = ((au[rr] + red[0][1][lane][rr]) + red[1][1][lane][rr]) + red[2][1][lane][rr];
-    }
-    const int j = lane & 15;
-    if (j < n) {
-        uint2 v;
-        v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
-        v.y = pack_bf16x2(silu(ag[2]) * au[2], silu(ag[3]) * au[3]);
-        uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0 + j) * I + i0 + 4 * g;
-        *reinterpret_cast<uint2 *>(act) = v;
+    for (int i = 0; i < 4; ++i) {
+        const float gv = ((ag[i] + red[0][0][lane][i]) + red[1][0][lane][i]) + red[2][0][lane][i];
+        const float uv = ((au[i] + red[0][1][lane][i]) + red[1][1][lane][i]) + red[2][1][lane][i];
+        if (4 * g + i < n)
+            act[int64_t(4 * g + i) * I] = f32_to_bf16(silu(gv) * uv);
     }
 }
 
 // Down, k6 stream path: a workgroup owns 64 output columns (16 per wavefront)
-// over all of I, in groups of G super-blocks; the first group's low-nibble
-// words, high-part half-words, sub-block scales and super-block scales are
-// issued before the act rows are staged.  Each 32-element block holds two
-// 16-element sub-blocks: two MFMAs with the other half's weight lanes zeroed
-// (lanes with g < 2 carry elements 0 .. 15), each partial scaled by its own
-// d * sc.
+// over all of I, in groups of G super-blocks whose low nibbles and high parts
+// (through WaveRows), act fragments and this lane's sub-block and
+// super-block scales are issued together.  Act rows are the A operand, read
+// straight from global memory (lanes past the item's rows repeat its last
+// row), and weights the B operand (lane: token r / weight row c0 + r,
+// elements 8g .. 8g + 7 of each block; outputs: tokens 4g .. 4g + 3 of column
+// c0 + r).  Each 32-element block holds two 16-element sub-blocks: two MFMAs
+// with the other half's weight lanes zeroed (lanes with g < 2 carry elements
+// 0 .. 15), each partial scaled by its own d * sc.
 template <int G>
 __global__ void __launch_bounds__(256, 2) stream_down_kq_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t as[];
+    constexpr int NB = 8 * G;                          // 32-element blocks per group
+    using QL = WaveRows<16 * NB>;                      // 16 bytes of low nibbles per block
+    using QH = WaveRows<8 * NB>;                       // 8 bytes of high parts per block
+    __shared__ __attribute__((aligned(16))) uint8_t lst[kqs::WAVES][16 * QL::RS];
+    __shared__ __attribute__((aligned(16))) uint8_t hst[kqs::WAVES][16 * QH::RS];
     int t;
     WorkItem it;
     if (!kq_tile(L, L.d / (kqs::WAVES * kqs::ROWS), t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    constexpr int NB = 8 * G;                          // 32-element blocks per group
-    const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8, nsb = I / 256;
+    const int n = it.nrows, d = L.d, I = L.I, nsb = I / 256;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c0 = ((t - it.tile0) * kqs::WAVES + wave) * kqs::ROWS;
     const int r = lane & 15, g = lane >> 4;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const K6Planes P = k6_planes(base + 2 * k4_bytes(I, d), d, I);
-    const uint32_t *qlp = reinterpret_cast<const uint32_t *>(P.ql + int64_t(c0 + r) * (I / 2)) + g;
-    const uint16_t *qhp = reinterpret_cast<const uint16_t *>(P.qh + int64_t(c0 + r) * (I / 4)) + g;
-    uint32_t ql[NB], qh[NB];
-    u32x4 sc[4][G];
-    float dd[4][G];
+    const int64_t row = c0 + r;                        // this lane's weight row (output column)
+    const uint8_t *qlrows = P.ql + int64_t(c0) * (I / 2);
+    const uint8_t *qhrows = P.qh + int64_t(c0) * (I / 4);
+    const u32x4 *scp = reinterpret_cast<const u32x4 *>(P.sc + row * (I / 16));
+    const uint16_t *ap = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act) +
+                         int64_t(it.row0 + min(r, n - 1)) * I + 8 * g;
+    QL wl;
+    QH wh;
+    u32x4 av[NB], sc[G];
+    float dd[G];
     auto issue = [&](int s0) {
+        wl.load(qlrows + 128 * s0, I / 2, lane);
+        wh.load(qhrows + 64 * s0, I / 4, lane);
 #pragma unroll
-        for (int u = 0; u < NB; ++u) {
-            ql[u] = __builtin_nontemporal_load(qlp + 4 * (8 * s0 + u));
-            qh[u] = qhp[4 * (8 * s0 + u)];
-        }
+        for (int u = 0; u < NB; ++u)
+            av[u] = *reinterpret_cast<const u32x4 *>(ap + 32 * (8 * s0 + u));
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            const int64_t row = c0 + 4 * g + rr;
-            const u32x4 *sp = reinterpret_cast<const u32x4 *>(P.sc + row * (I / 16)) + s0;
-#pragma unroll
-            for (int s = 0; s < G; ++s) {
-                sc[rr][s] = sp[s];
-                dd[rr][s] = h2f(P.d[row * nsb + s0 + s]);
-            }
+        for (int s = 0; s < G; ++s) {
+            sc[s] = scp[s0 + s];
+            dd[s] = h2f(P.d[row * nsb + s0 + s]);
         }
     };
-    issue(0);
-    {
-        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
-        StageRows<1> sr;                               // one pass for I <= 512
-        sr.load(asrc, nullptr, it.row0, n, I, 0);
-        sr.store(as, n, I, 0);
-        sr.rest(asrc, nullptr, it.row0, n, I, as);
-    }
-    __syncthreads();
-    const uint16_t *arow = as + r * ldk + 8 * g;       // rows past n hold stale data: not stored
     const bool first_half = g < 2;
     const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < nsb; s0 += G) {
-        if (s0 > 0)
-            issue(s0);
+        issue(s0);
+        wl.store(lst[wave], lane);
+        wh.store(hst[wave], lane);
+        const uint8_t *lq = lst[wave] + r * QL::RS + 4 * g, *hq = hst[wave] + r * QH::RS + 2 * g;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const bf16x8 ab = as_bf16x8(*reinterpret_cast<const u32x4 *>(arow + 32 * (8 * s0 + u)));
-            const bf16x8 w = unpack_k6(ql[u], qh[u]);
-            const f32x4 p0 = mfma16(first_half ? w : zero, ab, f32x4{0.f, 0.f, 0.f, 0.f});
-            const f32x4 p1 = mfma16(first_half ? zero : w, ab, f32x4{0.f, 0.f, 0.f, 0.f});
+            const bf16x8 ab = as_bf16x8(av[u]);
+            const bf16x8 w = unpack_k6(*reinterpret_cast<const uint32_t *>(lq + 16 * u),
+                                       *reinterpret_cast<const uint16_t *>(hq + 8 * u));
+            const f32x4 p0 = mfma16(ab, first_half ? w : zero, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 p1 = mfma16(ab, first_half ? zero : w, f32x4{0.f, 0.f, 0.f, 0.f});
             const int s = u >> 3, lb = u & 7;          // super-block of the group, block within it
+            // scales 2 lb and 2 lb + 1 of the super-block: bytes 2 (lb & 1) and + 1 of word lb / 2
+            const uint32_t word = sc[s][lb >> 1] >> (16 * (lb & 1));
+            const float s0v = dd[s] * float(int(int8_t(word & 0xFFu)));
+            const float s1v = dd[s] * float(int(int8_t((word >> 8) & 0xFFu)));
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                // scales 2 lb and 2 lb + 1 of the super-block: bytes 2 (lb & 1) and + 1 of word lb / 2
-                const uint32_t word = sc[rr][s][lb >> 1] >> (16 * (lb & 1));
-                acc[rr] = fmaf(dd[rr][s] * float(int(int8_t(word & 0xFFu))), p0[rr], acc[rr]);
-                acc[rr] = fmaf(dd[rr][s] * float(int(int8_t((word >> 8) & 0xFFu))), p1[rr], acc[rr]);
+            for (int i = 0; i < 4; ++i) {
+                acc[i] = fmaf(s0v, p0[i], acc[i]);
+                acc[i] = fmaf(s1v, p1[i], acc[i]);
             }
         }
     }
-    const int j = lane & 15;
-    if (j < n) {
-        const int64_t row = it.row0 + j;
-        const float w = sh ? 1.0f : L.row_weight[row];
-        uint2 v;
-        v.x = pack_bf16x2(acc[0] * w, acc[1] * w);
-        v.y = pack_bf16x2(acc[2] * w, acc[3] * w);
-        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * g) = v;
+    uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + int64_t(it.row0) * d + c0 + r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int tok = 4 * g + i;
+        if (tok < n) {
+            const float w = sh ? 1.0f : L.row_weight[it.row0 + tok];
+            y[int64_t(tok) * d] = f32_to_bf16(acc[i] * w);
+        }
     }
 }
 
@@ -333,15 +383,16 @@ hipError_t launch_gateup_kq_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     if (L.d % 256 != 0)
         return hipErrorInvalidValue;
-    // chunk: 8, 4 or 2 blocks, dividing a quarter of d's blocks (d / 128)
+    // chunk: 16, 8, 4 or 2 blocks, dividing a quarter of d's blocks (d / 128)
     const int nq = L.d / 128;
-    const size_t lds = size_t(16) * (L.d + 8) * 2;
-    if (nq % 8 == 0)
-        launch_k(stream_gateup_kq_kernel<8>, L.n_tiles, 256, lds, s, L);
+    if (nq % 16 == 0)
+        launch_k(stream_gateup_kq_kernel<16>, L.n_tiles, 256, 0, s, L);
+    else if (nq % 8 == 0)
+        launch_k(stream_gateup_kq_kernel<8>, L.n_tiles, 256, 0, s, L);
     else if (nq % 4 == 0)
-        launch_k(stream_gateup_kq_kernel<4>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_kq_kernel<4>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_gateup_kq_kernel<2>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_kq_kernel<2>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -351,18 +402,17 @@ hipError_t launch_down_kq_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     if (L.I % 256 != 0 || L.d % 64 != 0)
         return hipErrorInvalidValue;
-    const size_t lds = size_t(16) * (L.I + 8) * 2;
     if ((L.I / 256) % 2 == 0)
-        launch_k(stream_down_kq_kernel<2>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_kq_kernel<2>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_down_kq_kernel<1>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_kq_kernel<1>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
 // ============================================================== tile path
 
 namespace kqt {
-constexpr int BM = 128, BN = 128, BK = 64, THREADS = 256;
+constexpr int BM = 128, BN = 128, BK = 64, THREADS = 512;
 constexpr int LDA = BK + 8;                 // bf16 elements per staged A row
 constexpr int LDQ = BK / 2 + 4;             // bytes per staged low-nibble row (36: conflict-spread)
 constexpr int LDH = BK / 4 + 4;             // bytes per staged high-part row (k6)
@@ -398,17 +448,19 @@ TileGeom geom_down_kq_tile(int d, int I)
     return TileGeom{kqt::BM, d / kqt::BN};
 }
 
-// 128 tokens x 128 weight rows per workgroup, K in stages of 64 (two
-// 32-element blocks; a stage never crosses a 256-element super-block).
-// GATEUP: tile columns 0..63 are gate rows nt*64 .. nt*64+63, columns 64..127
-// the matching up rows (k4); wavefront (wm, wn) owns rows wm*64.., gate
-// columns wn*32.. and the matching up columns, so SiLU * up forms in
-// registers.  Per stage each weight row's coefficients are decoded once into
-// LDS as fp32: gate/up {a0, a1, b0, b1} (scale d sc_j and offset dmin m_j of
-// the stage's two blocks), down {s0 .. s3} (d sc_j of its four 16-element
-// sub-blocks).  The k4 offset multiplies the tokens' sums over the block,
-// from one MFMA against ones per token block; the k6 sub-blocks are two
-// MFMAs with the other half's weight lanes zeroed.
+// 128 tokens x 128 weight rows per workgroup of eight wavefronts, K in
+// stages of 64 (two 32-element blocks; a stage never crosses a 256-element
+// super-block).  Wavefront (wm, wn), wm in 0..1, wn in 0..3, owns token rows
+// wm*64 .. wm*64+63 and two 16-column blocks: for GATEUP the gate rows
+// nt*64 + wn*16 .. (tile columns wn*16..) and the matching up rows (tile
+// columns 64 + wn*16..), so SiLU * up forms in registers; for down the tile
+// columns wn*32 .. wn*32+31.  Per stage each weight row's coefficients are
+// decoded once into LDS as fp32: gate/up {a0, a1, b0', b1'} (scale d sc_j and
+// folded min dmin m_j + 128 d sc_j of the stage's two blocks), down
+// {s0 .. s3} (d sc_j of its four 16-element sub-blocks).  The k4 min
+// multiplies the tokens' sums over the block, from one MFMA against ones per
+// token block; the k6 sub-blocks are two MFMAs with the other half's weight
+// lanes zeroed.
 template <bool GATEUP>
 __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L)
 {
@@ -429,18 +481,18 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
     const int m0 = (local / ntn) * BM;
     const int nt = local % ntn;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave >> 2, wn = wave & 3;
 
     const uint16_t *abase = reinterpret_cast<const uint16_t *>(GATEUP ? L.x : (sh ? L.act_s : L.act));
     const int32_t *perm = (GATEUP && !sh) ? L.perm : nullptr;
     const uint8_t *obj = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mbytes = k4_bytes(I, d);
 
-    // A: 128 rows x 64 bf16 per stage = 8 chunks of 16 B per row; 4 per thread
-    uint32_t aoff[4];
+    // A: 128 rows x 64 bf16 per stage = 8 chunks of 16 B per row; 2 per thread
+    uint32_t aoff[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r = (tid >> 3) + 32 * i;
+    for (int i = 0; i < 2; ++i) {
+        const int r = (tid >> 3) + 64 * i;
         int64_t src = 0;
         if (m0 + r < it.nrows)
             src = perm ? int64_t(perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
@@ -456,10 +508,12 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
             return obj + (c < 64 ? 0u : mbytes);
         return obj + 2 * mbytes;
     };
-    // low nibbles: 128 rows x 32 B per stage, 2 chunks of 16 B per row, 1 per thread
-    const int brow_l = tid >> 1, bchunk = tid & 1;
+    // threads 0..255: low nibbles, 128 rows x 32 B per stage, 2 chunks of 16 B per row;
+    // threads 256..383: tile column tid - 256's header (gate/up) or high parts (down);
+    // threads 384..511: tile column tid - 384's sub-block scales (down)
+    const int role = tid >> 7;                      // 0, 1: nibbles; 2: header / high parts; 3: scales
+    const int brow_l = (tid & 255) >> 1, bchunk = tid & 1;
     const uint8_t *qrow = matrix_of(brow_l) + int64_t(weight_row(brow_l)) * (K / 2) + bchunk * 16;
-    // coefficients (and the k6 high parts): thread tid < 128 takes tile column tid
     const int cc = tid & 127;
     const uint8_t *cmat = matrix_of(cc);
     const int64_t crow = weight_row(cc);
@@ -467,67 +521,71 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
     const u32x4 *hdr = reinterpret_cast<const u32x4 *>(cmat + uint32_t(rows_m) * uint32_t(K / 2)) + crow * (K / 256);
     const K6Planes P = k6_planes(cmat, rows_m, K);
 
-    u32x4 ra[4], rq, rh, rc;
+    // the 16-byte word of roles 0..2 (nibbles, header or high parts) goes through one register
+    // quadruple, loaded from a per-role address
+    u32x4 ra[2], rw;
     uint32_t rsc = 0;
     uint16_t rd = 0;
     auto load = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 2; ++i)
             ra[i] = *reinterpret_cast<const u32x4 *>(abase + (aoff[i] + uint32_t(k0)));
-        rq = *reinterpret_cast<const u32x4 *>(qrow + k0 / 2);
-        if (tid < 128) {
-            if (GATEUP) {
-                rc = hdr[k0 / 256];
-            } else {
-                rh = *reinterpret_cast<const u32x4 *>(P.qh + crow * (K / 4) + k0 / 4);
-                rsc = *reinterpret_cast<const uint32_t *>(P.sc + crow * (K / 16) + k0 / 16);
-                rd = P.d[crow * (K / 256) + k0 / 256];
-            }
+        if (role < 3) {
+            const u32x4 *src = role < 2 ? reinterpret_cast<const u32x4 *>(qrow + k0 / 2)
+                               : GATEUP ? hdr + k0 / 256
+                                        : reinterpret_cast<const u32x4 *>(P.qh + crow * (K / 4) + k0 / 4);
+            rw = *src;
+        } else if (!GATEUP) {
+            rsc = *reinterpret_cast<const uint32_t *>(P.sc + crow * (K / 16) + k0 / 16);
+            rd = P.d[crow * (K / 256) + k0 / 256];
         }
     };
     auto store = [&](int buf, int k0) {
         uint8_t *st = lds8 + buf * STAGE;
         uint16_t *a = reinterpret_cast<uint16_t *>(st);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            *reinterpret_cast<u32x4 *>(a + ((tid >> 3) + 32 * i) * LDA + (tid & 7) * 8) = ra[i];
-        uint32_t *q = reinterpret_cast<uint32_t *>(st + A_BYTES + brow_l * LDQ + bchunk * 16);
+        for (int i = 0; i < 2; ++i)
+            *reinterpret_cast<u32x4 *>(a + ((tid >> 3) + 64 * i) * LDA + (tid & 7) * 8) = ra[i];
+        float *cfp = reinterpret_cast<float *>(st + A_BYTES + Q_BYTES + H_BYTES + cc * 16);
+        if (role < 2) {
+            uint32_t *q = reinterpret_cast<uint32_t *>(st + A_BYTES + brow_l * LDQ + bchunk * 16);
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-            q[w] = rq[w];
-        if (tid < 128) {
-            f32x4 cf;
+            for (int w = 0; w < 4; ++w)
+                q[w] = rw[w];
+        } else if (role == 2) {
             if (GATEUP) {
                 const int j0 = (k0 & 255) >> 5;
                 float a0, b0, a1, b1;
-                k4_coef(rc, j0, a0, b0);
-                k4_coef(rc, j0 + 1, a1, b1);
-                cf = f32x4{a0, a1, b0, b1};
+                k4_coef128(rw, j0, a0, b0);
+                k4_coef128(rw, j0 + 1, a1, b1);
+                *reinterpret_cast<f32x4 *>(cfp) = f32x4{a0, a1, b0, b1};
             } else {
                 uint32_t *h = reinterpret_cast<uint32_t *>(st + A_BYTES + Q_BYTES + cc * LDH);
 #pragma unroll
                 for (int w = 0; w < 4; ++w)
-                    h[w] = rh[w];
-                const float dv = h2f(rd);
-#pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    cf[s] = dv * float(int(int8_t((rsc >> (8 * s)) & 0xFFu)));
+                    h[w] = rw[w];
             }
-            *reinterpret_cast<f32x4 *>(st + A_BYTES + Q_BYTES + H_BYTES + cc * 16) = cf;
+        } else if (!GATEUP) {
+            const float dv = h2f(rd);
+            f32x4 cf;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                cf[k] = dv * float(int(int8_t((rsc >> (8 * k)) & 0xFFu)));
+            *reinterpret_cast<f32x4 *>(cfp) = cf;
         }
     };
 
-    f32x4 acc[4][4];
+    f32x4 acc[4][2];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < 2; ++b)
             acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int r16 = lane & 15, g = lane >> 4;
     auto col_of = [&](int nb) -> int {              // tile column block of this wavefront
         if (GATEUP)
-            return nb < 2 ? wn * 32 + nb * 16 : 64 + wn * 32 + (nb - 2) * 16;
-        return wn * 64 + nb * 16;
+            return nb * 64 + wn * 16;
+        return wn * 32 + nb * 16;
     };
     const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{BF16_ONE2, BF16_ONE2, BF16_ONE2, BF16_ONE2});
     const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
@@ -550,9 +608,9 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
                 for (int mb = 0; mb < 4; ++mb)
                     sx[mb] = mfma16(af[mb], ones, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
+                for (int nb = 0; nb < 2; ++nb) {
                     const int c = col_of(nb) + r16;                // B fragment: weight row c
-                    const bf16x8 bq = unpack_u4(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4));
+                    const bf16x8 bq = unpack_u4_128(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4));
                     const float sa = cf[c * 4 + kb], sb = cf[c * 4 + 2 + kb];   // output column = c
 #pragma unroll
                     for (int mb = 0; mb < 4; ++mb) {
@@ -563,11 +621,10 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
                             acc[mb][nb][rr] = fmaf(-sb, sx[mb][rr], acc[mb][nb][rr]);
                         }
                     }
-                    __builtin_amdgcn_sched_barrier(0);   // bounds the partial sums in flight
                 }
             } else {
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
+                for (int nb = 0; nb < 2; ++nb) {
                     const int c = col_of(nb) + r16;
                     const bf16x8 w = unpack_k6(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4),
                                                *reinterpret_cast<const uint16_t *>(h + c * LDH + kb * 8 + g * 2));
@@ -583,7 +640,6 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
                             acc[mb][nb][rr] = fmaf(s1, p1[rr], acc[mb][nb][rr]);
                         }
                     }
-                    __builtin_amdgcn_sched_barrier(0);   // bounds the partial sums in flight
                 }
             }
         }
@@ -615,16 +671,13 @@ __global__ void __launch_bounds__(kqt::THREADS, 1) tile_kq_kernel(ExpertLaunch L
             const int64_t orow = int64_t(it.row0) + m0 + row;
             if (GATEUP) {
                 uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + orow * I;
-#pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
-                    act[nt * 64 + wn * 32 + nb * 16 + r16] =
-                        f32_to_bf16(silu(acc[mb][nb][rr]) * acc[mb][nb + 2][rr]);
+                act[nt * 64 + wn * 16 + r16] = f32_to_bf16(silu(acc[mb][0][rr]) * acc[mb][1][rr]);
             } else {
                 uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + orow * d;
                 const float w = sh ? 1.0f : L.row_weight[orow];
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb)
-                    y[nt * BN + wn * 64 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * w);
+                for (int nb = 0; nb < 2; ++nb)
+                    y[nt * BN + wn * 32 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * w);
             }
         }
 }
@@ -651,12 +704,7 @@ hipError_t launch_down_kq_tile(const ExpertLaunch &L, hipStream_t s)
 
 hipError_t init_kq_attributes()
 {
-    const void *ks[] = {reinterpret_cast<const void *>(&stream_gateup_kq_kernel<8>),
-                        reinterpret_cast<const void *>(&stream_gateup_kq_kernel<4>),
-                        reinterpret_cast<const void *>(&stream_gateup_kq_kernel<2>),
-                        reinterpret_cast<const void *>(&stream_down_kq_kernel<2>),
-                        reinterpret_cast<const void *>(&stream_down_kq_kernel<1>),
-                        reinterpret_cast<const void *>(&tile_kq_kernel<true>),
+    const void *ks[] = {reinterpret_cast<const void *>(&tile_kq_kernel<true>),
                         reinterpret_cast<const void *>(&tile_kq_kernel<false>)};
     for (const void *k : ks) {
         const hipError_t e = allow_large_lds(k);
