@@ -147,42 +147,6 @@ int tiles_down_kq_stream(int nrows, int d, int I)
     return d / (kqs::WAVES * kqs::ROWS);
 }
 
-// Stream-path weight staging.  A wavefront's weights are 16 rows of W bytes
-// each (its share of one row); per-lane 4-byte loads of the MFMA layout would
-// touch 16 rows per load instruction, so the wavefront instead reads them with
-// 16-byte loads that run along the rows (each instruction covers 64 / (W / 16)
-// rows), writes them to its own LDS region, and reads the MFMA words back.
-// Rows are padded by 16 bytes there, which puts the 64 lanes' word reads on
-// distinct banks.  The region is the wavefront's alone: it needs no barrier
-// (a wavefront's LDS operations complete in order).
-template <int W>
-struct WaveRows {
-    static constexpr int RS = W + 16;                  // LDS bytes per row
-    static constexpr int CPR = W / 16;                 // 16-byte chunks per row
-    static constexpr int NL = (16 * CPR + 63) / 64;    // load instructions
-    u32x4 v[NL];
-
-    // rows row0 .. row0 + 15 of stride `stride` bytes, W bytes from `src` on
-    __device__ __forceinline__ void load(const uint8_t *src, int64_t stride, int lane)
-    {
-#pragma unroll
-        for (int k = 0; k < NL; ++k) {
-            const int ci = 64 * k + lane, row = ci / CPR, ch = ci % CPR;
-            if (row < 16)
-                v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + row * stride + 16 * ch));
-        }
-    }
-    __device__ __forceinline__ void store(uint8_t *lds, int lane) const
-    {
-#pragma unroll
-        for (int k = 0; k < NL; ++k) {
-            const int ci = 64 * k + lane, row = ci / CPR, ch = ci % CPR;
-            if (row < 16)
-                *reinterpret_cast<u32x4 *>(lds + row * RS + 16 * ch) = v[k];
-        }
-    }
-};
-
 // Gate/up, k4 stream path: a workgroup owns 16 rows of Wg and of Wu; its four
 // wavefronts take the quarters of d and add their partial sums in wavefront
 // order.  Tokens are the A operand and weights the B operand, so lane

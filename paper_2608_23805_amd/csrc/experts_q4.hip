@@ -7,9 +7,9 @@
 // block, so it returns the block's partial dot product (C = 0) and the scale
 // is applied in fp32: acc += scale * partial.
 //
-//  * stream path (<= 16 tokens per expert): weights as the A operand read
-//    straight from memory, tokens as the B operand from LDS (as the bf16
-//    stream path).
+//  * stream path (<= 16 tokens per expert): tokens as the A operand and
+//    weights as the B operand, tokens read straight from memory and the
+//    nibbles through row-contiguous loads rearranged in LDS (WaveRows).
 //  * tile path: 128 tokens x 128 weight rows per workgroup, packed nibbles and
 //    scales staged in LDS (a quarter of the bf16 staging traffic), unpacked
 //    to bf16 while the MFMA fragments are built.
@@ -76,8 +76,9 @@ __device__ __forceinline__ bool q4_tile(const ExpertLaunch &L, int per_item, int
     return true;
 }
 
-// CH consecutive fp16 block scales of one row, in one vector load (the row's
-// scales start 16-byte aligned and CH divides the blocks of a quarter of d).
+// CH consecutive fp16 block scales of one row, in one vector load (the
+// row's scales start 16-byte aligned and CH divides the blocks of a quarter
+// of d, or of I).
 template <int CH>
 __device__ __forceinline__ void load_scales(uint32_t (&w)[CH / 2], const uint16_t *p)
 {
@@ -110,22 +111,26 @@ __device__ __forceinline__ float scale_at(const uint32_t *w, int b)
 // Gate/up, 4-bit stream path: a workgroup owns 16 rows of Wg and of Wu; its
 // four wavefronts take the four quarters of d and add their fp32 partial sums
 // in wavefront order before SiLU(g) * u, so an item is I / 16 workgroups.
-// Within a quarter, blocks go in chunks of CH: every nibble word and block
-// scale of a chunk, for both matrices, is issued before its first MFMA.
-// Lane (row r = lane % 16, group g = lane / 16) holds elements 8g .. 8g + 7 of
-// each block of row r; the output lane (rows 4g .. 4g + 3, token lane % 16)
-// applies those rows' block scales to each block's exact partial sum.
+// Tokens are the A operand and weights the B operand: lane (r = lane % 16,
+// g = lane / 16) holds elements 8g .. 8g + 7 of each block of token r and of
+// weight row i0 + r, and its outputs are tokens 4g .. 4g + 3 of that weight
+// row, so each lane applies one row's block scales.  Token fragments come
+// straight from global memory (lanes past the item's rows repeat its last
+// row and are not stored); the nibbles go through WaveRows (row-contiguous
+// 16-byte loads, rearranged in the wavefront's own LDS region).  Blocks go
+// in chunks of CH, each chunk's loads issued before its first MFMA.
 template <int CH>
 __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    using Rows = WaveRows<16 * CH>;
+    __shared__ __attribute__((aligned(16))) uint8_t wst[q4s::WAVES][2][16 * Rows::RS];
     __shared__ f32x4 red[3][2][64];
     int t;
     WorkItem it;
     if (!q4_tile(L, L.I / q4s::ROWS, t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    const int n = it.nrows, d = L.d, I = L.I, ldk = d + 8, nblk = d / 32, nq = nblk / q4s::WAVES;
+    const int n = it.nrows, d = L.d, I = L.I, nblk = d / 32, nq = nblk / q4s::WAVES;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int i0 = (t - it.tile0) * q4s::ROWS;
@@ -133,50 +138,49 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
     const int bq = wave * nq;                          // this wavefront's first block
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mb = q4_matrix_bytes(I, d);
-    const uint32_t *qp[2];
+    const uint8_t *qrows[2];
     const uint16_t *sp[2];
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
         const uint8_t *mat = base + m * mb;
-        qp[m] = reinterpret_cast<const uint32_t *>(mat + int64_t(i0 + r) * (d / 2)) + 4 * bq + g;
-        sp[m] = reinterpret_cast<const uint16_t *>(mat + int64_t(I) * (d / 2)) + int64_t(i0 + 4 * g) * nblk + bq;
+        qrows[m] = mat + int64_t(i0) * (d / 2) + 16 * bq;
+        sp[m] = reinterpret_cast<const uint16_t *>(mat + int64_t(I) * (d / 2)) + int64_t(i0 + r) * nblk + bq;
     }
-    uint32_t q[2][CH], sc[2][4][CH / 2];
+    const int tr = min(r, n - 1);
+    const int64_t xrow = sh ? int64_t(it.row0 + tr) : int64_t(L.perm[it.row0 + tr]);
+    const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + 8 * g + 32 * bq;
+    Rows wr[2];
+    u32x4 xv[CH];
+    uint32_t sc[2][CH / 2];
     auto issue = [&](int c0) {
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int m = 0; m < 2; ++m)
+            wr[m].load(qrows[m] + 16 * c0, d / 2, lane);
 #pragma unroll
-            for (int u = 0; u < CH; ++u)
-                q[m][u] = __builtin_nontemporal_load(qp[m] + 4 * (c0 + u));
+        for (int u = 0; u < CH; ++u)
+            xv[u] = *reinterpret_cast<const u32x4 *>(xp + 32 * (c0 + u));
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                load_scales<CH>(sc[m][rr], sp[m] + rr * nblk + c0);
-        }
+        for (int m = 0; m < 2; ++m)
+            load_scales<CH>(sc[m], sp[m] + c0);
     };
-    issue(0);                                          // the first chunk goes out before the token rows
-    {
-        const uint16_t *xsrc = reinterpret_cast<const uint16_t *>(L.x);
-        const int32_t *xperm = sh ? nullptr : L.perm;
-        StageRows<4> sr;                               // one pass for d <= 2048
-        sr.load(xsrc, xperm, it.row0, n, d, 0);
-        sr.store(xs, n, d, 0);
-        sr.rest(xsrc, xperm, it.row0, n, d, xs);
-    }
-    __syncthreads();
-    const uint16_t *xrow = xs + r * ldk + 8 * g + 32 * bq;   // rows past n hold stale data: not stored
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
     for (int c0 = 0; c0 < nq; c0 += CH) {
-        if (c0 > 0)
-            issue(c0);
+        issue(c0);
+        wr[0].store(wst[wave][0], lane);
+        wr[1].store(wst[wave][1], lane);
+        const uint8_t *q0 = wst[wave][0] + r * Rows::RS + 4 * g, *q1 = wst[wave][1] + r * Rows::RS + 4 * g;
 #pragma unroll
         for (int u = 0; u < CH; ++u) {
-            const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4 *>(xrow + 32 * (c0 + u)));
-            const f32x4 pg = mfma16(unpack_q4(q[0][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
-            const f32x4 pu = mfma16(unpack_q4(q[1][u]), xb, f32x4{0.f, 0.f, 0.f, 0.f});
+            const bf16x8 xb = as_bf16x8(xv[u]);
+            const f32x4 pg = mfma16(xb, unpack_q4(*reinterpret_cast<const uint32_t *>(q0 + 16 * u)),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 pu = mfma16(xb, unpack_q4(*reinterpret_cast<const uint32_t *>(q1 + 16 * u)),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
+            const float s_g = scale_at(sc[0], u), s_u = scale_at(sc[1], u);
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                ag[rr] = fmaf(scale_at(sc[0][rr], u), pg[rr], ag[rr]);
-                au[rr] = fmaf(scale_at(sc[1][rr], u), pu[rr], au[rr]);
+            for (int k = 0; k < 4; ++k) {
+                ag[k] = fmaf(s_g, pg[k], ag[k]);
+                au[k] = fmaf(s_u, pu[k], au[k]);
             }
         }
     }
@@ -188,80 +192,73 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
     __syncthreads();
     if (wave != 0)
         return;
+    uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0) * I + i0 + r;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-        ag[rr] = ((ag[rr] + red[0][0][lane][rr]) + red[1][0][lane][rr]) + red[2][0][lane][rr];
-        au[rr] = ((au[rr] + red[0][1][lane][rr]) + red[1][1][lane][rr]) + red[2][1][lane][rr];
-    }
-    const int j = lane & 15;
-    if (j < n) {
-        uint2 v;
-        v.x = pack_bf16x2(silu(ag[0]) * au[0], silu(ag[1]) * au[1]);
-        v.y = pack_bf16x2(silu(ag[2]) * au[2], silu(ag[3]) * au[3]);
-        uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0 + j) * I + i0 + 4 * g;
-        *reinterpret_cast<uint2 *>(act) = v;
+    for (int k = 0; k < 4; ++k) {
+        const float gv = ((ag[k] + red[0][0][lane][k]) + red[1][0][lane][k]) + red[2][0][lane][k];
+        const float uv = ((au[k] + red[0][1][lane][k]) + red[1][1][lane][k]) + red[2][1][lane][k];
+        if (4 * g + k < n)
+            act[int64_t(4 * g + k) * I] = f32_to_bf16(silu(gv) * uv);
     }
 }
 
 // Down, 4-bit stream path: a workgroup owns 64 output columns (16 per
-// wavefront) over all of I, in chunks of CH blocks; the first chunk's nibble
-// words and block scales are issued before the act rows are staged.
+// wavefront) over all of I, in chunks of CH blocks whose nibbles (through
+// WaveRows), act fragments and this lane's block scales are issued together.
+// Act rows are the A operand, read straight from global memory (lanes past
+// the item's rows repeat its last row), and weights the B operand (outputs:
+// tokens 4g .. 4g + 3 of column c0 + r).
 template <int CH>
 __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
 {
-    extern __shared__ __attribute__((aligned(16))) uint16_t as[];
+    using Rows = WaveRows<16 * CH>;
+    __shared__ __attribute__((aligned(16))) uint8_t wst[q4s::WAVES][16 * Rows::RS];
     int t;
     WorkItem it;
     if (!q4_tile(L, L.d / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    const int n = it.nrows, d = L.d, I = L.I, ldk = I + 8, nblk = I / 32;
+    const int n = it.nrows, d = L.d, I = L.I, nblk = I / 32;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c0 = ((t - it.tile0) * q4s::WAVES + wave) * q4s::ROWS;
     const int r = lane & 15, g = lane >> 4;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint8_t *wd = base + 2 * q4_matrix_bytes(I, d);
-    const uint32_t *qp = reinterpret_cast<const uint32_t *>(wd + int64_t(c0 + r) * (I / 2)) + g;
-    const uint16_t *sp = reinterpret_cast<const uint16_t *>(wd + int64_t(d) * (I / 2)) + int64_t(c0 + 4 * g) * nblk;
-    uint32_t q[CH], sc[4][CH / 2];
-    auto issue = [&](int b0) {
-#pragma unroll
-        for (int u = 0; u < CH; ++u)
-            q[u] = __builtin_nontemporal_load(qp + 4 * (b0 + u));
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-            load_scales<CH>(sc[rr], sp + rr * nblk + b0);
-    };
-    issue(0);
-    {
-        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
-        StageRows<1> sr;                               // one pass for I <= 512
-        sr.load(asrc, nullptr, it.row0, n, I, 0);
-        sr.store(as, n, I, 0);
-        sr.rest(asrc, nullptr, it.row0, n, I, as);
-    }
-    __syncthreads();
-    const uint16_t *arow = as + r * ldk + 8 * g;       // rows past n hold stale data: not stored
+    const uint8_t *qrows = wd + int64_t(c0) * (I / 2);
+    const uint16_t *sp = reinterpret_cast<const uint16_t *>(wd + int64_t(d) * (I / 2)) + int64_t(c0 + r) * nblk;
+    const uint16_t *ap = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act) +
+                         int64_t(it.row0 + min(r, n - 1)) * I + 8 * g;
+    Rows wr;
+    u32x4 av[CH];
+    uint32_t sc[CH / 2];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int b0 = 0; b0 < nblk; b0 += CH) {
-        if (b0 > 0)
-            issue(b0);
+        wr.load(qrows + 16 * b0, I / 2, lane);
+#pragma unroll
+        for (int u = 0; u < CH; ++u)
+            av[u] = *reinterpret_cast<const u32x4 *>(ap + 32 * (b0 + u));
+        load_scales<CH>(sc, sp + b0);
+        wr.store(wst[wave], lane);
+        const uint8_t *q = wst[wave] + r * Rows::RS + 4 * g;
 #pragma unroll
         for (int u = 0; u < CH; ++u) {
-            const bf16x8 ab = as_bf16x8(*reinterpret_cast<const u32x4 *>(arow + 32 * (b0 + u)));
-            const f32x4 part = mfma16(unpack_q4(q[u]), ab, f32x4{0.f, 0.f, 0.f, 0.f});
+            const f32x4 part = mfma16(as_bf16x8(av[u]), unpack_q4(*reinterpret_cast<const uint32_t *>(q + 16 * u)),
+                                      f32x4{0.f, 0.f, 0.f, 0.f});
+            const float sv = scale_at(sc, u);
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                acc[rr] = fmaf(scale_at(sc[rr], u), part[rr], acc[rr]);
+            for (int k = 0; k < 4; ++k)
+                acc[k] = fmaf(sv, part[k], acc[k]);
         }
     }
-    const int j = lane & 15;
-    if (j < n) {
-        const int64_t row = it.row0 + j;
-        const float w = sh ? 1.0f : L.row_weight[row];
-        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(sh ? L.ys : L.y) + row * d + c0 + 4 * g) =
-            make_uint2(pack_bf16x2(acc[0] * w, acc[1] * w), pack_bf16x2(acc[2] * w, acc[3] * w));
+    uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + int64_t(it.row0) * d + c0 + r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int tok = 4 * g + k;
+        if (tok < n) {
+            const float w = sh ? 1.0f : L.row_weight[it.row0 + tok];
+            y[int64_t(tok) * d] = f32_to_bf16(acc[k] * w);
+        }
     }
 }
 
@@ -271,15 +268,14 @@ hipError_t launch_gateup_q4_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     // chunk: the largest of 16, 8, 4, 2 blocks dividing a quarter of d (d % 256 == 0)
     const int nq = L.d / 128;
-    const size_t lds = size_t(16) * (L.d + 8) * 2;
     if (nq % 16 == 0)
-        launch_k(stream_gateup_q4_kernel<16>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_q4_kernel<16>, L.n_tiles, 256, 0, s, L);
     else if (nq % 8 == 0)
-        launch_k(stream_gateup_q4_kernel<8>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_q4_kernel<8>, L.n_tiles, 256, 0, s, L);
     else if (nq % 4 == 0)
-        launch_k(stream_gateup_q4_kernel<4>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_q4_kernel<4>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_gateup_q4_kernel<2>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_gateup_q4_kernel<2>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -289,13 +285,12 @@ hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     // chunk: the largest of 16, 8, 4 blocks dividing I / 32 (I % 128 == 0)
     const int nblk = L.I / 32;
-    const size_t lds = size_t(16) * (L.I + 8) * 2;
     if (nblk % 16 == 0)
-        launch_k(stream_down_q4_kernel<16>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_q4_kernel<16>, L.n_tiles, 256, 0, s, L);
     else if (nblk % 8 == 0)
-        launch_k(stream_down_q4_kernel<8>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_q4_kernel<8>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_down_q4_kernel<4>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_q4_kernel<4>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
@@ -516,21 +511,7 @@ hipError_t launch_down_q4_tile(const ExpertLaunch &L, hipStream_t s)
 
 hipError_t init_q4_attributes()
 {
-    hipError_t e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<16>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<8>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<4>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_gateup_q4_kernel<2>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<16>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<8>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&stream_down_q4_kernel<4>));
-    if (e == hipSuccess)
-        e = allow_large_lds(reinterpret_cast<const void *>(&tile_q4_kernel<true>));
+    hipError_t e = allow_large_lds(reinterpret_cast<const void *>(&tile_q4_kernel<true>));
     if (e == hipSuccess)
         e = allow_large_lds(reinterpret_cast<const void *>(&tile_q4_kernel<false>));
     return e;
