@@ -297,8 +297,9 @@ __device__ __forceinline__ int xcd_swizzle(int b, int n)
 // 16-byte loads that run along the rows (each instruction covers 64 / (W / 16)
 // rows), writes them to its own LDS region, and reads the MFMA words back.
 // Rows are padded by 16 bytes there, which puts the 64 lanes' word reads on
-// distinct banks.  The region is the wavefront's alone: it needs no barrier
-// (a wavefront's LDS operations complete in order).
+// distinct banks.  The region is the wavefront's alone, so no workgroup
+// barrier is needed; store() waits for the wavefront's earlier LDS reads
+// before it overwrites the region and for its writes before it returns.
 template <int W>
 struct WaveRows {
     static constexpr int RS = W + 16;                  // LDS bytes per row
@@ -316,14 +317,21 @@ struct WaveRows {
                 v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + row * stride + 16 * ch));
         }
     }
+    // write the rows to the wavefront's region and wait until they are there
+    // (lgkmcnt(0)); the compiler may not move the caller's reads above it
     __device__ __forceinline__ void store(uint8_t *lds, int lane) const
     {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xC07F);           // earlier reads of the region have returned
 #pragma unroll
         for (int k = 0; k < NL; ++k) {
             const int ci = 64 * k + lane, row = ci / CPR, ch = ci % CPR;
             if (row < 16)
                 *reinterpret_cast<u32x4 *>(lds + row * RS + 16 * ch) = v[k];
         }
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("" ::: "memory");
     }
 };
 

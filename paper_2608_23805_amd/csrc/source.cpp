@@ -290,6 +290,12 @@ void SourceService::inject(uint64_t tag, int extent, SourceFault f)
 void SourceService::release_holds()
 {
     std::lock_guard<std::mutex> lk(mu_);
+    // held reads still queued are let go too: a worker checks the hold under
+    // this lock, so every held read is either waiting (woken by the epoch) or
+    // not yet taken (its hold cleared here)
+    for (Read &r : queue_)
+        if (r.fault == SourceFault::Hold)
+            r.fault = SourceFault::None;
     hold_epoch_++;
     hold_cv_.notify_all();
 }

@@ -124,7 +124,8 @@ public:
     void use_bounce_buffers() { bounce_.store(true, std::memory_order_relaxed); }
 
     // Test hook: the next read of extent `extent` of the request tagged `tag`
-    // is cut short, fails with EIO, or is held until release_holds().
+    // is cut short, fails with EIO, or is held until release_holds(), which
+    // lets go every submitted held read, running or still queued.
     void inject(uint64_t tag, int extent, SourceFault f);
     void release_holds();
 

@@ -177,8 +177,23 @@ static void test_hold_and_drain()
         S.release_holds();
         auto d = wait_all(S, 2);
         CHECK(d.size() == 2);
+        // a release that comes before the worker reaches a held read lets it go too:
+        // with one worker busy on held read 4, read 5 (also held) is still queued
+        S.set_free(0);
+        S.set_free(1);
+        S.inject(4, 0, SourceFault::Hold);
+        S.inject(5, 0, SourceFault::Hold);
+        CHECK(S.submit(0, ext, 1, 4, 0, 1));
+        CHECK(S.submit(1, ext, 1, 5, 0, 1));
+        CHECK(S.collect(100, always).empty());
+        const auto tr = std::chrono::steady_clock::now();
+        S.release_holds();
+        d = wait_all(S, 2);
+        CHECK(d.size() == 2);
+        CHECK(std::chrono::steady_clock::now() - tr < std::chrono::seconds(10));
         // a held read at destruction: the destructor lets it go and drains
         S.set_free(0);
+        S.set_free(1);
         S.inject(3, 0, SourceFault::Hold);
         CHECK(S.submit(0, ext, 1, 3, 0, 1));
         const auto t0 = std::chrono::steady_clock::now();
