@@ -257,16 +257,17 @@ __global__ void __launch_bounds__(256, 3) stream_gateup_kernel(ExpertLaunch L)
 // Down, stream path: a workgroup owns 64 output columns (16 per wavefront)
 // over all of I, in chunks of NB batches of 4 K steps (2 slabs of Wd rows,
 // loaded in whole lines and rearranged through the wavefront's LDS as in the
-// gate/up kernel), each chunk fully unrolled.  The expert's act rows (the B
-// operand, shared by the four wavefronts) are staged once in LDS; the first
-// two weight batches are issued before them.
+// gate/up kernel), each chunk fully unrolled.  The lanes of token j (B
+// operand) read row j of the item's act rows straight from memory with each
+// weight batch (the rows are contiguous and few; lanes past the item's rows
+// read its last row, whose outputs are never stored), so no workgroup
+// barrier or LDS staging comes before the first MFMA.
 template <int NB>
 __global__ void __launch_bounds__(256, 4) stream_down_kernel(ExpertLaunch L)
 {
     constexpr int U = 4, SL = U / 2;
-    extern __shared__ __attribute__((aligned(16))) uint16_t as[];   // [16][I + 8]
     __shared__ __attribute__((aligned(16))) uint8_t tr[stream::WAVES][SL * slab::BYTES];
-    const int d = L.d, I = L.I, ldk = I + 8;
+    const int d = L.d, I = L.I;
     const StreamTile st = stream_tile(L, d / (stream::WAVES * stream::ROWS));
     if (!st.valid)
         return;
@@ -282,45 +283,33 @@ __global__ void __launch_bounds__(256, 4) stream_down_kernel(ExpertLaunch L)
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint16_t *w0 = reinterpret_cast<const uint16_t *>(base) + int64_t(2) * I * d + int64_t(c0) * I;
     const uint16_t *gp0 = w0 + slab::src(lane, 0, I), *gp1 = w0 + slab::src(lane, 1, I);
+    const uint16_t *ap = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act) +
+                         int64_t(it.row0 + min(j, n - 1)) * I + kg;
     const bool live = j < n;
     uint8_t *t = tr[wave];
-    auto load_w = [&](u32x4(&dst)[SL][2], int k0) {
+    auto load_w = [&](u32x4(&dst)[SL][2], u32x4(&adst)[U], int k0) {
 #pragma unroll
         for (int s = 0; s < SL; ++s) {
             dst[s][0] = load_stream16(gp0 + k0 + 64 * s);
             dst[s][1] = load_stream16(gp1 + k0 + 64 * s);
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            adst[u] = *reinterpret_cast<const u32x4 *>(ap + k0 + 32 * u);
     };
-    u32x4 w[2][SL][2];
-    asm volatile("" ::: "memory");
-    load_w(w[0], 0);
-    if (NB > 1)
-        load_w(w[1], 32 * U);
-    asm volatile("" ::: "memory");
-    // the expert's act rows are contiguous
-    {
-        const uint16_t *asrc = reinterpret_cast<const uint16_t *>(sh ? L.act_s : L.act);
-        StageRows<1> sr;                              // one pass for I <= 512
-        sr.load(asrc, nullptr, it.row0, n, I, 0);
-        sr.store(as, n, I, 0);
-        sr.rest(asrc, nullptr, it.row0, n, I, as);
-    }
-    __syncthreads();
-    const uint16_t *ar = as + j * ldk + kg;          // rows past n hold stale data: their outputs are not stored
-
+    u32x4 w[2][SL][2], av[2][U];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     const int nchunk = I / (32 * U * NB);
     for (int c = 0; c < nchunk; ++c) {
         const int kc = c * 32 * U * NB;
-        if (c > 0) {
-            load_w(w[0], kc);
-            if (NB > 1)
-                load_w(w[1], kc + 32 * U);
-        }
+        asm volatile("" ::: "memory");
+        load_w(w[0], av[0], kc);
+        if (NB > 1)
+            load_w(w[1], av[1], kc + 32 * U);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             if (b >= 1 && b + 1 < NB)                 // batches 0 and 1 went out with the chunk
-                load_w(w[(b + 1) & 1], kc + (b + 1) * 32 * U);
+                load_w(w[(b + 1) & 1], av[(b + 1) & 1], kc + (b + 1) * 32 * U);
 #pragma unroll
             for (int s = 0; s < SL; ++s)
 #pragma unroll
@@ -330,8 +319,7 @@ __global__ void __launch_bounds__(256, 4) stream_down_kernel(ExpertLaunch L)
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const u32x4 fw = *reinterpret_cast<const u32x4 *>(t + (u >> 1) * slab::BYTES + slab::frag(lane, u & 1));
-                const uint4 av = *reinterpret_cast<const uint4 *>(ar + kc + b * 32 * U + 32 * u);
-                acc = mfma16(as_bf16x8(fw), as_bf16x8(av), acc);
+                acc = mfma16(as_bf16x8(fw), as_bf16x8(av[b & 1][u]), acc);
             }
             lds_wait();                               // the next batch overwrites this wavefront's slabs
         }
@@ -368,13 +356,12 @@ hipError_t launch_down_stream(const ExpertLaunch &L, hipStream_t s)
     if (L.n_tiles == 0)
         return hipSuccess;
     // chunks of NB batches of 128 columns must divide I (I % 128 == 0)
-    const size_t lds = size_t(stream::MAXN) * (L.I + 8) * sizeof(uint16_t);
     if (L.I % 512 == 0)
-        launch_k(stream_down_kernel<4>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_kernel<4>, L.n_tiles, 256, 0, s, L);
     else if (L.I % 256 == 0)
-        launch_k(stream_down_kernel<2>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_kernel<2>, L.n_tiles, 256, 0, s, L);
     else
-        launch_k(stream_down_kernel<1>, L.n_tiles, 256, lds, s, L);
+        launch_k(stream_down_kernel<1>, L.n_tiles, 256, 0, s, L);
     return hipGetLastError();
 }
 
