@@ -582,12 +582,25 @@ msi_status enqueue_fills(msi_plan *p, uint32_t layer, const std::vector<FillReco
             pub.value[pub.n++] = f->gen;
         }
         HIP_OK(launch_set_gens(p->gen_dev, inval, side));
-        for (size_t i = b; i < e; ++i) {
+        // consecutive fills whose sources follow each other in one window and
+        // whose slots follow each other in the pool (objects exactly one
+        // stride long) go out as one copy: each copy costs the copy engine a
+        // fixed setup time, about a sixth of a 6 MiB object's transfer
+        for (size_t i = b; i < e;) {
             const FillRecord *f = &fills[i];
             const uint32_t gs = c.global_slot(layer, f->slot);
             uint8_t *dst = static_cast<uint8_t *>(p->desc.slot_pool) + uint64_t(gs) * p->desc.slot_stride;
             const uint8_t *src = static_cast<const uint8_t *>(p->windows[f->window]) + f->offset;
-            HIP_OK(hipMemcpyAsync(dst, src, f->nbytes, hipMemcpyHostToDevice, side));
+            uint64_t bytes = f->nbytes;
+            size_t j = i + 1;
+            while (j < e && f->nbytes == p->desc.slot_stride && fills[j].nbytes == f->nbytes &&
+                   fills[j].window == f->window && fills[j].offset == f->offset + (j - i) * f->nbytes &&
+                   c.global_slot(layer, fills[j].slot) == gs + (j - i)) {
+                bytes += f->nbytes;
+                ++j;
+            }
+            HIP_OK(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, side));
+            i = j;
         }
         HIP_OK(launch_set_gens(p->gen_dev, pub, side));
     }

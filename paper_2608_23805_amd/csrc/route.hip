@@ -452,14 +452,26 @@ __global__ void __launch_bounds__(1024) route_small_kernel(const float *__restri
 // counter wraps back to zero on its arrival) acquires every workgroup's
 // logits and runs the selection and permutation of route_small_kernel.  No
 // workgroup waits for another, so the launch completes in any schedule.
-template <int PER>
+//
+// STAGED (d <= 4096, at most 8 K steps per wavefront): the router rows are
+// read with 16-byte loads that run along the rows (16 rows x 64 B per K step,
+// 64 / (4 * steps) rows per load instruction) into the wavefront's own LDS
+// region and the MFMA fragments are read back from there, as in the
+// quantized stream kernels; loads in the fragment layout touch all 16 rows
+// with every instruction.  A wavefront's LDS operations execute in order, so
+// the region needs no barrier.
+constexpr int ROUTE_STAGE_MAX_STEPS = 8;
+
+__host__ __device__ constexpr int route_stage_row_bytes(int steps) { return steps * 64 + 16; }
+
+template <int PER, bool STAGED>
 __global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__restrict__ x,
                                                             const uint16_t *__restrict__ wr,
                                                             const float *__restrict__ bias, float *L,
                                                             uint32_t *__restrict__ arrive, RouteOut o, int T, int d,
                                                             int K, int E)
 {
-    extern __shared__ uint32_t bits[];          // [E][1]
+    extern __shared__ uint32_t bits[];          // [E][1], then (STAGED) 16 wavefront regions
     __shared__ f32x4 red[16][64];
     __shared__ uint32_t last;
     constexpr int GROUPS = 4, WPG = 16 / GROUPS;   // summation groups, wavefronts per group
@@ -470,21 +482,47 @@ __global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__re
     const int e0 = int(blockIdx.x) * 16;
     const int j = lane & 15, kg = (lane >> 4) * 8;
     // rows past E and tokens past T read a valid row; their sums are never stored
-    const uint16_t *wp = wr + int64_t(min(e0 + j, E - 1)) * d + kg;
     const uint16_t *xp = x + int64_t(min(j, T - 1)) * d + kg;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int st = s0; st < s1; st += 4) {
-        u32x4 wv[4], xv[4];
+    if constexpr (STAGED) {
+        const int nst = s1 - s0, cpr = 4 * nst;        // K steps and 16-byte chunks per row
+        const int RS = route_stage_row_bytes(per);
+        uint8_t *wst = reinterpret_cast<uint8_t *>(bits + ((E + 3) & ~3)) + wave * 16 * RS;
+        u32x4 v[ROUTE_STAGE_MAX_STEPS], xv[ROUTE_STAGE_MAX_STEPS];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int k = min(st + u, s1 - 1) * 32;       // clamped: no branch around the loads
-            wv[u] = load_stream16(wp + k);
-            xv[u] = *reinterpret_cast<const u32x4 *>(xp + k);
+        for (int k = 0; k < ROUTE_STAGE_MAX_STEPS; ++k)
+            if (k < nst) {
+                const int ci = 64 * k + lane, row = ci / cpr, ch = ci % cpr;
+                v[k] = load_stream16(wr + int64_t(min(e0 + row, E - 1)) * d + s0 * 32 + 8 * ch);
+                xv[k] = *reinterpret_cast<const u32x4 *>(xp + s0 * 32 + 32 * k);
+            }
+#pragma unroll
+        for (int k = 0; k < ROUTE_STAGE_MAX_STEPS; ++k)
+            if (k < nst) {
+                const int ci = 64 * k + lane, row = ci / cpr, ch = ci % cpr;
+                *reinterpret_cast<u32x4 *>(wst + row * RS + 16 * ch) = v[k];
+            }
+#pragma unroll
+        for (int k = 0; k < ROUTE_STAGE_MAX_STEPS; ++k)
+            if (k < nst) {
+                const u32x4 wv = *reinterpret_cast<const u32x4 *>(wst + j * RS + 64 * k + 2 * kg);
+                acc = mfma16(as_bf16x8(wv), as_bf16x8(xv[k]), acc);
+            }
+    } else {
+        const uint16_t *wp = wr + int64_t(min(e0 + j, E - 1)) * d + kg;
+        for (int st = s0; st < s1; st += 4) {
+            u32x4 wv[4], xv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int k = min(st + u, s1 - 1) * 32;       // clamped: no branch around the loads
+                wv[u] = load_stream16(wp + k);
+                xv[u] = *reinterpret_cast<const u32x4 *>(xp + k);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (st + u < s1)
+                    acc = mfma16(as_bf16x8(wv[u]), as_bf16x8(xv[u]), acc);
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (st + u < s1)
-                acc = mfma16(as_bf16x8(wv[u]), as_bf16x8(xv[u]), acc);
     }
     red[wave][lane] = acc;
     __syncthreads();
@@ -539,6 +577,10 @@ hipError_t init_route_attributes()
     set(reinterpret_cast<const void *>(&route_small_kernel<4>));
     set(reinterpret_cast<const void *>(&route_small_kernel<8>));
     set(reinterpret_cast<const void *>(&route_small_kernel<16>));
+    set(reinterpret_cast<const void *>(&route_decode_kernel<2, true>));
+    set(reinterpret_cast<const void *>(&route_decode_kernel<4, true>));
+    set(reinterpret_cast<const void *>(&route_decode_kernel<8, true>));
+    set(reinterpret_cast<const void *>(&route_decode_kernel<16, true>));
     return e;
 }
 
@@ -556,8 +598,14 @@ template <int PER>
 static void launch_route_decode_t(const uint16_t *x, const uint16_t *wr, const float *bias, float *L,
                                   uint32_t *arrive, const RouteOut &o, int T, int d, int K, int E, hipStream_t s)
 {
-    launch_k(route_decode_kernel<PER>, unsigned((E + 15) / 16), 1024, size_t(E) * sizeof(uint32_t), s, x, wr, bias,
-             L, arrive, o, T, d, K, E);
+    const int per = (d / 32 + 15) / 16;
+    const size_t bits = size_t((E + 3) & ~3) * sizeof(uint32_t);
+    if (per <= ROUTE_STAGE_MAX_STEPS)
+        launch_k(route_decode_kernel<PER, true>, unsigned((E + 15) / 16), 1024,
+                 bits + size_t(16) * 16 * route_stage_row_bytes(per), s, x, wr, bias, L, arrive, o, T, d, K, E);
+    else
+        launch_k(route_decode_kernel<PER, false>, unsigned((E + 15) / 16), 1024, bits, s, x, wr, bias, L, arrive, o,
+                 T, d, K, E);
 }
 
 hipError_t launch_route_decode(const uint16_t *x, const uint16_t *wr, const float *bias, float *L,
