@@ -189,7 +189,9 @@ typedef struct {
     uint32_t hit;                /* 1 if the object was already resident       */
 } msi_ticket;
 
-/* Device arrays describing one routing of T tokens (all caller-owned). */
+/* Device arrays describing one routing of T tokens (all caller-owned).  For
+ * an empty batch (T == 0) the per-row arrays may be null; counts, offsets and
+ * demand are always written (all zero for T == 0). */
 typedef struct {
     int32_t *idx;                /* [T, K] selected experts, ascending per token      */
     float *weights;              /* [T, K] gate weights (restricted softmax), fp32    */

@@ -607,9 +607,12 @@ msi_status enqueue_fills(msi_plan *p, uint32_t layer, const std::vector<FillReco
     return MSI_OK;
 }
 
-bool routing_ok(const msi_routing &r)
+// The per-expert arrays are always written; the per-row ones may be null
+// for an empty batch (zero-length arrays).
+bool routing_ok(const msi_routing &r, uint64_t T)
 {
-    return r.idx && r.weights && r.counts && r.offsets && r.demand && r.perm && r.inv && r.row_weight;
+    return r.counts && r.offsets && r.demand &&
+           (T == 0 || (r.idx && r.weights && r.perm && r.inv && r.row_weight));
 }
 
 RouteOut route_out(const msi_routing &r)
@@ -968,7 +971,7 @@ msi_status msi_route(msi_plan *p, const msi_route_args *a, void *stream)
     const std::string lim = batch_limit_error(d, a->n_tokens);
     if (!lim.empty())
         return fail(MSI_E_INVALID_ARG, lim);
-    if (!routing_ok(a->r) || (T > 0 && (!a->x || !a->w_router)))
+    if (!routing_ok(a->r, a->n_tokens) || (T > 0 && (!a->x || !a->w_router)))
         return fail(MSI_E_INVALID_ARG, "null routing or input pointer");
     const Workspace ws = workspace_layout(d, a->n_tokens);
     if (!a->workspace || a->workspace_bytes < ws.total)
@@ -1015,7 +1018,7 @@ static msi_status forward_check(const msi_plan *p, const msi_forward_args *a)
     const std::string lim = batch_limit_error(d, a->n_tokens);
     if (!lim.empty())
         return fail(MSI_E_INVALID_ARG, lim);
-    if (!routing_ok(a->r) || !a->out || (a->n_tokens > 0 && !a->x))
+    if (!routing_ok(a->r, a->n_tokens) || (a->n_tokens > 0 && (!a->x || !a->out)))
         return fail(MSI_E_INVALID_ARG, "null routing, input or output pointer");
     return MSI_OK;
 }

@@ -143,6 +143,27 @@ def test_small_bf16_ragged_T(o, small):
         plan.close()
 
 
+def test_empty_batch(small):
+    """T = 0: routing writes zero counts, offsets and an empty demanded list
+    (per-row arrays are empty, passed as null), the forward publishes nothing
+    and returns MSI_OK, and the next full batch is unaffected."""
+    import torch
+    import paper_2608_23805_amd as msi
+    log("case small_bf16 T=0")
+    dl = device_layer(small)
+    plan = make_plan(small, capacity=32)
+    ref = run_layer(plan, dl)["out"].cpu().numpy()
+    for _ in range(2):                            # after a full batch, and after an empty one
+        res = run_layer(plan, dl, T=0)
+        assert res["status"] == 0
+        assert not res["counts"].any() and not res["offsets"].any() and res["demand"][0] == 0
+        assert res["out"].shape == (0, SMALL.shape.d)
+    st = plan.stats()
+    assert st["fills_in_flight"] == 0 and st["consumers_live"] == 0
+    assert run_layer(plan, dl)["out"].cpu().numpy().tobytes() == ref.tobytes()
+    plan.close()
+
+
 def test_stream_and_tile_paths_agree(small):
     """Forcing every expert through the tile path (threshold 1) changes only
     rounding, never more than the bf16 tolerance."""
