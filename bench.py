@@ -304,7 +304,10 @@ def bench_stack(args, cs, side):
     overlap fraction of a pass with fills compares its wall W with copies
     alone, C = H2D bytes / measured pinned H2D peak, and compute alone, K =
     the warm all-resident pass: (C + K - W) / min(C, K), 1 when the smaller
-    hides entirely under the larger, 0 when they run one after the other."""
+    hides entirely under the larger, 0 when they run one after the other
+    (or when W - C, the time beyond the copies, exceeds K: then the pass is
+    bound by the copies and their overheads, and copy_efficiency = C / W says
+    how close it comes to the copies alone)."""
     import time as _t
     import torch
     import synth
@@ -341,6 +344,10 @@ def bench_stack(args, cs, side):
         r["copy_alone_s"] = round(C, 3)
         r["overlap_fraction"] = round(max(0.0, (C + K - W) / min(C, K)), 3) if C > 0 else None
         r["h2d_frac_of_peak"] = round(r["h2d_GBs"] / peak, 3)
+        # the pass beyond its copies at the measured peak: an upper bound on exposed compute
+        # (K) plus per-copy and per-layer overheads; copy_efficiency = C / W
+        r["beyond_copies_s"] = round(W - C, 3) if C > 0 else None
+        r["copy_efficiency"] = round(C / W, 3) if C > 0 else None
     log(f"[bench] stack: pinned H2D peak {peak:.1f} GB/s, overlap "
         f"{[res[f'capacity_{c}']['overlap_fraction'] for c in (0, 64, 512)]}")
     return res

@@ -506,6 +506,14 @@ msi_status PlanCore::schedule_forward(uint32_t layer, const std::vector<int32_t>
         }
         (resident_slot(layer, uint32_t(e)) >= 0 ? hits : misses).push_back(e);
     }
+    // misses go in storage order (window, offset) for window-backed plans:
+    // with victims handed out in slot order, objects stored one after another
+    // then fill consecutive slots and their copies merge into one
+    if (!source_backed_)
+        std::stable_sort(misses.begin(), misses.end(), [&](int32_t a, int32_t b) {
+            const ObjectInfo *oa = object(layer, uint32_t(a)), *ob = object(layer, uint32_t(b));
+            return oa->window != ob->window ? oa->window < ob->window : oa->offset < ob->offset;
+        });
     // rounds are sized by the demand bank: misses fill only there, hits in the
     // prefetch bank take no demand slot
     const uint32_t A = demand_slots();

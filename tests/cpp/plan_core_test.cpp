@@ -193,7 +193,7 @@ static void test_rounds(uint32_t slots, uint32_t transient, size_t ndem)
             std::set<int32_t> filled;
             for (const FillRecord &fr : r.fills) {
                 filled.insert(int32_t(fr.expert));
-                CHECK(!misses_started || int32_t(fr.expert) > last_miss);   // misses ascending
+                CHECK(!misses_started || int32_t(fr.expert) > last_miss);   // storage order (= id order here)
                 last_miss = int32_t(fr.expert);
             }
             if (!r.fills.empty())
@@ -334,9 +334,32 @@ static void test_prefetch_bank()
     CHECK(PlanCore(g.d, OB).status() == MSI_E_INVALID_ARG);
 }
 
+// Misses are scheduled in storage order: with objects stored in reverse id
+// order, a cold forward fills them from the window's start, in consecutive
+// slots (so their copies can merge).
+static void test_storage_order()
+{
+    Fixture f(1, 8, 8);
+    for (uint32_t e = 0; e < 8; ++e)
+        f.objs[e].offset = (7 - e) * OB;
+    PlanCore c(f.d, OB);
+    CHECK(c.status() == MSI_OK);
+    Schedule s;
+    CHECK(c.schedule_forward(0, {0, 1, 2, 3, 4, 5, 6, 7}, &s) == MSI_OK && s.rounds.size() == 1);
+    const std::vector<FillRecord> &fl = s.rounds[0].fills;
+    CHECK(fl.size() == 8);
+    for (size_t i = 0; i < fl.size(); ++i) {
+        CHECK(fl[i].expert == 7 - i && fl[i].offset == i * OB);
+        CHECK(fl[i].slot == fl[0].slot + i);
+    }
+    complete_all(c, s);
+    c.end_forward(0, s);
+}
+
 int main()
 {
     test_manifest();
+    test_storage_order();
     test_protected_lru();
     test_prefetch_bank();
     test_batch_limits();
