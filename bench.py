@@ -71,13 +71,17 @@ def _setup(wl, capacity, T=None, n_batches=1):
 
 
 def _run(plan, xs, dev, r, ws, out, steps, warmup, cs, side, on_step=None):
-    """warmup + timed steps; returns ms per step of the timed region."""
+    """warmup + timed steps; returns ms per step of the timed region.  Each
+    step is msi_route then msi_moe_forward through argument structs built
+    once per input buffer (the binding's prepare_step)."""
     import torch
+    import paper_2608_23805_amd as msi
+    calls = [plan.prepare_step(0, x, dev["wr"], dev["bias"], r, dev["shared"], out, ws, cs, side) for x in xs]
 
     def step(i):
-        x = xs[i % len(xs)]
-        plan.route(x, dev["wr"], dev["bias"], r, ws, cs)
-        plan.forward(0, x, r, dev["shared"], out, ws, cs, side)
+        st = calls[i % len(calls)]()
+        if st != 0:
+            raise msi.MsiError(st, msi.last_error())
         if on_step is not None:
             on_step(i)
 

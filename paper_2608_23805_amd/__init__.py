@@ -378,6 +378,30 @@ class Plan:
                 side_stream=None):
         _check(self.forward_status(layer, x, routing, shared, out, workspace, compute_stream, side_stream))
 
+    def prepare_step(self, layer: int, x, w_router, bias, routing: Routing, shared, out, workspace,
+                     compute_stream=None, side_stream=None):
+        """msi_route then msi_moe_forward on fixed buffers, with the argument
+        structs built once: calling the result (no arguments) issues both
+        calls and returns the forward's status.  For loops that reuse the same
+        buffers, where rebuilding the structs on every call would be most of
+        the host time between steps."""
+        ra = msi_route_args(n_tokens=x.shape[0], reserved=0, x=_ptr(x), w_router=_ptr(w_router),
+                            bias=_ptr(bias), r=routing.c(), workspace=_ptr(workspace),
+                            workspace_bytes=workspace.numel())
+        fa = msi_forward_args(layer=layer, n_tokens=x.shape[0], x=_ptr(x), r=routing.c(),
+                              shared_object=_ptr(shared), out=_ptr(out), workspace=_ptr(workspace),
+                              workspace_bytes=workspace.numel())
+        h, cs, ss = self.h, _stream(compute_stream), _stream(side_stream)
+        rp, fp = ctypes.byref(ra), ctypes.byref(fa)
+        route, forward = lib.msi_route, lib.msi_moe_forward
+        keep = (x, w_router, bias, routing, shared, out, workspace, ra, fa)   # buffers outlive the calls
+
+        def step() -> int:
+            _ = keep
+            st = route(h, rp, cs)
+            return st if st != MSI_OK else forward(h, fp, cs, ss)
+        return step
+
     def hold(self, layer: int, slot: int):
         _check(lib.msi_slot_hold(self.h, layer, slot))
 
