@@ -232,35 +232,95 @@ struct StageRows {
     }
 };
 
-// ---- wavefront reductions (64 lanes)
+// ---- wavefront reductions and scans (64 lanes)
+// Cross-lane moves without LDS: DPP (permutations and shifts within rows of
+// 16 lanes, broadcasts of lanes 15 and 31) and the gfx950 lane swaps, which
+// exchange lanes 16 or 32 apart.
+namespace dpp {
+constexpr int QUAD_1032 = 0xB1, QUAD_2301 = 0x4E;   // lanes l ^ 1, l ^ 2 within a quad
+constexpr int ROW_SHR = 0x110;                      // + n: lane l - n of the same row
+constexpr int ROW_MIRROR = 0x140, ROW_HALF_MIRROR = 0x141;
+constexpr int ROW_BCAST15 = 0x142, ROW_BCAST31 = 0x143;
+}  // namespace dpp
+
+// v of the lane CTRL names, in the lanes the row and bank masks enable; 0 in
+// the others and where the named lane lies outside the row.
+template <int CTRL, int ROWS = 0xF, int BANKS = 0xF>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t v)
+{
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, ROWS, BANKS, true));
+}
+
+// op over all 64 lanes, the same value in every lane: each step combines lane
+// l with a partner whose own step combines the same two values (commutative
+// op, so all lanes agree bit for bit), in a fixed tree.
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op)
+{
+    v = op(v, __uint_as_float(dpp_move<dpp::QUAD_1032>(__float_as_uint(v))));
+    v = op(v, __uint_as_float(dpp_move<dpp::QUAD_2301>(__float_as_uint(v))));
+    v = op(v, __uint_as_float(dpp_move<dpp::ROW_HALF_MIRROR>(__float_as_uint(v))));
+    v = op(v, __uint_as_float(dpp_move<dpp::ROW_MIRROR>(__float_as_uint(v))));
+    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return op(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+}
+
 __device__ __forceinline__ float wave_max(float v)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1)
-        v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
+    return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
 
 __device__ __forceinline__ float wave_sum(float v)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1)
-        v += __shfl_xor(v, off, 64);
-    return v;
+    return wave_reduce(v, [](float a, float b) { return a + b; });
+}
+
+// Inclusive prefix sum over the 64 lanes: within each row the sums of up to
+// 4, 8 and 16 preceding lanes, then the totals of rows 0 and 1 broadcast
+// into the rows after them.
+__device__ __forceinline__ int wave_scan_incl(int v)
+{
+    const uint32_t u = uint32_t(v);
+    uint32_t s = u + dpp_move<dpp::ROW_SHR + 1>(u);
+    s += dpp_move<dpp::ROW_SHR + 2>(u);
+    s += dpp_move<dpp::ROW_SHR + 3>(u);
+    s += dpp_move<dpp::ROW_SHR + 4, 0xF, 0xE>(s);
+    s += dpp_move<dpp::ROW_SHR + 8, 0xF, 0xC>(s);
+    s += dpp_move<dpp::ROW_BCAST15, 0xA, 0xF>(s);
+    s += dpp_move<dpp::ROW_BCAST31, 0xC, 0xF>(s);
+    return int(s);
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (uint64_t(1) << lane) - 1; }
 
-// Inclusive scan of part[0..1023] by a 1024-thread workgroup.
+// Inclusive scan of one value per thread of a 1024-thread workgroup (wsum:
+// 16 words of LDS): wavefront scans, then the totals of the earlier
+// wavefronts (integers, so the grouping does not change the result).  The
+// caller separates consecutive uses of wsum with a barrier.
+__device__ __forceinline__ int block_scan_incl_1024(int v, int32_t *wsum)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int x = wave_scan_incl(v);
+    if (lane == 63)
+        wsum[wave] = x;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wave; ++w)
+        base += wsum[w];
+    return x + base;
+}
+
+// Inclusive scan of part[0..1023] in place by a 1024-thread workgroup.
 __device__ __forceinline__ void block_scan_1024(int32_t *part)
 {
+    __shared__ int32_t wsum[16];
     const int e = threadIdx.x;
-    for (int off = 1; off < 1024; off <<= 1) {
-        const int v = e >= off ? part[e - off] : 0;
-        __syncthreads();
-        part[e] += v;
-        __syncthreads();
-    }
+    const int x = block_scan_incl_1024(part[e], wsum);
+    __syncthreads();
+    part[e] = x;
+    __syncthreads();
 }
 
 // Work counts of a launch whose work list was built on the device: the grid

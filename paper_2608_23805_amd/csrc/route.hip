@@ -336,33 +336,13 @@ __global__ void __launch_bounds__(256) perm_scatter_kernel(const int32_t *__rest
     }
 }
 
-// Inclusive scan of one value per thread of a 1024-thread workgroup:
-// wavefront scans, then the totals of the earlier wavefronts (integers, so
-// the grouping does not change the result).
-__device__ __forceinline__ int block_scan_incl_1024(int v, int32_t *wsum)
-{
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(v, off, 64);
-        if (lane >= off)
-            v += u;
-    }
-    if (lane == 63)
-        wsum[wave] = v;
-    __syncthreads();
-    int base = 0;
-    for (int w = 0; w < wave; ++w)
-        base += wsum[w];
-    return v + base;
-}
-
 // T <= TMAX (<= PERM_BLOCK): top-K of every token (one wavefront per token),
 // then the histogram, scans and scatter, by one 1024-thread workgroup, with a
 // bitmask of W = ceil(T / 32) words per expert (`bits`, E * W words of LDS).
 // The logits are read from L (bias included).  With select == 0 the
-// selection is read from o.idx / o.w instead.
-template <int PER, int TMAX>
+// selection is read from o.idx / o.w instead.  CLEARED: the caller zeroed
+// the bitmask before its last barrier.
+template <int PER, int TMAX, bool CLEARED = false>
 __device__ __forceinline__ void route_small_body(uint32_t *bits, const float *L, int select, const RouteOut &o,
                                                  int T, int K, int E)
 {
@@ -374,9 +354,11 @@ __device__ __forceinline__ void route_small_body(uint32_t *bits, const float *L,
     __shared__ int32_t cand_e[16][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int W = (T + 31) >> 5;
-    for (int i = threadIdx.x; i < E * W; i += blockDim.x)
-        bits[i] = 0;
-    __syncthreads();
+    if constexpr (!CLEARED) {
+        for (int i = threadIdx.x; i < E * W; i += blockDim.x)
+            bits[i] = 0;
+        __syncthreads();
+    }
     if (select) {
         for (int t = wave; t < T; t += 16) {
             float v[PER];
@@ -481,6 +463,16 @@ __global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__re
     const int s0 = min(wave * per, nks), s1 = min(s0 + per, nks);
     const int e0 = int(blockIdx.x) * 16;
     const int j = lane & 15, kg = (lane >> 4) * 8;
+    // issued before the router rows: the bias of this wavefront's output rows (wavefront 0) and the
+    // selection's bitmask (one word per expert for T <= 32), which only the last workgroup uses
+    float bv[4] = {0.f, 0.f, 0.f, 0.f};
+    if (wave == 0 && bias) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            bv[r] = bias[min(e0 + 4 * (lane >> 4) + r, E - 1)];
+    }
+    for (int i = threadIdx.x; i < E; i += blockDim.x)
+        bits[i] = 0;
     // rows past E and tokens past T read a valid row; their sums are never stored
     const uint16_t *xp = x + int64_t(min(j, T - 1)) * d + kg;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -527,10 +519,6 @@ __global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__re
     red[wave][lane] = acc;
     __syncthreads();
     if (wave == 0) {
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            bv[r] = bias ? bias[min(e0 + 4 * (lane >> 4) + r, E - 1)] : 0.f;
         if (j < T) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -561,7 +549,7 @@ __global__ void __launch_bounds__(1024) route_decode_kernel(const uint16_t *__re
     __syncthreads();                            // orders this workgroup's reads after the acquire
     if (!last)
         return;
-    route_small_body<PER, 16>(bits, L, 1, o, T, K, E);
+    route_small_body<PER, 16, true>(bits, L, 1, o, T, K, E);
 }
 
 // ---------------------------------------------------------------- launchers

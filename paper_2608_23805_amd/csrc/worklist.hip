@@ -12,13 +12,7 @@ namespace msi {
 __device__ __forceinline__ int scan_excl_1024(int v, int32_t *wsum, int &total)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(x, off, 64);
-        if (lane >= off)
-            x += u;
-    }
+    const int x = wave_scan_incl(v);
     __syncthreads();                            // wsum is reused by consecutive scans
     if (lane == 63)
         wsum[wave] = x;
