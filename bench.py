@@ -382,7 +382,10 @@ def bench_source_df(args, cs, side, pool=None):
     tmpdir = os.environ.get("TMPDIR", "/tmp")
     path = os.path.join(tmpdir, f"msi_canonical_{os.getpid()}.bin")
     comps = synth.component_sizes(s)
-    ext = synth.write_canonical_file(path, [pool.expert(e) for e in range(s.E)], comps, seed=1)
+    objects = [pool.expert(e) for e in range(s.E)]
+    # every arm reads a file written (and flushed) just for it, with the same bytes at the same offsets, so
+    # no arm finds the extents in a read cache that an earlier arm filled
+    ext = synth.write_canonical_file(path, objects, comps, seed=1, sync=True)
     loc = {}
     for (i, c, off, n) in ext:
         loc.setdefault(i, []).append((c, off, n))
@@ -421,10 +424,15 @@ def bench_source_df(args, cs, side, pool=None):
         return wall, outs, stt, ss
 
     pairs = []
+    fresh = False                   # the file written above serves the first arm
     try:
         for order in ("DF", "FD")[:args.df_pairs]:
             res = {}
             for a in order:
+                if fresh:
+                    os.remove(path)
+                    assert synth.write_canonical_file(path, objects, comps, seed=1, sync=True) == ext
+                fresh = True
                 res[a] = arm(1, 1) if a == "D" else arm(8, 8)
                 log(f"[bench] source arm {a}: {res[a][0]:.2f} s, fills {res[a][2]['fills']}, "
                     f"waited {res[a][3]['wait_seconds']:.2f} s, peak depth {res[a][3]['peak_depth']}")

@@ -43,6 +43,7 @@ tokens, with uneven counts".
 """
 from __future__ import annotations
 
+import os
 import dataclasses
 from typing import Optional
 
@@ -415,12 +416,13 @@ def component_sizes(shape: LayerShape):
     return [m(shape.I, shape.d), m(shape.I, shape.d), m(shape.d, shape.I)]
 
 
-def write_canonical_file(path: str, objects, comp_sizes, seed: int = 0, gap: int = 1000):
+def write_canonical_file(path: str, objects, comp_sizes, seed: int = 0, gap: int = 1000, sync: bool = False):
     """Write objects (uint8 arrays, each the concatenation of its components)
     to one canonical file with every component at its own offset: components
     in a seeded shuffled order, each followed by ``gap`` filler bytes so that
-    no extent is aligned to the direct-I/O block.  Returns the extents as
-    (object index, component, offset, nbytes) tuples."""
+    no extent is aligned to the direct-I/O block (``sync``: flushed to the
+    device before returning).  Returns the extents as (object index,
+    component, offset, nbytes) tuples; the same arguments give the same file."""
     import numpy as np
     order = [(i, c) for i in range(len(objects)) for c in range(len(comp_sizes))]
     perm = np.random.Generator(np.random.PCG64(np.random.SeedSequence([MASTER, 900, seed]))).permutation(len(order))
@@ -437,4 +439,7 @@ def write_canonical_file(path: str, objects, comp_sizes, seed: int = 0, gap: int
             off += comp_sizes[c]
             fh.write(b"\xa5" * gap)
             off += gap
+        if sync:
+            fh.flush()
+            os.fsync(fh.fileno())
     return sorted(extents)
