@@ -156,6 +156,7 @@ struct WorklistArgs {
     WorkItem *items[4];                  // gate/up tile, down tile, gate/up stream, down stream; E + 1 each
     DevCount *counts_out;                // [4]
     int E, T, thr, has_shared;
+    int clear_status;                    // zero the status word first (the last forward left it set)
     TileGeom gu, dn;                     // tile-path geometry
     int per_gu_stream, per_dn_stream;    // tiles per stream item
 };

@@ -1149,8 +1149,7 @@ static msi_status forward_impl(msi_plan *p, const msi_forward_args *a, const Fwd
         W.dn = ks.geom_dn(D, I);
         W.per_gu_stream = ks.tiles_gu_stream(1, D, I);
         W.per_dn_stream = ks.tiles_dn_stream(1, D, I);
-        if (!p->status_clean)
-            HIP_OK(launch_clear_word(p->status_dev, cs));
+        W.clear_status = p->status_clean ? 0 : 1;
         p->status_clean = false;
         __atomic_store_n(&p->tail_host[0], 0u, __ATOMIC_RELAXED);
         HIP_OK(p->timed_launch(MSI_K_PERMUTE, cs, [&] { return launch_build_worklist(W, cs); }));

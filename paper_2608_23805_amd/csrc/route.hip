@@ -381,6 +381,29 @@ __device__ __forceinline__ void route_small_body(uint32_t *bits, const float *L,
     }
     __syncthreads();
     const int e = threadIdx.x;
+    if (T == 1) {
+        // one token: its K experts, ascending, are the demanded list and rows 0 .. K-1 of the permutation;
+        // the first permuted row of expert e is the number of selected experts below e
+        int below = 0;
+        for (int k = 0; k < K; ++k)
+            below += sidx[k] < e ? 1 : 0;
+        if (e < E) {
+            const bool mine = below < K && sidx[below] == e;
+            o.counts[e] = mine ? 1 : 0;
+            o.offsets[e] = below;
+        }
+        if (e < K) {
+            o.demand[1 + e] = sidx[e];
+            o.perm[e] = 0;
+            o.inv[e] = e;
+            o.row_weight[e] = sw[e];
+        }
+        if (e == 0) {
+            o.offsets[E] = K;
+            o.demand[0] = K;
+        }
+        return;
+    }
     int c = 0;
     if (e < E)
         for (int q = 0; q < W; ++q)

@@ -32,9 +32,17 @@ __device__ __forceinline__ int scan_excl_1024(int v, int32_t *wsum, int &total)
 // expert, the shared expert's item first in the tile lists, so the lists and
 // their tile numbering are those the host schedule builds for an all-resident
 // round.  A demanded expert without a published slot raises STATUS_MISS.
+// With clear_status the kernel first zeroes the status word (in place of a
+// launch of its own): the store completes before the workgroup's barrier,
+// ahead of any bit this forward raises.
 __global__ void __launch_bounds__(1024) build_worklist_kernel(WorklistArgs A)
 {
     __shared__ int32_t wsum[16];
+    if (A.clear_status) {
+        if (threadIdx.x == 0)
+            __hip_atomic_store(A.status, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+    }
     const int e = threadIdx.x;
     const bool in = e < A.E;
     const int c = in ? A.counts[e] : 0;

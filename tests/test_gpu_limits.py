@@ -1,7 +1,7 @@
 """A layer at the ABI's largest expert count and top-k (E = 1024, K = 16;
-bf16, d = 256, I = 128) through the C ABI on every selection path: T = 16
-(one launch: logits, selection and permutation; the device-built decode
-list on repeats), T = 200 (one-workgroup selection) and T = 600 (one
+bf16, d = 256, I = 128) through the C ABI on every selection path: T = 1
+(one launch, the one-token permutation) and T = 16 (one launch: logits,
+selection and permutation; the device-built decode list on repeats), T = 200 (one-workgroup selection) and T = 600 (one
 wavefront per token, then the histogram / scan / scatter permutation).  Every
 token's output against the fp64 oracle (max-abs / max|ref| <= 1e-2), the
 permutation against the oracle's counting sort, and outputs byte-identical at
@@ -29,7 +29,7 @@ def li():
     return synth.layer_inputs(WL)
 
 
-@pytest.mark.parametrize("T", [16, 200, 600])
+@pytest.mark.parametrize("T", [1, 16, 200, 600])
 def test_largest_expert_count_and_topk(o, li, T):
     dl = device_layer(li)
     outs = []

@@ -298,6 +298,7 @@ def test_decode_q4_full(o):
         if cap == 512:
             err, near, _ = oracle_compare(o, li, res, [0], TOL_BF16)
             log(f"decode_q4 err={err:.3e} near_ties={len(near)}")
+            _check_permutation(o, res, wl.shape.E)
         outs.append(res["out"].cpu().numpy())
         plan.close()
     assert outs[0].tobytes() == outs[1].tobytes()
