@@ -458,14 +458,16 @@ __global__ void __launch_bounds__(1024) route_small_kernel(const float *__restri
 // logits and runs the selection and permutation of route_small_kernel.  No
 // workgroup waits for another, so the launch completes in any schedule.
 //
-// STAGED (d <= 4096, at most 8 K steps per wavefront): the router rows are
+// STAGED (d <= 3584, at most 7 K steps per wavefront): the router rows are
 // read with 16-byte loads that run along the rows (16 rows x 64 B per K step,
 // 64 / (4 * steps) rows per load instruction) into the wavefront's own LDS
 // region and the MFMA fragments are read back from there, as in the
 // quantized stream kernels; loads in the fragment layout touch all 16 rows
 // with every instruction.  A wavefront's LDS operations execute in order, so
-// the region needs no barrier.
-constexpr int ROUTE_STAGE_MAX_STEPS = 8;
+// the region needs no barrier.  The regions (16 x 16 rows of 64 steps + 16
+// bytes), the bitmask (up to 4 KiB) and the kernel's 30 KiB of static LDS
+// must fit the workgroup's 160 KiB: 7 steps take 150 KiB, 8 would take 166.
+constexpr int ROUTE_STAGE_MAX_STEPS = 7;
 
 __host__ __device__ constexpr int route_stage_row_bytes(int steps) { return steps * 64 + 16; }
 
