@@ -2,7 +2,8 @@
 K steps per wavefront through its LDS regions; d = 4096 and 4352: rows read
 in the fragment layout straight from memory) through the C ABI, at T = 1 and
 16 (one-launch decode routing, stream path), and T = 600 (tile router and
-tile path: 75 rows per expert).  Every token's output against the fp64
+tile path: 75 rows per expert); bf16 at all three, the 4-bit and the
+quantized-expert mix at d = 4352.  Every token's output against the fp64
 oracle (max-abs / max|ref| <= 1e-2) and the permutation against the
 oracle's counting sort."""
 import numpy as np
@@ -13,9 +14,15 @@ from _gpu_helpers import device_layer, log, make_plan, oracle_compare, run_layer
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = {d: synth.Workload(f"wide_d{d}_bf16", 30 + i, synth.LayerShape(600, d, 32, 4, 128, "bf16"),
-                            prior="zipf", prior_param=1.1, tau=0.3)
+SHAPES = {f"d{d}_bf16": synth.Workload(f"wide_d{d}_bf16", 30 + i, synth.LayerShape(600, d, 32, 4, 128, "bf16"),
+                                       prior="zipf", prior_param=1.1, tau=0.3)
           for i, d in enumerate((3584, 4096, 4352))}
+# the quantized formats at d = 4352 (17 super-blocks, 34 blocks per quarter row: the narrowest chunking
+# of their stream kernels)
+SHAPES["d4352_q4"] = synth.Workload("wide_d4352_q4", 33, synth.LayerShape(600, 4352, 32, 4, 128, "q4b32"),
+                                    prior="zipf", prior_param=1.1, tau=0.3)
+SHAPES["d4352_kq"] = synth.Workload("wide_d4352_kq", 34, synth.LayerShape(600, 4352, 32, 4, 256, "kq"),
+                                    prior="zipf", prior_param=1.1, tau=0.3)
 
 
 @pytest.fixture(scope="module")
@@ -24,9 +31,9 @@ def o():
     return oracle.Oracle()
 
 
-@pytest.mark.parametrize("d", list(SHAPES))
-def test_wide_rows(o, d):
-    wl = SHAPES[d]
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_wide_rows(o, name):
+    wl = SHAPES[name]
     li = synth.layer_inputs(wl)
     dl = device_layer(li)
     plan = make_plan(li, capacity=wl.shape.E)
