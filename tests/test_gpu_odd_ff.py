@@ -1,0 +1,54 @@
+"""Expert intermediate sizes that are not powers of two (d_ff = 384 for bf16
+and the 4-bit format, 768 for the quantized-expert mix; d = 512) through
+the C ABI at T = 1 and 16 (stream path) and T = 600 (tile path), so every
+kernel runs with its odd-sized chunkings: three gate/up slices of the tile
+kernels, twelve K stages of the down tile, the single-batch stream down.
+Every token's output against the fp64 oracle (max-abs / max|ref| <= 1e-2),
+the permutation against the oracle's counting sort, and outputs
+byte-identical between an all-resident plan and one with a third of the
+slots."""
+import numpy as np
+import pytest
+
+import synth
+from _gpu_helpers import device_layer, log, make_plan, oracle_compare, run_layer
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = {
+    "bf16_I384": synth.Workload("odd_ff_bf16", 35, synth.LayerShape(600, 512, 24, 4, 384, "bf16"),
+                                prior="zipf", prior_param=1.1, tau=0.3),
+    "q4_I384": synth.Workload("odd_ff_q4", 36, synth.LayerShape(600, 512, 24, 4, 384, "q4b32"),
+                              prior="zipf", prior_param=1.1, tau=0.3),
+    "kq_I768": synth.Workload("odd_ff_kq", 37, synth.LayerShape(600, 512, 24, 4, 768, "kq"),
+                              prior="zipf", prior_param=1.1, tau=0.3),
+}
+
+
+@pytest.fixture(scope="module")
+def o():
+    import oracle
+    return oracle.Oracle()
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_odd_intermediate(o, name):
+    wl = SHAPES[name]
+    li = synth.layer_inputs(wl)
+    dl = device_layer(li)
+    for T in (1, 16, 600):
+        outs = []
+        for cap in (wl.shape.E, 8):
+            log(f"case {wl.name} T={T} capacity={cap}")
+            plan = make_plan(li, capacity=cap)
+            res = run_layer(plan, dl, T=T)
+            assert res["status"] == 0
+            if cap == wl.shape.E:
+                err, near, _ = oracle_compare(o, li, res, list(range(T)), 1e-2)
+                log(f"{wl.name} T={T} err={err:.3e} near_ties={len(near)}")
+                counts, offsets, perm, inv = o.permute(np.sort(res["idx"], axis=1), wl.shape.E)
+                assert np.array_equal(res["counts"], counts) and np.array_equal(res["perm"], perm)
+                assert np.array_equal(res["offsets"], offsets) and np.array_equal(res["inv"], inv)
+            outs.append(res["out"].cpu().numpy())
+            plan.close()
+        assert outs[0].tobytes() == outs[1].tobytes()
