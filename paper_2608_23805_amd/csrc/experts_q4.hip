@@ -2,21 +2,25 @@
 //
 // Storage (per matrix [rows, cols]): nibbles [rows, cols/2] (element 2j in the
 // low nibble of byte j, 4-bit two's complement) then fp16 scales
-// [rows, cols/32]; value = scale * q.  Dequantization is exact: q in [-8, 7]
-// is exact in bf16, every 16x16x32 MFMA spans exactly one 32-element scale
-// block, so it returns the block's partial dot product (C = 0) and the scale
-// is applied in fp32: acc += scale * partial.
+// [rows, cols/32]; value = scale * q.  Every 16x16x32 MFMA spans exactly one
+// 32-element scale block, so it returns the block's partial dot product and
+// the scale is applied in fp32: acc += scale * partial.
 //
 //  * stream path (<= 16 tokens per expert): tokens as the A operand and
 //    weights as the B operand, tokens read straight from memory and the
-//    nibbles through row-contiguous loads rearranged in LDS (WaveRows).
-//  * tile path: 128 tokens x 128 weight rows per workgroup, packed nibbles and
-//    scales staged in LDS (a quarter of the bf16 staging traffic), unpacked
-//    to bf16 while the MFMA fragments are built.
+//    nibbles through row-contiguous loads rearranged in LDS (WaveRows); the
+//    codes unpacked to exact bf16 q (C = 0).
+//  * tile path: 128 tokens x 128 weight rows per workgroup; A rows, packed
+//    nibbles and scales copied from memory straight into two LDS stage
+//    buffers (three workgroups per CU); the codes enter the MFMA as the exact
+//    bf16 136 + q, and the offset leaves through the C input (-136 times the
+//    A row's block sum, from one more MFMA per A fragment).
 #include "common.h"
 #include "kernels.h"
 
 namespace msi {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ uint32_t q4_matrix_bytes(int rows, int cols)
 {
@@ -33,6 +37,25 @@ __device__ __forceinline__ bf16x8 unpack_q4(uint32_t q)
         const int hi = int(q << (24 - 8 * h)) >> 28;          // element 2h + 1
         r[h] = (__float_as_uint(float(lo)) >> 16) | (__float_as_uint(float(hi)) & 0xFFFF0000u);
     }
+    return __builtin_bit_cast(bf16x8, r);
+}
+
+// 8 nibbles (element e at bits 4e..4e+3, two's complement q) -> 8 exact bf16
+// values 136 + q: the bits 0x4300 | u are the bf16 128 + u, u = q + 8 = the
+// nibble with its top bit flipped.  Byte permutes place the nibbles (even
+// elements from the low halves of the bytes, odd ones from the high halves)
+// under the 0x43 bytes: nine operations per 8 values.
+__device__ __forceinline__ bf16x8 unpack_q4_136(uint32_t w)
+{
+    const uint32_t e = (w ^ 0x08080808u) & 0x0F0F0F0Fu;           // u of elements 0, 2, 4, 6
+    const uint32_t o = ((w >> 4) ^ 0x08080808u) & 0x0F0F0F0Fu;    // u of elements 1, 3, 5, 7
+    const uint32_t lo = __builtin_amdgcn_perm(o, e, 0x05010400u);  // bytes u0 u1 u2 u3
+    const uint32_t hi = __builtin_amdgcn_perm(o, e, 0x07030602u);  // bytes u4 u5 u6 u7
+    u32x4 r;
+    r[0] = __builtin_amdgcn_perm(0x43434343u, lo, 0x04010400u);
+    r[1] = __builtin_amdgcn_perm(0x43434343u, lo, 0x04030402u);
+    r[2] = __builtin_amdgcn_perm(0x43434343u, hi, 0x04010400u);
+    r[3] = __builtin_amdgcn_perm(0x43434343u, hi, 0x04030402u);
     return __builtin_bit_cast(bf16x8, r);
 }
 
@@ -297,14 +320,15 @@ hipError_t launch_down_q4_stream(const ExpertLaunch &L, hipStream_t s)
 // ============================================================== tile path
 
 namespace q4t {
-constexpr int BM = 128, BN = 128, BK = 64, THREADS = 256;
-constexpr int LDA = BK + 8;                 // bf16 elements per staged A row
-constexpr int LDQ = BK / 2 + 4;             // bytes per staged nibble row (36: conflict-spread)
-constexpr int A_BYTES = BM * LDA * 2;
-constexpr int Q_BYTES = BN * LDQ;
-constexpr int S_BYTES = BN * (BK / 32) * 2;
+constexpr int BM = 128, BN = 128, BK = 64, THREADS = 256, NBUF = 2;
+constexpr int A_ROWB = BK * 2;              // bytes of bf16 per staged A row
+constexpr int Q_ROWB = BK / 2;              // bytes of codes per staged weight row
+constexpr int A_BYTES = BM * A_ROWB;        // 16 KiB
+constexpr int Q_BYTES = BN * Q_ROWB;        // 4 KiB
+constexpr int S_BYTES = 2 * BN * (BK / 32) * 2;   // the 512 bytes of scales, then a spare 512 for idle copies
 constexpr int STAGE = A_BYTES + Q_BYTES + S_BYTES;
-constexpr size_t LDS_BYTES = size_t(2) * STAGE;
+constexpr int COPIES = 6;                   // copy instructions per wavefront per stage
+constexpr size_t LDS_BYTES = size_t(NBUF) * STAGE;
 }  // namespace q4t
 
 int tiles_gateup_q4_tile(int nrows, int d, int I)
@@ -335,7 +359,7 @@ TileGeom geom_down_q4_tile(int d, int I)
 // matching up rows; wavefront (wm, wn) owns rows wm*64.., gate columns
 // wn*32.. and the matching up columns, so SiLU * up forms in registers.
 template <bool GATEUP>
-__global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L)
+__global__ void __launch_bounds__(q4t::THREADS, 3) tile_q4_kernel(ExpertLaunch L)
 {
     using namespace q4t;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds8[];
@@ -353,7 +377,8 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
     const int local = t - it.tile0;
     const int m0 = (local / ntn) * BM;
     const int nt = local % ntn;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // (uniform: copy destinations and resources)
     const int wm = wave >> 1, wn = wave & 1;
 
     const uint16_t *abase = reinterpret_cast<const uint16_t *>(GATEUP ? L.x : (sh ? L.act_s : L.act));
@@ -361,57 +386,66 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
     const uint8_t *obj = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mbytes = q4_matrix_bytes(I, d);
 
-    // A: 128 rows x 64 bf16 per stage = 8 chunks of 16 B per row; 4 per thread
+    // Stage copies go from memory straight into a ring of three LDS stage buffers (buffer loads with an
+    // LDS destination, no register staging).  Per stage and wavefront: four 1 KiB copies of A rows (lane l
+    // of copy i brings row 8 (4 i + w) + l / 8 into slot l % 8 of its 128-byte LDS row, the 16-byte chunk
+    // (l % 8) ^ aswz(row) of the row's 64 elements), one of weight codes (row 32 w + l / 2, slot l % 2 =
+    // chunk (l % 2) ^ bit 3 of the row) and one of scales (4 bytes: row 64 w + l; wavefronts 2 and 3 copy
+    // nothing into a spare region, so every wavefront waits on the same counts).  The slot permutations put
+    // the 16 rows of each fragment read on distinct banks.
+    auto aswz = [](int r) { return (r >> 1) & 7; };
+    const __amdgpu_buffer_rsrc_t ar =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(abase), 0, 0x7fffffff, 0x00020000u);
+    const __amdgpu_buffer_rsrc_t wr_ = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(obj), 0, 0x7fffffff,
+                                                                         0x00020000u);
+    const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(obj), 0,
+                                                                        wave < 2 ? 0x7fffffff : 0, 0x00020000u);
     uint32_t aoff[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int r = (tid >> 3) + 32 * i;
+        const int r = 8 * (4 * i + wave) + (lane >> 3);
         int64_t src = 0;
         if (m0 + r < it.nrows)
             src = perm ? int64_t(perm[it.row0 + m0 + r]) : int64_t(it.row0 + m0 + r);
-        aoff[i] = uint32_t(src * K) + (tid & 7) * 8;
+        aoff[i] = uint32_t(src * K) * 2u + uint32_t(16 * ((lane & 7) ^ aswz(r)));
     }
-    // B: 128 weight rows x 32 nibble bytes per stage: 2 chunks of 16 B per row, 1 per thread;
-    // scales: 128 rows x 2 fp16 per stage, one 4-byte word per thread for tid < 128
-    const int brow_l = tid >> 1, bchunk = tid & 1;
     auto weight_row = [&](int c) -> int {          // tile column -> matrix row
         if (GATEUP)
             return (c < 64 ? 0 : I) + nt * 64 + (c & 63);
         return nt * BN + c;
     };
-    const int wr_b = weight_row(brow_l);
-    const uint8_t *qmat = GATEUP ? obj + (wr_b >= I ? mbytes : 0u) : obj + 2 * mbytes;
-    const int wr_local = GATEUP ? (wr_b >= I ? wr_b - I : wr_b) : wr_b;
-    const int qrows = GATEUP ? I : d;
-    const uint8_t *qrow = qmat + int64_t(wr_local) * (K / 2) + bchunk * 16;
-    const int wr_s = weight_row(tid & 127);
-    const uint8_t *smat = GATEUP ? obj + (wr_s >= I ? mbytes : 0u) : obj + 2 * mbytes;
-    const int ws_local = GATEUP ? (wr_s >= I ? wr_s - I : wr_s) : wr_s;
-    const uint16_t *srow = reinterpret_cast<const uint16_t *>(smat + uint32_t(qrows) * uint32_t(K / 2)) +
-                           int64_t(ws_local) * (K / 32);
-
-    u32x4 ra[4], rq;
-    uint32_t rs = 0;
-    auto load = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            ra[i] = *reinterpret_cast<const u32x4 *>(abase + (aoff[i] + uint32_t(k0)));
-        rq = *reinterpret_cast<const u32x4 *>(qrow + k0 / 2);
-        if (tid < 128)
-            rs = *reinterpret_cast<const uint32_t *>(srow + k0 / 32);
+    // (a tile column's matrix: gate rows, then up rows, for gate/up; the down matrix for down)
+    auto row_base = [&](int c) -> uint32_t {
+        const int wrw = weight_row(c);
+        const uint32_t mat = GATEUP ? (wrw >= I ? mbytes : 0u) : 2u * mbytes;
+        return mat + uint32_t(GATEUP ? (wrw >= I ? wrw - I : wrw) : wrw) * uint32_t(K / 2);
     };
-    auto store = [&](int buf) {
+    auto scale_base = [&](int c) -> uint32_t {
+        const int wrw = weight_row(c);
+        const uint32_t mat = GATEUP ? (wrw >= I ? mbytes : 0u) : 2u * mbytes;
+        const int rows = GATEUP ? I : d;
+        return mat + uint32_t(rows) * uint32_t(K / 2) + uint32_t(GATEUP ? (wrw >= I ? wrw - I : wrw) : wrw) *
+                                                            uint32_t(K / 32) * 2u;
+    };
+    const int qr = 32 * wave + (lane >> 1);
+    const uint32_t qoff = row_base(qr) + uint32_t(16 * ((lane & 1) ^ ((qr >> 3) & 1)));
+    const uint32_t soff = wave < 2 ? scale_base(64 * wave + lane) : 0u;
+    auto issue = [&](int k0, int buf, bool real) {
         uint8_t *st = lds8 + buf * STAGE;
-        uint16_t *a = reinterpret_cast<uint16_t *>(st);
+        const __amdgpu_buffer_rsrc_t none = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(obj), 0, 0,
+                                                                              0x00020000u);
+#if defined(__HIP_DEVICE_COMPILE__)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            *reinterpret_cast<u32x4 *>(a + ((tid >> 3) + 32 * i) * LDA + (tid & 7) * 8) = ra[i];
-        uint32_t *q = reinterpret_cast<uint32_t *>(st + A_BYTES + brow_l * LDQ + bchunk * 16);
-#pragma unroll
-        for (int w = 0; w < 4; ++w)
-            q[w] = rq[w];
-        if (tid < 128)
-            *reinterpret_cast<uint32_t *>(st + A_BYTES + Q_BYTES + (tid & 127) * 4) = rs;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(real ? ar : none, (lds_void_t *)(st + (4 * i + wave) * 1024), 16,
+                                                     aoff[i], k0 * 2, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(real ? wr_ : none, (lds_void_t *)(st + A_BYTES + wave * 1024), 16,
+                                                 qoff, k0 / 2, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(real ? sr : none, (lds_void_t *)(st + A_BYTES + Q_BYTES + wave * 256),
+                                                 4, soff, k0 / 16, 0, 0);
+#else
+        (void)st, (void)none, (void)k0, (void)real;
+#endif
     };
 
     f32x4 acc[4][4];
@@ -426,25 +460,33 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
             return nb < 2 ? wn * 32 + nb * 16 : 64 + wn * 32 + (nb - 2) * 16;
         return wn * 64 + nb * 16;
     };
+    // The codes enter the MFMA as 136 + q; the -136 * (block sum of the A row) that takes the offset back
+    // out comes from one more MFMA per A fragment, against a fragment of -136, and is the C input of that
+    // fragment's four block partials.
+    const bf16x8 neg136 = __builtin_bit_cast(bf16x8, u32x4{0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u});
     auto compute = [&](int buf) {
         const uint8_t *st = lds8 + buf * STAGE;
-        const uint16_t *a = reinterpret_cast<const uint16_t *>(st);
         const uint8_t *q = st + A_BYTES;
         const uint16_t *sc = reinterpret_cast<const uint16_t *>(st + A_BYTES + Q_BYTES);
 #pragma unroll
         for (int kb = 0; kb < BK / 32; ++kb) {
             bf16x8 af[4];
+            f32x4 corr[4];
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb)
-                af[mb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(a + (wm * 64 + mb * 16 + r16) * LDA + kb * 32 + g * 8));
+            for (int mb = 0; mb < 4; ++mb) {
+                const int r = wm * 64 + mb * 16 + r16;
+                af[mb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(st + r * A_ROWB + 16 * ((4 * kb + g) ^ aswz(r))));
+                corr[mb] = mfma16(af[mb], neg136, f32x4{0.f, 0.f, 0.f, 0.f});
+            }
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
                 const int c = col_of(nb) + r16;                    // B fragment: weight row c
-                const bf16x8 bq = unpack_q4(*reinterpret_cast<const uint32_t *>(q + c * LDQ + kb * 16 + g * 4));
+                const bf16x8 bq = unpack_q4_136(
+                    *reinterpret_cast<const uint32_t *>(q + c * Q_ROWB + 16 * (kb ^ ((c >> 3) & 1)) + 4 * g));
                 const float s = half_to_float(sc[c * 2 + kb]);    // output column of this lane = c
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb) {
-                    const f32x4 part = mfma16(af[mb], bq, f32x4{0.f, 0.f, 0.f, 0.f});
+                    const f32x4 part = mfma16(af[mb], bq, corr[mb]);
 #pragma unroll
                     for (int rr = 0; rr < 4; ++rr)
                         acc[mb][nb][rr] = fmaf(s, part[rr], acc[mb][nb][rr]);
@@ -454,18 +496,16 @@ __global__ void __launch_bounds__(q4t::THREADS, 2) tile_q4_kernel(ExpertLaunch L
     };
 
     const int nk = K / BK;
-    load(0);
-    store(0);
-    if (nk > 1)
-        load(BK);
-    __syncthreads();
+    constexpr int AHEAD = NBUF - 1;                            // stages in flight beside the one computed
+#pragma unroll
+    for (int j = 0; j < AHEAD; ++j)
+        issue(j * BK, j, j < nk);
     for (int kt = 0; kt < nk; ++kt) {
-        compute(kt & 1);
-        if (kt + 1 < nk)
-            store((kt + 1) & 1);
-        if (kt + 2 < nk)
-            load((kt + 2) * BK);
-        __syncthreads();
+        __builtin_amdgcn_s_waitcnt(VMCNT_WAIT(COPIES * (AHEAD - 1)));   // this stage landed
+        __builtin_amdgcn_s_barrier();                          // ... for every wavefront; the buffer refilled
+        asm volatile("" ::: "memory");                         //     next was last read one stage ago
+        issue((kt + AHEAD) * BK, (kt + AHEAD) % NBUF, kt + AHEAD < nk);
+        compute(kt % NBUF);
     }
 
     // lane holds rows 4g + rr of each 16x16 block, column r16
