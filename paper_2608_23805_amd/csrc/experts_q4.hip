@@ -386,7 +386,7 @@ __global__ void __launch_bounds__(q4t::THREADS, 3) tile_q4_kernel(ExpertLaunch L
     const uint8_t *obj = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mbytes = q4_matrix_bytes(I, d);
 
-    // Stage copies go from memory straight into a ring of three LDS stage buffers (buffer loads with an
+    // Stage copies go from memory straight into two LDS stage buffers (buffer loads with an
     // LDS destination, no register staging).  Per stage and wavefront: four 1 KiB copies of A rows (lane l
     // of copy i brings row 8 (4 i + w) + l / 8 into slot l % 8 of its 128-byte LDS row, the 16-byte chunk
     // (l % 8) ^ aswz(row) of the row's 64 elements), one of weight codes (row 32 w + l / 2, slot l % 2 =
@@ -508,29 +508,51 @@ __global__ void __launch_bounds__(q4t::THREADS, 3) tile_q4_kernel(ExpertLaunch L
         compute(kt % NBUF);
     }
 
-    // lane holds rows 4g + rr of each 16x16 block, column r16
+    // Epilogue through LDS (the stage buffers are free once every wavefront has left the K loop): each lane
+    // writes its outputs, rows 4g + rr of each 16x16 block in column r16, as bf16 into a [128][OUTW + 8]
+    // tile, then every thread stores whole 16-byte pieces of the tile's rows.  The row weights of the
+    // lane's 16 rows are read first, all at once.
+    constexpr int OUTW = GATEUP ? 64 : BN;         // output columns of the tile
+    constexpr int LDO = OUTW + 8;                  // bf16 per LDS output row (16 bytes of padding)
+    float rwv[4][4];
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
             const int row = wm * 64 + mb * 16 + 4 * g + rr;
-            if (m0 + row >= it.nrows)
-                continue;
-            const int64_t orow = int64_t(it.row0) + m0 + row;
+            rwv[mb][rr] = (GATEUP || sh || m0 + row >= it.nrows) ? 1.0f : L.row_weight[int64_t(it.row0) + m0 + row];
+        }
+    static_assert(size_t(BM) * LDO * 2 <= LDS_BYTES, "output tile fits the stage buffers");
+    __builtin_amdgcn_s_waitcnt(VMCNT_WAIT(0));    // the last (idle) stage copies have written LDS too
+    __syncthreads();
+    uint16_t *ot = reinterpret_cast<uint16_t *>(lds8);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            uint16_t *orow_l = ot + (wm * 64 + mb * 16 + 4 * g + rr) * LDO;
             if (GATEUP) {
-                uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + orow * I;
 #pragma unroll
                 for (int nb = 0; nb < 2; ++nb)
-                    act[nt * 64 + wn * 32 + nb * 16 + r16] =
-                        f32_to_bf16(silu(acc[mb][nb][rr]) * acc[mb][nb + 2][rr]);
+                    orow_l[wn * 32 + nb * 16 + r16] = f32_to_bf16(silu(acc[mb][nb][rr]) * acc[mb][nb + 2][rr]);
             } else {
-                uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + orow * d;
-                const float w = sh ? 1.0f : L.row_weight[orow];
 #pragma unroll
                 for (int nb = 0; nb < 4; ++nb)
-                    y[nt * BN + wn * 64 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * w);
+                    orow_l[wn * 64 + nb * 16 + r16] = f32_to_bf16(acc[mb][nb][rr] * rwv[mb][rr]);
             }
         }
+    __syncthreads();
+    constexpr int PPR = OUTW / 8;                  // 16-byte pieces per tile row
+    uint16_t *obase = GATEUP ? reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + nt * 64
+                             : static_cast<uint16_t *>(sh ? L.ys : L.y) + nt * BN;
+    const int ostride = GATEUP ? I : d;
+#pragma unroll
+    for (int k = 0; k < BM * PPR / THREADS; ++k) {
+        const int pidx = k * THREADS + tid, row = pidx / PPR, pc = pidx % PPR;
+        if (m0 + row < it.nrows)
+            *reinterpret_cast<u32x4 *>(obase + (int64_t(it.row0) + m0 + row) * ostride + pc * 8) =
+                *reinterpret_cast<const u32x4 *>(ot + row * LDO + pc * 8);
+    }
 }
 
 hipError_t launch_gateup_q4_tile(const ExpertLaunch &L, hipStream_t s)
