@@ -470,6 +470,14 @@ __global__ void __launch_bounds__(q4t::THREADS, 3) tile_q4_kernel(ExpertLaunch L
         const uint16_t *sc = reinterpret_cast<const uint16_t *>(st + A_BYTES + Q_BYTES);
 #pragma unroll
         for (int kb = 0; kb < BK / 32; ++kb) {
+            uint32_t cw[4];
+            uint16_t sr16[4];
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                const int c = col_of(nb) + r16;                    // B fragment: weight row c
+                cw[nb] = *reinterpret_cast<const uint32_t *>(q + c * Q_ROWB + 16 * (kb ^ ((c >> 3) & 1)) + 4 * g);
+                sr16[nb] = sc[c * 2 + kb];
+            }
             bf16x8 af[4];
             f32x4 corr[4];
 #pragma unroll
@@ -478,19 +486,22 @@ __global__ void __launch_bounds__(q4t::THREADS, 3) tile_q4_kernel(ExpertLaunch L
                 af[mb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(st + r * A_ROWB + 16 * ((4 * kb + g) ^ aswz(r))));
                 corr[mb] = mfma16(af[mb], neg136, f32x4{0.f, 0.f, 0.f, 0.f});
             }
+            bf16x8 bq[4];
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+                bq[nb] = unpack_q4_136(cw[nb]);
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
-                const int c = col_of(nb) + r16;                    // B fragment: weight row c
-                const bf16x8 bq = unpack_q4_136(
-                    *reinterpret_cast<const uint32_t *>(q + c * Q_ROWB + 16 * (kb ^ ((c >> 3) & 1)) + 4 * g));
-                const float s = half_to_float(sc[c * 2 + kb]);    // output column of this lane = c
+                const float s = half_to_float(sr16[nb]);          // output column of this lane = c
+                f32x4 part[4];
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) {
-                    const f32x4 part = mfma16(af[mb], bq, corr[mb]);
+                for (int mb = 0; mb < 4; ++mb)
+                    part[mb] = mfma16(af[mb], bq[nb], corr[mb]);
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
                     for (int rr = 0; rr < 4; ++rr)
-                        acc[mb][nb][rr] = fmaf(s, part[rr], acc[mb][nb][rr]);
-                }
+                        acc[mb][nb][rr] = fmaf(s, part[mb][rr], acc[mb][nb][rr]);
             }
         }
     };
