@@ -21,12 +21,15 @@ namespace msi {
 // to arrive (the counter wraps back to zero) clears the word, after every
 // workgroup has read it, so the next forward starts from a clean word without
 // a launch of its own.  Without a counter every thread reads the word.
-// The launch's last workgroup, which has no rows of its own (one more than
+// The launch's first workgroup, which has no rows of its own (one more than
 // the rows need), publishes to pinned host words: the demanded experts
 // (count, then ids) when `demand` is given, then status | STATUS_DONE with a
 // system-scope release, so a host that sees the done bit also sees the list.
 // The release waits for the host stores; in a workgroup of its own that wait
-// runs beside the row work instead of before it.
+// runs beside the row work instead of before it.  Being dispatched first, it
+// publishes when the combine starts (the status is final then: the expert
+// kernels have completed), so the host returns and queues its next work
+// while the row workgroups still write `out`.
 __device__ __forceinline__ uint32_t combine_status(const CombinePublish &P, uint32_t &ticket)
 {
     uint32_t st;
@@ -42,7 +45,7 @@ __device__ __forceinline__ uint32_t combine_status(const CombinePublish &P, uint
     } else {
         st = __hip_atomic_load(P.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (blockIdx.x == gridDim.x - 1 && P.host) {
+    if (blockIdx.x == 0 && P.host) {
         if (P.demand) {
             const int n = P.demand[0];
             for (int i = threadIdx.x; i <= n; i += blockDim.x)
@@ -75,8 +78,8 @@ __global__ void __launch_bounds__(256) combine_f32_kernel(const float *__restric
     if (st != 0u)
         return;
     const int d4 = d / 4;
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= int64_t(T) * d4)
+    const int64_t i = (int64_t(blockIdx.x) - 1) * blockDim.x + threadIdx.x;   // workgroup 0: no rows
+    if (i < 0 || i >= int64_t(T) * d4)
         return;
     const int t = int(i / d4), c = int(i % d4) * 4;
     float4 acc = ys ? *reinterpret_cast<const float4 *>(ys + int64_t(t) * d + c) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -112,8 +115,8 @@ __global__ void __launch_bounds__(256) combine_kernel(const uint16_t *__restrict
 {
     const int d8 = d / 8;
     const int64_t n = int64_t(T) * d8;
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    const bool live = i < n;
+    const int64_t i = (int64_t(blockIdx.x) - 1) * blockDim.x + threadIdx.x;   // workgroup 0: no rows
+    const bool live = i >= 0 && i < n;
     const int64_t ic = live ? i : 0;
     const int t = int(ic / d8), c = int(ic % d8) * 8;
     int32_t row[16];
@@ -161,7 +164,7 @@ hipError_t launch_combine(const void *y, const void *ys, bool f32, const int32_t
 {
     if (!P.status)
         return hipErrorInvalidValue;
-    // the row workgroups, then the publishing one (also for T == 0: the status is still published
+    // the publishing workgroup, then the row ones (also for T == 0: the status is still published
     // and cleared)
     if (f32) {
         const int64_t n = int64_t(T) * (d / 4);
