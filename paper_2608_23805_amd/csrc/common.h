@@ -154,6 +154,22 @@ __device__ __forceinline__ bool direct_item(const DirectList &D, int i, int per_
     return true;
 }
 
+// Generation word of the tile's slot (read early, compared late).
+__device__ __forceinline__ uint32_t slot_gen_now(const WorkItem &it, const uint32_t *gen_dev)
+{
+    return it.slot < 0 ? it.gen : __hip_atomic_load(gen_dev + it.slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool slot_gen_ok(const WorkItem &it, uint32_t g, uint32_t *status)
+{
+    asm volatile("" : "+v"(g));     // the compare stays here, after the work: the load's wait is not hoisted
+    if (g == it.gen)
+        return true;
+    if (threadIdx.x == 0)
+        atomicOr(status, STATUS_STALE);
+    return false;
+}
+
 // Generation check done by every tile before it reads a slot: true if the
 // slot denotes the version the host scheduled.  A mismatch raises the stale
 // bit (vector atomic) and the tile must write nothing.

@@ -73,22 +73,6 @@ __device__ __forceinline__ StreamTile stream_tile(const ExpertLaunch &L, int per
     return st;
 }
 
-// Generation word of the tile's slot (read early, compared late).
-__device__ __forceinline__ uint32_t slot_gen_now(const WorkItem &it, const uint32_t *gen_dev)
-{
-    return it.slot < 0 ? it.gen : __hip_atomic_load(gen_dev + it.slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ bool slot_gen_ok(const WorkItem &it, uint32_t g, uint32_t *status)
-{
-    asm volatile("" : "+v"(g));     // the compare stays here, after the work: the load's wait is not hoisted
-    if (g == it.gen)
-        return true;
-    if (threadIdx.x == 0)
-        atomicOr(status, STATUS_STALE);
-    return false;
-}
-
 // Weight slabs.  A wavefront's 16 weight rows reach registers in whole
 // 128-byte lines: one 16-byte load per lane covers 8 rows x 128 bytes (lane l:
 // row l / 8, chunk l % 8), two loads cover a slab of 16 rows x 64 columns.

@@ -148,17 +148,28 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
     using Rows = WaveRows<16 * CH>;
     __shared__ __attribute__((aligned(16))) uint8_t wst[q4s::WAVES][2][16 * Rows::RS];
     __shared__ f32x4 red[3][2][64];
-    int t;
-    WorkItem it;
-    if (!q4_tile(L, L.I / q4s::ROWS, t, it) || it.nrows == 0 ||
-        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
-        return;
-    const int n = it.nrows, d = L.d, I = L.I, nblk = d / 32, nq = nblk / q4s::WAVES;
-    const bool sh = it.slot < 0;
+    const int d = L.d, I = L.I, nblk = d / 32, nq = nblk / q4s::WAVES;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int i0 = (t - it.tile0) * q4s::ROWS;
     const int r = lane & 15, g = lane >> 4;
     const int bq = wave * nq;                          // this wavefront's first block
+    // One token (a device-built decode list of T = 1): every row is token 0, so the token fragments of the
+    // first chunk are requested before the item is known, and the generation is compared after the work
+    // (before the stores), so the weights are requested as soon as the slot is known.
+    const bool one = L.direct.demand && L.direct.T == 1;
+    u32x4 xv[CH];
+    if (one) {
+#pragma unroll
+        for (int u = 0; u < CH; ++u)
+            xv[u] = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(L.x) + 8 * g + 32 * (bq + u));
+    }
+    int t;
+    WorkItem it;
+    if (!q4_tile(L, L.I / q4s::ROWS, t, it) || it.nrows == 0)   // nrows 0: unpublished expert, no work
+        return;
+    const uint32_t gnow = slot_gen_now(it, L.gen_dev);
+    const int n = it.nrows;
+    const bool sh = it.slot < 0;
+    const int i0 = (t - it.tile0) * q4s::ROWS;
     const uint8_t *base = sh ? L.shared_w : L.wbase + uint64_t(it.slot) * L.wstride;
     const uint32_t mb = q4_matrix_bytes(I, d);
     const uint8_t *qrows[2];
@@ -170,18 +181,19 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
         sp[m] = reinterpret_cast<const uint16_t *>(mat + int64_t(I) * (d / 2)) + int64_t(i0 + r) * nblk + bq;
     }
     const int tr = min(r, n - 1);
-    const int64_t xrow = sh ? int64_t(it.row0 + tr) : int64_t(L.perm[it.row0 + tr]);
+    const int64_t xrow = one ? 0 : sh ? int64_t(it.row0 + tr) : int64_t(L.perm[it.row0 + tr]);
     const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + 8 * g + 32 * bq;
     Rows wr[2];
-    u32x4 xv[CH];
     uint32_t sc[2][CH / 2];
     auto issue = [&](int c0) {
 #pragma unroll
         for (int m = 0; m < 2; ++m)
             wr[m].load(qrows[m] + 16 * c0, d / 2, lane);
+        if (!(one && c0 == 0)) {
 #pragma unroll
-        for (int u = 0; u < CH; ++u)
-            xv[u] = *reinterpret_cast<const u32x4 *>(xp + 32 * (c0 + u));
+            for (int u = 0; u < CH; ++u)
+                xv[u] = *reinterpret_cast<const u32x4 *>(xp + 32 * (c0 + u));
+        }
 #pragma unroll
         for (int m = 0; m < 2; ++m)
             load_scales<CH>(sc[m], sp[m] + c0);
@@ -213,7 +225,7 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_q4_kernel(ExpertLaunch L
         red[wave - 1][1][lane] = au;
     }
     __syncthreads();
-    if (wave != 0)
+    if (wave != 0 || !slot_gen_ok(it, gnow, L.status))
         return;
     uint16_t *act = reinterpret_cast<uint16_t *>(sh ? L.act_s : L.act) + int64_t(it.row0) * I + i0 + r;
 #pragma unroll
@@ -238,9 +250,11 @@ __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
     __shared__ __attribute__((aligned(16))) uint8_t wst[q4s::WAVES][16 * Rows::RS];
     int t;
     WorkItem it;
-    if (!q4_tile(L, L.d / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0 ||
-        !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
+    if (!q4_tile(L, L.d / (q4s::WAVES * q4s::ROWS), t, it) || it.nrows == 0)   // nrows 0: unpublished expert
         return;
+    // the generation is read here and compared before the stores, and the row weights are read with the
+    // first weights, so nothing waits between the item lookup and the weight loads
+    const uint32_t gnow = slot_gen_now(it, L.gen_dev);
     const int n = it.nrows, d = L.d, I = L.I, nblk = I / 32;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -256,6 +270,10 @@ __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
     u32x4 av[CH];
     uint32_t sc[CH / 2];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float rw[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        rw[k] = (sh || 4 * g + k >= n) ? 1.0f : L.row_weight[it.row0 + 4 * g + k];
     for (int b0 = 0; b0 < nblk; b0 += CH) {
         wr.load(qrows + 16 * b0, I / 2, lane);
 #pragma unroll
@@ -274,15 +292,13 @@ __global__ void __launch_bounds__(256, 2) stream_down_q4_kernel(ExpertLaunch L)
                 acc[k] = fmaf(sv, part[k], acc[k]);
         }
     }
+    if (!slot_gen_ok(it, gnow, L.status))
+        return;
     uint16_t *y = static_cast<uint16_t *>(sh ? L.ys : L.y) + int64_t(it.row0) * d + c0 + r;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int tok = 4 * g + k;
-        if (tok < n) {
-            const float w = sh ? 1.0f : L.row_weight[it.row0 + tok];
-            y[int64_t(tok) * d] = f32_to_bf16(acc[k] * w);
-        }
-    }
+    for (int k = 0; k < 4; ++k)
+        if (4 * g + k < n)
+            y[int64_t(4 * g + k) * d] = f32_to_bf16(acc[k] * rw[k]);
 }
 
 hipError_t launch_gateup_q4_stream(const ExpertLaunch &L, hipStream_t s)
