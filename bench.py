@@ -40,6 +40,14 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f) for f in
 PREFILL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ring_gemm_prefill_bf16_traffic.md")
 PREFILL_KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f)
                           for f in ("gemm_ring.h", "tiles.hip", "common.h")]
+# and for the quantized prefill gate/up tiles (int4; the k4 / k6 mix)
+PREFILL_TRAFFIC_BY_FORMAT = {
+    "bf16": (PREFILL_TRAFFIC_FILE, PREFILL_KERNEL_SOURCES),
+    "q4b32": (os.path.join(ROOT, "profiles", "tile_q4_prefill_traffic.md"),
+              [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f) for f in ("experts_q4.hip", "common.h")]),
+    "kq": (os.path.join(ROOT, "profiles", "tile_kq_prefill_traffic.md"),
+           [os.path.join(ROOT, "paper_2608_23805_amd", "csrc", f) for f in ("experts_kq.hip", "common.h")]),
+}
 
 
 def log(*a):
@@ -222,8 +230,7 @@ def bench_prefill(args, cs, side, name="prefill_bf16"):
                          "achieved": round(achieved, 1),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-                         "traffic": None if s.wdtype != "bf16" else recorded_traffic(PREFILL_TRAFFIC_FILE,
-                                                                                     PREFILL_KERNEL_SOURCES),
+                         "traffic": recorded_traffic(*PREFILL_TRAFFIC_BY_FORMAT[s.wdtype]),
                          "flops_per_launch": flops_gu, "algorithmic_bytes_per_launch": bytes_gu,
                          "avg_launch_us": round(avg_gu * 1e3, 1),
                          "note": {"q4b32": "int4 weights unpacked to bf16 MFMA operands",
