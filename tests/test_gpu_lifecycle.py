@@ -272,6 +272,69 @@ def test_stale_generation_persistent_tiles():
     _stale_tile_cell(synth.layer_inputs(wl), capacity=16, persistent=True)
 
 
+QUANT_CELLS = {
+    "q4_T1": ("q4b32", 1), "q4_T300": ("q4b32", 300), "kq_T12": ("kq", 12), "kq_T300": ("kq", 300),
+}
+
+
+@pytest.mark.parametrize("cell", sorted(QUANT_CELLS))
+def test_stale_generation_quantized(cell):
+    """Stale generation on the quantized kernels: the stream kernels of a
+    device-built decode list (T = 1: the int4 kernels' token-0 path, whose
+    generation compare comes after the work; T = 12 for the 4.5-bit mix) and
+    the tile kernels of a device-built prefill list (T = 300).  The forward
+    returns MSI_E_STALE with the output untouched and the stale expert's act
+    and y rows unwritten while another expert's rows are overwritten; the
+    next forward refills and is exact."""
+    import torch
+    import paper_2608_23805_amd as msi
+    from _gpu_helpers import workspace_parts
+    fmt, T = QUANT_CELLS[cell]
+    wl = synth.Workload(f"cells_{cell}", 40 + sorted(QUANT_CELLS).index(cell),
+                        synth.LayerShape(300, 512, 24, 4, 256, fmt), prior="dirichlet", prior_param=0.5, tau=0.4)
+    li = synth.layer_inputs(wl)
+    s = wl.shape
+    log(f"cell stale_generation_quantized {cell}")
+    dl = device_layer(li)
+    plan = make_plan(li, capacity=s.E)
+    run_layer(plan, dl, T=T)                                   # fills
+    ref = run_layer(plan, dl, T=T)                             # no fill: the next forward takes a device-built list
+    counts, offsets = ref["counts"], ref["offsets"]
+    dem = [int(e) for e in np.nonzero(counts)[0]]
+    bad = max(dem, key=lambda e: (int(counts[e]), -e))
+    other = next(e for e in dem if e != bad)
+    slot = next(q for q in range(s.E) if plan.query(0, q).expert == bad)
+    plan.debug_set_device_gen(0, slot, plan.query(0, slot).generation + 1000)
+    x = dl.x[:T]
+    r = msi.Routing.alloc(T, s.K, s.E)
+    ws = plan.workspace(T)
+    cs = torch.cuda.current_stream()
+    plan.route(x, dl.wr, dl.bias, r, ws, cs)
+    torch.cuda.synchronize()
+    P = workspace_parts(T, s.E, s.K, s.d, s.I, s.wdtype)
+
+    def rows(part, e, width):
+        a = P[part] + int(offsets[e]) * width * 2
+        return ws[a:a + int(counts[e]) * width * 2]
+    for e in (bad, other):
+        rows("act", e, s.I).fill_(0x5A)
+        rows("y", e, s.d).fill_(0x5A)
+    canary = torch.full((T, s.d), 6.25, device="cuda")
+    st = plan.forward_status(0, x, r, dl.shared, canary, ws, cs, torch.cuda.Stream())
+    torch.cuda.synchronize()
+    log(f"  T={T} bad expert {bad} ({int(counts[bad])} rows), other {other} ({int(counts[other])} rows): status {st}")
+    assert st == msi.MSI_E_STALE, st
+    assert torch.all(canary == 6.25), "output written despite a stale slot"
+    assert torch.all(rows("act", bad, s.I) == 0x5A), "gate/up wrote rows of a stale slot"
+    assert torch.all(rows("y", bad, s.d) == 0x5A), "down wrote rows of a stale slot"
+    assert not torch.all(rows("act", other, s.I) == 0x5A) and not torch.all(rows("y", other, s.d) == 0x5A)
+    assert balanced(plan)["stale_detected"] == 1
+    again = run_layer(plan, dl, T=T)
+    assert again["out"].cpu().numpy().tobytes() == ref["out"].cpu().numpy().tobytes()
+    balanced(plan)
+    plan.close()
+
+
 def test_batch_limit_rejected():
     """A batch whose hidden states reach 2^31 bytes is rejected before any
     device work (the tile kernels address token rows with 32-bit offsets)."""
