@@ -46,4 +46,11 @@ def test_wide_rows(o, name):
         counts, offsets, perm, inv = o.permute(np.sort(res["idx"], axis=1), wl.shape.E)
         assert np.array_equal(res["counts"], counts) and np.array_equal(res["offsets"], offsets)
         assert np.array_equal(res["perm"], perm) and np.array_equal(res["inv"], inv)
+    # every expert is resident now: a forward that needs no fill, then one on the device work list
+    for T in (1, 16):
+        first = run_layer(plan, dl, T=T)
+        direct = run_layer(plan, dl, T=T)
+        assert direct["out"].cpu().numpy().tobytes() == first["out"].cpu().numpy().tobytes()
+        err, near, _ = oracle_compare(o, li, direct, list(range(T)), 1e-2)
+        log(f"{wl.name} T={T} device work list err={err:.3e} near_ties={len(near)}")
     plan.close()
