@@ -57,10 +57,10 @@ __device__ __forceinline__ bf16x8 unpack_u4_128(uint32_t q)
 
 // 8 k6 elements: low nibbles (element e at bits 4e of lo) and 2-bit high
 // parts (element e at bits 2e of hi) -> 8 exact bf16 values q - 32.  The
-// codes are assembled one per byte (even and odd elements in two words); the
-// binary32 with bits 0x4B000000 | q is 2^23 + q, so subtracting 2^23 + 32
-// leaves q - 32 exactly, and that integer (at most 6 significant bits) is exact
-// in the top half of its binary32.
+// codes are assembled one per byte (even and odd elements in two words), each
+// byte converted to binary32 by the byte-to-float instructions and 32
+// subtracted: q - 32 exactly, and that integer (at most 6 significant bits) is
+// exact in the top half of its binary32.
 __device__ __forceinline__ bf16x8 unpack_k6(uint32_t lo, uint32_t hi)
 {
     // spread the four 4-bit groups of hi (two elements each) to bytes 0..3
@@ -69,10 +69,12 @@ __device__ __forceinline__ bf16x8 unpack_k6(uint32_t lo, uint32_t hi)
     const uint32_t ev = (lo & 0x0F0F0F0Fu) | ((t & 0x03030303u) << 4);          // elements 0, 2, 4, 6
     const uint32_t od = ((lo >> 4) & 0x0F0F0F0Fu) | ((t & 0x0C0C0C0Cu) << 2);   // elements 1, 3, 5, 7
     u32x4 r;
+    float c32 = 32.0f;
+    asm("" : "+v"(c32));        // (kept a register: the byte conversions then stay v_cvt_f32_ubyte)
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-        const float fe = __uint_as_float(__builtin_amdgcn_perm(0x4B000000u, ev, 0x070C0C00u | h)) - 8388640.0f;
-        const float fo = __uint_as_float(__builtin_amdgcn_perm(0x4B000000u, od, 0x070C0C00u | h)) - 8388640.0f;
+        const float fe = float((ev >> (8 * h)) & 0xFFu) - c32;
+        const float fo = float((od >> (8 * h)) & 0xFFu) - c32;
         r[h] = __builtin_amdgcn_perm(__float_as_uint(fo), __float_as_uint(fe), 0x07060302u);
     }
     return __builtin_bit_cast(bf16x8, r);
