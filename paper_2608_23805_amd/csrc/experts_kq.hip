@@ -167,20 +167,27 @@ int tiles_down_kq_stream(int nrows, int d, int I)
 // fragments come straight from global memory (the few rows of a decode step
 // stay in cache; lanes past the item's rows repeat its last row and are not
 // stored); weights go through WaveRows.  Blocks go in chunks of CH (CH
-// divides 8, or is 16: whole super-blocks), each chunk's loads issued before
-// its first MFMA.
+// divides 8: at most one super-block), each chunk's loads issued before its
+// first MFMA.  The four lanes of a weight row share the decoding of its
+// sub-block coefficients: lane (r, g) decodes those of blocks g, g + 4 of
+// the chunk into the wavefront's LDS table, and every lane reads the block's
+// four coefficients back.  Chunks of 8 and the table keep the kernel at 80
+// registers, three workgroups per CU.
 template <int CH>
-__global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L)
+__global__ void __launch_bounds__(256, 3) stream_gateup_kq_kernel(ExpertLaunch L)
 {
     using Rows = WaveRows<16 * CH>;
     __shared__ __attribute__((aligned(16))) uint8_t wst[kqs::WAVES][2][16 * Rows::RS];
-    __shared__ f32x4 red[3][2][64];
+    // the coefficient table of the chunks, then the cross-wavefront sums (after a barrier)
+    __shared__ f32x4 cbuf[kqs::WAVES * CH * 16 > 3 * 2 * 64 ? kqs::WAVES * CH * 16 : 3 * 2 * 64];
+    f32x4 (*coef)[CH][16] = reinterpret_cast<f32x4 (*)[CH][16]>(cbuf);   // {a_g, b_g, a_u, b_u} of block u, row r
+    f32x4 (*red)[2][64] = reinterpret_cast<f32x4 (*)[2][64]>(cbuf);
     int t;
     WorkItem it;
     if (!kq_tile(L, L.I / kqs::ROWS, t, it) || it.nrows == 0 ||
         !slot_current(it, L.gen_dev, L.status))      // nrows 0: unpublished expert, no work
         return;
-    constexpr int HS = CH > 8 ? CH / 8 : 1;            // super-blocks per chunk
+    static_assert(CH <= 8, "a chunk stays within one super-block");
     const int n = it.nrows, d = L.d, I = L.I, nsb = d / 256, nq = d / 32 / kqs::WAVES;
     const bool sh = it.slot < 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -201,7 +208,7 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
     const int64_t xrow = sh ? int64_t(it.row0 + tr) : int64_t(L.perm[it.row0 + tr]);
     const uint16_t *xp = reinterpret_cast<const uint16_t *>(L.x) + xrow * d + 8 * g + 32 * bq;
     Rows wr[2];
-    u32x4 xv[CH], hd[2][HS];
+    u32x4 xv[CH], hd[2];                               // token fragments; the chunk's super-block headers
     auto issue = [&](int c0) {
 #pragma unroll
         for (int m = 0; m < 2; ++m)
@@ -211,9 +218,7 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
             xv[u] = *reinterpret_cast<const u32x4 *>(xp + 32 * (c0 + u));
 #pragma unroll
         for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int h = 0; h < HS; ++h)
-                hd[m][h] = hp[m][((bq + c0) >> 3) + h];
+            hd[m] = hp[m][(bq + c0) >> 3];
     };
     const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{BF16_ONE2, BF16_ONE2, BF16_ONE2, BF16_ONE2});
     f32x4 ag = {0.f, 0.f, 0.f, 0.f}, au = {0.f, 0.f, 0.f, 0.f};
@@ -223,18 +228,26 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
         wr[1].store(wst[wave][1], lane);
         const uint8_t *q0 = wst[wave][0] + r * Rows::RS + 4 * g, *q1 = wst[wave][1] + r * Rows::RS + 4 * g;
 #pragma unroll
+        for (int u0 = 0; u0 < CH; u0 += 4) {
+            const int u = u0 + g;
+            if (u < CH) {
+                const int j = (bq + c0 + u) & 7;       // sub-block within the super-block
+                float a_g, b_g, a_u, b_u;
+                k4_coef128(hd[0], j, a_g, b_g);
+                k4_coef128(hd[1], j, a_u, b_u);
+                coef[wave][u][r] = f32x4{a_g, b_g, a_u, b_u};
+            }
+        }
+#pragma unroll
         for (int u = 0; u < CH; ++u) {
-            const int j = (bq + c0 + u) & 7;           // sub-block within the super-block
-            const int h = CH > 8 ? u >> 3 : 0;
             const bf16x8 xb = as_bf16x8(xv[u]);
             const f32x4 pg = mfma16(xb, unpack_u4_128(*reinterpret_cast<const uint32_t *>(q0 + 16 * u)),
                                     f32x4{0.f, 0.f, 0.f, 0.f});
             const f32x4 pu = mfma16(xb, unpack_u4_128(*reinterpret_cast<const uint32_t *>(q1 + 16 * u)),
                                     f32x4{0.f, 0.f, 0.f, 0.f});
             const f32x4 sx = mfma16(xb, ones, f32x4{0.f, 0.f, 0.f, 0.f});    // the tokens' sums over the block
-            float a_g, b_g, a_u, b_u;
-            k4_coef128(hd[0][h], j, a_g, b_g);
-            k4_coef128(hd[1][h], j, a_u, b_u);
+            const f32x4 cf = coef[wave][u][r];
+            const float a_g = cf[0], b_g = cf[1], a_u = cf[2], b_u = cf[3];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 ag[i] = fmaf(a_g, pg[i], ag[i]);
@@ -245,6 +258,7 @@ __global__ void __launch_bounds__(256, 2) stream_gateup_kq_kernel(ExpertLaunch L
         }
     }
     // quarters of d added in wavefront order
+    __syncthreads();                                   // (the table's last reads are done)
     if (wave > 0) {
         red[wave - 1][0][lane] = ag;
         red[wave - 1][1][lane] = au;
@@ -358,11 +372,9 @@ hipError_t launch_gateup_kq_stream(const ExpertLaunch &L, hipStream_t s)
         return hipSuccess;
     if (L.d % 256 != 0)
         return hipErrorInvalidValue;
-    // chunk: 16, 8, 4 or 2 blocks, dividing a quarter of d's blocks (d / 128)
+    // chunk: 8, 4 or 2 blocks, dividing a quarter of d's blocks (d / 128)
     const int nq = L.d / 128;
-    if (nq % 16 == 0)
-        launch_k(stream_gateup_kq_kernel<16>, L.n_tiles, 256, 0, s, L);
-    else if (nq % 8 == 0)
+    if (nq % 8 == 0)
         launch_k(stream_gateup_kq_kernel<8>, L.n_tiles, 256, 0, s, L);
     else if (nq % 4 == 0)
         launch_k(stream_gateup_kq_kernel<4>, L.n_tiles, 256, 0, s, L);
